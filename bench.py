@@ -1,0 +1,243 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused RNN-T loss + gradient on one MI355X.
+
+One step = one rnnt_loss call with a gradient output (kernel 1 log-normaliser
+and gather, kernel 2 lattice sweep and arc posteriors, kernel 3 gradient) over
+one batch of the workload, inputs already resident in HBM.  Prints ONE JSON
+line: throughput in joint-logit elements/s (padded tensor B*T_max*(U_max+1)*V
+per step), the achieved HBM bandwidth of the dominant kernel against the
+MI355X peak, and the CPU oracle timed on a bounded sample.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload bpe]
+"""
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+ROWREC_BYTES = 16      # per-row record written by kernel 2 and read by kernel 3
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class HipEvents:
+    """hipEvent_t handles through the HIP runtime torch already loaded."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self, n):
+        arr = (ctypes.c_void_p * n)()
+        for i in range(n):
+            h = ctypes.c_void_p()
+            assert self.hip.hipEventCreate(ctypes.byref(h)) == 0
+            arr[i] = h
+        return arr
+
+    def elapsed_ms(self, a, b):
+        ms = ctypes.c_float()
+        assert self.hip.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(a), ctypes.c_void_p(b)) == 0
+        return ms.value
+
+    def destroy(self, arr):
+        for h in arr:
+            self.hip.hipEventDestroy(ctypes.c_void_p(h))
+
+
+def source_digest(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def profiled_traffic(workload):
+    """HBM bytes per gradient-kernel launch from the committed rocprofv3 counter
+    summary, if it was taken on the kernel sources as they are now; else None."""
+    path = os.path.join(PROFILE_DIR, "k3_grad_%s_traffic.json" % workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_digest") != source_digest(rec.get("sources", [])):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_oracle_worker(args):
+    import numpy as np
+
+    from oracle import rnnt_ref
+    T_b, U_b, V, sigma, seed, labels, variant = args
+    z = np.random.default_rng(seed).standard_normal((T_b, U_b + 1, V), dtype=np.float32) * np.float32(sigma)
+    t0 = time.perf_counter()
+    rnnt_ref.utterance_loss_grad(z.astype(np.float64), labels, 0, variant, need_grad=True)
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(w, tl, ul, labels, budget_s):
+    """Time the float64 oracle (loss + gradient) on utterances of this workload
+    (same lengths and labels, same logit distribution), spread over a process
+    pool.  Runs before the GPU is touched, so the workers are plain forks."""
+    import multiprocessing as mp
+
+    cores = max(1, min(16, len(os.sched_getaffinity(0))))
+    per_utt_elems = w.T_max * (w.U_max + 1) * w.V
+    jobs = [(int(tl[b]), int(ul[b]), w.V, w.sigma, w.seed * 1000 + b, labels[b, :int(ul[b])].copy(), w.variant)
+            for b in range(w.B)]
+    ctx = mp.get_context("fork")
+    with ctx.Pool(cores) as pool:
+        t0 = time.perf_counter()
+        pool.map(cpu_oracle_worker, jobs[:cores])  # one round, to size the sample
+        t_round = time.perf_counter() - t0
+        rounds = max(1, min(-(-len(jobs) // cores), int(budget_s / max(t_round, 1e-3))))
+        sample = jobs[:rounds * cores]
+        log("[bench] cpu oracle: one round of %d utterances took %.1f s; timing %d utterances"
+            % (min(cores, len(jobs)), t_round, len(sample)))
+        t0 = time.perf_counter()
+        pool.map(cpu_oracle_worker, sample)
+        dt = time.perf_counter() - t0
+    n = len(sample)
+    return {
+        "value": n * per_utt_elems / dt,
+        "unit": "joint-logit elements/s",
+        "cores": min(cores, n),
+        "kind": "oracle",
+        "sample": "%d of the %d utterances of the batch (their lengths and labels, N(0,%g) logits), float64 "
+                  "loss + gradient, %d worker processes, %.1f s; elements counted as padded rows x V like the "
+                  "GPU value" % (n, w.B, w.sigma, min(cores, n), dt),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="bpe", choices=["tiny", "char", "bpe", "wrnnt", "large"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work to time")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the loss has no multi-GPU path in this build "
+              "(utterances are independent; see the design notes on batch sharding). Use --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2303_10384_amd import binding
+    from paper_2303_10384_amd import workloads as W
+
+    w = W.WORKLOADS[args.workload]
+    log("[bench] workload", w.describe())
+    tl, ul, labels = W.make_lengths_labels(w)
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle (budget %.0f s)" % args.cpu_budget)
+        cpu = cpu_baseline(w, tl, ul, labels, args.cpu_budget)
+        log("[bench] cpu oracle: %.3g elements/s on %d cores" % (cpu["value"], cpu["cores"]))
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    binding.load_library()
+    logits = W.make_logits(w, dev)
+    labels_d = torch.from_numpy(labels).to(dev)
+    tl_d = torch.from_numpy(tl).to(dev)
+    ul_d = torch.from_numpy(ul).to(dev)
+    grad = torch.empty_like(logits)
+    loss = torch.empty(w.B, dtype=torch.float32, device=dev)
+    ws = torch.empty(binding.loss_workspace_bytes(w.B, w.T_max, w.U_max, w.V, binding.dtype_code(logits.dtype)),
+                     dtype=torch.uint8, device=dev)
+    call = lambda ev=None: binding.rnnt_loss(logits, labels_d, tl_d, ul_d, 0, w.variant, True, ws, grad,  # noqa: E731
+                                             loss, ev)
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    log("[bench] warmup done")
+
+    ev = HipEvents()
+    events = [ev.create(4) for _ in range(args.steps)]
+    torch.cuda.synchronize()  # barrier: one process, one GPU
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        call(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    k_ms = [[ev.elapsed_ms(e[i], e[i + 1]) for i in range(3)] for e in events]
+    total_ms = ev.elapsed_ms(events[0][0], events[-1][3])
+    for e in events:
+        ev.destroy(e)
+    ms_per_step = total_ms / args.steps
+    k1_ms, k2_ms, k3_ms = (float(np.mean([r[i] for r in k_ms])) for i in range(3))
+    log("[bench] per step %.4f ms (wall %.4f ms): k1 %.4f  k2 %.4f  k3 %.4f ms"
+        % (ms_per_step, wall * 1e3 / args.steps, k1_ms, k2_ms, k3_ms))
+
+    s = logits.element_size()
+    V = w.V
+    r_valid = int(np.sum(tl.astype(np.int64) * (ul.astype(np.int64) + 1)))
+    r_total = w.B * w.T_max * (w.U_max + 1)
+    elems = r_total * V
+    k1_bytes = r_valid * V * s
+    k3_bytes = r_valid * V * s + r_total * V * s + r_total * ROWREC_BYTES
+    step_bytes = 2 * r_valid * V * s + r_total * V * s
+    k3_gbs = k3_bytes / (k3_ms * 1e-3) / 1e9
+    traffic = profiled_traffic(args.workload)
+    roofline = {
+        "bound": "hbm",
+        "kernel": "k3_grad (fused gradient)",
+        "achieved": round(k3_gbs, 1),
+        "peak": PEAK_HBM_GBS,
+        "unit": "GB/s",
+        "frac": round(k3_gbs / PEAK_HBM_GBS, 4),
+        "traffic": traffic,
+        "bytes_per_launch": k3_bytes,
+        "launch_ms": round(k3_ms, 5),
+    }
+    result = {
+        "metric": "joint-logit elements/sec (loss+grad fwd/bwd) and achieved HBM GB/s vs peak",
+        "value": elems / (ms_per_step * 1e-3),
+        "unit": "joint-logit elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {"f32": "f32", "bf16": "bf16", "f16": "f16"}[w.dtype],
+        "data": "synthetic",
+        "config": {
+            "workload": w.describe(),
+            "B": w.B, "T_max": w.T_max, "U_max": w.U_max, "V": V, "variant": w.variant,
+            "valid_rows": r_valid, "padded_rows": r_total,
+            "lattice_scores": "f64", "softmax": "f32",
+        },
+        "hbm_gbs_step": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "hbm_frac_step": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "kernel_ms": {"k1_populate": round(k1_ms, 5), "k2_lattice": round(k2_ms, 5), "k3_grad": round(k3_ms, 5)},
+        "kernel_gbs": {"k1_populate": round(k1_bytes / (k1_ms * 1e-3) / 1e9, 1), "k3_grad": round(k3_gbs, 1)},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,188 @@
+/*
+ * rnnt_mi355x.h -- RNN-Transducer and W-Transducer loss and gradient over the
+ * T x (U+1) alignment grid, for AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Powerful and Extensible WFST Framework for RNN-Transducer Losses"
+ * (Laptev, Bataev, Gitman, Ginsburg, ICASSP 2023).
+ *   - Eq. 1: the loss of an utterance is the negative forward score of its
+ *     training lattice, -ln P(Y | X), summed over every alignment.
+ *   - Fig. 1 and Section 2.3 (Grid-Transducer): the lattice is a grid of nodes
+ *     (t, u), 0 <= t < T, 0 <= u <= U.  A blank arc leaves (t, u) for (t+1, u)
+ *     when t < T-1; a label arc carrying unit y_{u+1} leaves (t, u) for
+ *     (t, u+1) when u < U; the closing blank leaves (T-1, U) for the final
+ *     state.  Arc weights are selected from the log-softmax of the joint
+ *     logits row (t, u) (Populate, Section 2.2).
+ *   - Section 3.2 and Fig. 4 (W-Transducer, "force-final"): additional
+ *     probability-one arcs from (0, 0) to every (t, 0), t >= 1, and from every
+ *     (t, U), t <= T-2, to (T-1, U); the closing blank is still required.
+ *   - Section 4.3 ("allow-ignore"): those final arcs go to the final state.
+ *
+ * Conventions shared by every entry point
+ *   - All pointers are DEVICE pointers unless a comment says otherwise, and
+ *     belong to the caller.  The library keeps no state between calls and
+ *     never synchronises the stream: work is queued on `stream` and the call
+ *     returns RNNT_OK before the results exist.
+ *   - logits / grad are dense row-major (B, T_max, U_max+1, V), V innermost,
+ *     16-byte aligned.  Element offsets are 64-bit (more than 2^31 elements
+ *     are fine).
+ *   - labels is dense (B, U_max) int32; row b is read for u < label_lens[b].
+ *     logit_lens and label_lens are (B) int32.
+ *   - Errors that the host can see (NULL pointer, bad shape, blank outside
+ *     [0, V), unknown dtype or variant, workspace too small, misalignment)
+ *     return a status and launch nothing.  Data errors that only the device
+ *     can see (T_b outside [1, T_max], U_b outside [0, U_max], a label equal
+ *     to blank or outside [0, V)) give loss NaN for that utterance and a zero
+ *     gradient for all its rows; other utterances are unaffected.
+ *   - Logits outside an utterance's valid rows (t >= T_b or u > U_b) are
+ *     never used, so they may hold anything, NaN included.
+ */
+#ifndef RNNT_MI355X_H
+#define RNNT_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RNNT_OK = 0,
+  RNNT_ERR_NULL_PTR = 1,     /* a required pointer is NULL                       */
+  RNNT_ERR_BAD_SHAPE = 2,    /* B < 1, T_max < 1, U_max < 0, V < 2, or too large */
+  RNNT_ERR_BAD_BLANK = 3,    /* blank outside [0, V)                             */
+  RNNT_ERR_BAD_DTYPE = 4,    /* unknown rnnt_dtype_t                             */
+  RNNT_ERR_BAD_VARIANT = 5,  /* unknown rnnt_variant_t                           */
+  RNNT_ERR_WORKSPACE = 6,    /* workspace given but smaller than required        */
+  RNNT_ERR_ALIGNMENT = 7,    /* logits or grad not 16-byte aligned               */
+  RNNT_ERR_HIP = 8,          /* a HIP runtime call failed (launch, allocation)   */
+  RNNT_ERR_UNSUPPORTED = 9   /* shape outside what this build handles (U_max+1 > 1024) */
+} rnnt_status_t;
+
+typedef enum {
+  RNNT_VARIANT_RNNT = 0,               /* Fig. 1, Section 2.3                      */
+  RNNT_VARIANT_WRNNT = 1,              /* W-Transducer force-final, Section 3.2     */
+  RNNT_VARIANT_WRNNT_ALLOW_IGNORE = 2  /* final wild-card arcs to the final state,  */
+                                       /* Section 4.3                               */
+} rnnt_variant_t;
+
+typedef enum {
+  RNNT_DTYPE_F32 = 0,   /* IEEE binary32 logits and gradient                       */
+  RNNT_DTYPE_BF16 = 1,  /* bfloat16 logits and gradient, fp32 arithmetic inside    */
+  RNNT_DTYPE_F16 = 2    /* IEEE binary16 logits and gradient, fp32 arithmetic      */
+                        /* inside (the half-precision lattice of Section 4.2)      */
+} rnnt_dtype_t;
+
+/* Padded problem shape: logits are (B, T_max, U_max+1, V) of `dtype`. */
+typedef struct {
+  int32_t B;
+  int32_t T_max;
+  int32_t U_max;
+  int32_t V;
+  rnnt_dtype_t dtype;
+} rnnt_shape_t;
+
+/* Bytes of device workspace that rnnt_loss needs for `shape` (0 if the shape
+ * is invalid).  Host-only; touches no device. */
+size_t rnnt_loss_workspace_bytes(rnnt_shape_t shape);
+
+/*
+ * Per-utterance loss -ln P(Y_b | X_b) (Eq. 1) and, if grad_out != NULL, the
+ * gradient of sum_b loss_b with respect to the logits.
+ *
+ *   logits      (B, T_max, U_max+1, V) of shape.dtype; only rows t < T_b,
+ *               u <= U_b are read.
+ *   labels      (B, U_max) int32 units y_1..y_{U_b} per row.
+ *   logit_lens  (B) int32 T_b;  label_lens (B) int32 U_b.
+ *   blank       index of the blank symbol in [0, V).
+ *   variant     rnnt_variant_t.
+ *   loss_out    (B) float32: loss_b, no reduction (NaN for bad data).
+ *   grad_out    NULL (loss only) or (B, T_max, U_max+1, V) of shape.dtype:
+ *               every element is written; rows outside t < T_b, u <= U_b and
+ *               all rows of a bad utterance are exactly 0.  The gradient of
+ *               row (t, u) is softmax * (g_blank + g_label) - g_blank at
+ *               v = blank - g_label at v = y_{u+1}, where g_* are the arc
+ *               posteriors; wild-card arcs carry no parameter.
+ *   workspace   device buffer of at least rnnt_loss_workspace_bytes(shape)
+ *               bytes, 256-byte aligned, or NULL: the library then takes and
+ *               releases one with hipMallocAsync / hipFreeAsync on `stream`.
+ *               Its contents need no initialisation and are not preserved.
+ *   stream      HIP stream the work is ordered on.
+ * Calls that overlap in time must not share a workspace.
+ */
+rnnt_status_t rnnt_loss(const void* logits, rnnt_shape_t shape, const int32_t* labels,
+                        const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
+                        rnnt_variant_t variant, float* loss_out, void* grad_out, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * rnnt_loss that also records timing events on `stream`: events[0] before the
+ * first kernel, events[1] after kernel 1 (log-normaliser and gather),
+ * events[2] after kernel 2 (lattice scores and arc posteriors), events[3]
+ * after kernel 3 (gradient; recorded right after events[2] when grad_out is
+ * NULL).  `events` is a HOST array of 4 events created by the caller (for
+ * example with hipEventCreate); NULL behaves exactly like rnnt_loss.  Used to
+ * time each kernel in place (hipEventElapsedTime between consecutive events).
+ */
+rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int32_t* labels,
+                              const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
+                              rnnt_variant_t variant, float* loss_out, void* grad_out, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream, hipEvent_t* events);
+
+/*
+ * Populate step alone (Section 2.2 Populate; Fig. 1 arc weights): for every
+ * valid row (t < T_b, u <= U_b) of every good utterance
+ *   lse[b,t,u]       = ln sum_v exp(logits[b,t,u,v])
+ *   lp_blank[b,t,u]  = logits[b,t,u,blank] - lse
+ *   lp_label[b,t,u]  = logits[b,t,u,y_{u+1}] - lse for u < U_b, -inf at u = U_b
+ * as dense (B, T_max, U_max+1) float64 arrays.  Other entries are not written.
+ * Label values are not validated here beyond the bounds needed to read safely
+ * (an out-of-range label gives NaN in lp_label).
+ */
+rnnt_status_t rnnt_log_softmax_gather(const void* logits, rnnt_shape_t shape, const int32_t* labels,
+                                      const int32_t* logit_lens, const int32_t* label_lens,
+                                      int32_t blank, double* lse_out, double* lp_blank_out,
+                                      double* lp_label_out, hipStream_t stream);
+
+/*
+ * Forward and backward scores on given lattice weights (Eq. 1's Fwd and its
+ * backward counterpart), with no softmax: the lattice of Fig. 1 / Fig. 4 is
+ * populated directly from
+ *   lp_blank, lp_label  dense (B, T_max, U_max+1) float64 arc weights; entries
+ *                       outside t < T_b, u <= U_b (and lp_label at u = U_b)
+ *                       are never read.
+ * Outputs (dense (B, T_max, U_max+1) float64 unless noted; any may be NULL):
+ *   alpha_out           forward score of each node, -inf never written for
+ *                       nodes outside the utterance (those entries untouched)
+ *   beta_out            backward score of each node
+ *   loss_out            (B) float64: -(forward score of the final state)
+ *   loss_bwd_out        (B) float64: -beta(0, 0), computed by the backward sweep
+ *   occ_blank_out       posterior of the blank arc leaving each node (0 where
+ *                       absent)
+ *   occ_label_out       posterior of the label arc leaving each node
+ * label_lens/logit_lens as in rnnt_loss; shape.V and shape.dtype are ignored
+ * (pass V >= 2).  A bad utterance (lengths out of range) gets NaN losses and
+ * no other output.  Needs a workspace of rnnt_lattice_workspace_bytes(shape)
+ * bytes or NULL (then allocated stream-ordered).
+ */
+size_t rnnt_lattice_workspace_bytes(rnnt_shape_t shape);
+rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label, rnnt_shape_t shape,
+                                  const int32_t* logit_lens, const int32_t* label_lens,
+                                  rnnt_variant_t variant, double* alpha_out, double* beta_out,
+                                  double* loss_out, double* loss_bwd_out, double* occ_blank_out,
+                                  double* occ_label_out, void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream);
+
+/* Static description of a status code (never NULL). */
+const char* rnnt_status_string(rnnt_status_t status);
+
+/* Library version string, e.g. "rnnt_mi355x 0.1.0 gfx950". */
+const char* rnnt_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RNNT_MI355X_H */

@@ -1,0 +1,206 @@
+"""ctypes binding of librnnt_mi355x.so (argument marshalling only).
+
+Every step of the loss runs in the HIP library; torch is used for device
+memory and the current stream.  There is no CPU fallback: if the library is
+missing or the tensors are not on a GPU, the calls raise.
+"""
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "librnnt_mi355x.so")
+
+RNNT_OK = 0
+STATUS_NAMES = {
+    0: "RNNT_OK", 1: "RNNT_ERR_NULL_PTR", 2: "RNNT_ERR_BAD_SHAPE", 3: "RNNT_ERR_BAD_BLANK",
+    4: "RNNT_ERR_BAD_DTYPE", 5: "RNNT_ERR_BAD_VARIANT", 6: "RNNT_ERR_WORKSPACE", 7: "RNNT_ERR_ALIGNMENT",
+    8: "RNNT_ERR_HIP", 9: "RNNT_ERR_UNSUPPORTED",
+}
+VARIANTS = {"rnnt": 0, "wrnnt": 1, "wrnnt_allow_ignore": 2}
+DTYPE_F32, DTYPE_BF16, DTYPE_F16 = 0, 1, 2
+
+# every symbol declared in include/rnnt_mi355x.h
+EXPORTED = ("rnnt_loss_workspace_bytes", "rnnt_loss", "rnnt_loss_timed", "rnnt_log_softmax_gather", "rnnt_lattice_workspace_bytes",
+            "rnnt_lattice_scores", "rnnt_status_string", "rnnt_version")
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("T_max", ctypes.c_int32), ("U_max", ctypes.c_int32),
+                ("V", ctypes.c_int32), ("dtype", ctypes.c_int)]
+
+
+class RNNTError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__("%s failed: %s (%s)" % (where, STATUS_NAMES.get(status, status), status_string(status)))
+
+
+_lib = None
+
+
+def load_library():
+    """Load the in-tree library once; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("librnnt_mi355x.so is not built (run __graft_entry__.build() or "
+                           "python -m paper_2303_10384_amd.build)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    lib.rnnt_loss_workspace_bytes.argtypes = [Shape]
+    lib.rnnt_loss_workspace_bytes.restype = sz
+    lib.rnnt_lattice_workspace_bytes.argtypes = [Shape]
+    lib.rnnt_lattice_workspace_bytes.restype = sz
+    lib.rnnt_loss.argtypes = [vp, Shape, vp, vp, vp, i32, ctypes.c_int, vp, vp, vp, sz, vp]
+    lib.rnnt_loss.restype = ctypes.c_int
+    lib.rnnt_loss_timed.argtypes = [vp, Shape, vp, vp, vp, i32, ctypes.c_int, vp, vp, vp, sz, vp, vp]
+    lib.rnnt_loss_timed.restype = ctypes.c_int
+    lib.rnnt_log_softmax_gather.argtypes = [vp, Shape, vp, vp, vp, i32, vp, vp, vp, vp]
+    lib.rnnt_log_softmax_gather.restype = ctypes.c_int
+    lib.rnnt_lattice_scores.argtypes = [vp, vp, Shape, vp, vp, ctypes.c_int, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.rnnt_lattice_scores.restype = ctypes.c_int
+    lib.rnnt_status_string.argtypes = [ctypes.c_int]
+    lib.rnnt_status_string.restype = ctypes.c_char_p
+    lib.rnnt_version.argtypes = []
+    lib.rnnt_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def status_string(status):
+    return load_library().rnnt_status_string(int(status)).decode()
+
+
+def version():
+    return load_library().rnnt_version().decode()
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def dtype_code(dtype):
+    torch = _torch()
+    codes = {torch.float32: DTYPE_F32, torch.bfloat16: DTYPE_BF16, torch.float16: DTYPE_F16}
+    if dtype not in codes:
+        raise TypeError("logits must be float32, bfloat16 or float16, got %s" % dtype)
+    return codes[dtype]
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _check_gpu(name, t, dtype=None):
+    if not t.is_cuda:
+        raise ValueError("%s must be a GPU tensor (no CPU path exists)" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+
+
+def _stream_handle(device):
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def shape_of(logits):
+    B, T, U1, V = logits.shape
+    return Shape(B, T, U1 - 1, V, dtype_code(logits.dtype))
+
+
+def loss_workspace_bytes(B, T_max, U_max, V, dtype_code_=DTYPE_F32):
+    return load_library().rnnt_loss_workspace_bytes(Shape(B, T_max, U_max, V, dtype_code_))
+
+
+def rnnt_loss(logits, labels, logit_lens, label_lens, blank=0, variant="rnnt", need_grad=True,
+              workspace=None, grad_out=None, loss_out=None, events=None):
+    """Per-utterance loss (float32, shape (B,)) and gradient (logits' shape and dtype, or None).
+
+    logits (B, T_max, U_max+1, V) float32/bfloat16/float16 on the GPU; labels (B, U_max) int32;
+    logit_lens, label_lens (B,) int32.  workspace: optional uint8 GPU tensor of at least
+    loss_workspace_bytes(...) bytes; grad_out / loss_out: optional preallocated outputs;
+    events: optional ctypes array of 4 hipEvent_t recorded around the three kernels.
+    """
+    torch = _torch()
+    lib = load_library()
+    _check_gpu("logits", logits)
+    _check_gpu("labels", labels, torch.int32)
+    _check_gpu("logit_lens", logit_lens, torch.int32)
+    _check_gpu("label_lens", label_lens, torch.int32)
+    if logits.dim() != 4:
+        raise ValueError("logits must be (B, T_max, U_max+1, V)")
+    shape = shape_of(logits)
+    if labels.shape != (shape.B, shape.U_max) or logit_lens.shape != (shape.B,) or label_lens.shape != (shape.B,):
+        raise ValueError("labels must be (B, U_max) and the length vectors (B,)")
+    if variant not in VARIANTS:
+        raise ValueError("variant must be one of %s" % sorted(VARIANTS))
+    dev = logits.device
+    loss = loss_out if loss_out is not None else torch.empty(shape.B, dtype=torch.float32, device=dev)
+    _check_gpu("loss_out", loss, torch.float32)
+    grad = None
+    if need_grad:
+        grad = grad_out if grad_out is not None else torch.empty_like(logits)
+        _check_gpu("grad_out", grad, logits.dtype)
+        if grad.shape != logits.shape:
+            raise ValueError("grad_out must have the logits' shape")
+    ws_ptr, ws_bytes = ctypes.c_void_p(0), 0
+    if workspace is not None:
+        _check_gpu("workspace", workspace)
+        ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
+    if events is None:
+        st = lib.rnnt_loss(_ptr(logits), shape, _ptr(labels), _ptr(logit_lens), _ptr(label_lens), int(blank),
+                           VARIANTS[variant], _ptr(loss), _ptr(grad), ws_ptr, ws_bytes, _stream_handle(dev))
+    else:  # host array of 4 hipEvent_t handles
+        st = lib.rnnt_loss_timed(_ptr(logits), shape, _ptr(labels), _ptr(logit_lens), _ptr(label_lens),
+                                 int(blank), VARIANTS[variant], _ptr(loss), _ptr(grad), ws_ptr, ws_bytes,
+                                 _stream_handle(dev), events)
+    if st != RNNT_OK:
+        raise RNNTError(st, "rnnt_loss")
+    return loss, grad
+
+
+def log_softmax_gather(logits, labels, logit_lens, label_lens, blank=0):
+    """(lse, lp_blank, lp_label) float64 (B, T_max, U_max+1); entries outside the valid rows are NaN."""
+    torch = _torch()
+    lib = load_library()
+    _check_gpu("logits", logits)
+    shape = shape_of(logits)
+    dev = logits.device
+    outs = [torch.full((shape.B, shape.T_max, shape.U_max + 1), float("nan"), dtype=torch.float64, device=dev)
+            for _ in range(3)]
+    st = lib.rnnt_log_softmax_gather(_ptr(logits), shape, _ptr(labels), _ptr(logit_lens), _ptr(label_lens),
+                                     int(blank), _ptr(outs[0]), _ptr(outs[1]), _ptr(outs[2]), _stream_handle(dev))
+    if st != RNNT_OK:
+        raise RNNTError(st, "rnnt_log_softmax_gather")
+    return tuple(outs)
+
+
+def lattice_scores(lp_blank, lp_label, logit_lens, label_lens, variant="rnnt"):
+    """GPU forward/backward on given float64 lattice weights (B, T_max, U_max+1).
+
+    Returns dict with alpha, beta, occ_blank, occ_label (NaN outside the valid
+    nodes), loss and loss_bwd (B,) float64.
+    """
+    torch = _torch()
+    lib = load_library()
+    for n, t in (("lp_blank", lp_blank), ("lp_label", lp_label)):
+        _check_gpu(n, t, torch.float64)
+    B, T, U1 = lp_blank.shape
+    shape = Shape(B, T, U1 - 1, 2, DTYPE_F32)
+    dev = lp_blank.device
+    nan = float("nan")
+    out = {k: torch.full((B, T, U1), nan, dtype=torch.float64, device=dev)
+           for k in ("alpha", "beta", "occ_blank", "occ_label")}
+    out["loss"] = torch.full((B,), nan, dtype=torch.float64, device=dev)
+    out["loss_bwd"] = torch.full((B,), nan, dtype=torch.float64, device=dev)
+    st = lib.rnnt_lattice_scores(_ptr(lp_blank), _ptr(lp_label), shape, _ptr(logit_lens), _ptr(label_lens),
+                                 VARIANTS[variant], _ptr(out["alpha"]), _ptr(out["beta"]), _ptr(out["loss"]),
+                                 _ptr(out["loss_bwd"]), _ptr(out["occ_blank"]), _ptr(out["occ_label"]),
+                                 ctypes.c_void_p(0), 0, _stream_handle(dev))
+    if st != RNNT_OK:
+        raise RNNTError(st, "rnnt_lattice_scores")
+    return out

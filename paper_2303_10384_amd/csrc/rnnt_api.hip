@@ -1,0 +1,410 @@
+// C-ABI of the RNN-T / W-Transducer loss library (declarations and contract in
+// include/rnnt_mi355x.h).  Host side: argument checks that need no device,
+// workspace carve-up, kernel selection and launches on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+
+#include "rnnt_mi355x.h"
+#include "rnnt_device.h"
+#include "rnnt_k1_populate.h"
+#include "rnnt_k2_lattice.h"
+#include "rnnt_k3_grad.h"
+
+namespace rnnt {
+namespace {
+
+constexpr int kMaxUnits1 = 1024;  // U_max + 1 handled by one wavefront (16 units per lane)
+
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+
+bool dtype_known(int dt) { return dt == RNNT_DTYPE_F32 || dt == RNNT_DTYPE_BF16 || dt == RNNT_DTYPE_F16; }
+
+rnnt_status_t check_shape(const rnnt_shape_t& s) {
+  if (s.B < 1 || s.T_max < 1 || s.U_max < 0 || s.V < 2) return RNNT_ERR_BAD_SHAPE;
+  // keep every 32-bit block count and per-utterance row count in range
+  const int64_t rows_per_utt = static_cast<int64_t>(s.T_max) * (s.U_max + 1);
+  if (rows_per_utt > (int64_t{1} << 30)) return RNNT_ERR_BAD_SHAPE;
+  if (static_cast<int64_t>(s.B) * rows_per_utt > (int64_t{1} << 40)) return RNNT_ERR_BAD_SHAPE;
+  if (s.V > (1 << 30)) return RNNT_ERR_BAD_SHAPE;
+  if (!dtype_known(s.dtype)) return RNNT_ERR_BAD_DTYPE;
+  return RNNT_OK;
+}
+
+// Workspace of rnnt_loss, all pieces 256-byte aligned:
+//   rowinfo  (B*T_max*(U_max+1)) RowInfo
+//   lp       (B, T_max+U_max, U_max+1) double2 {lp_blank, lp_label}, indexed by diagonal
+//   alpha    (B, T_max+U_max, U_max+1) double, indexed by diagonal
+//   beta     same
+//   lnp      2*B double
+struct LossLayout {
+  size_t rowinfo, lp, alpha, beta, lnp, total;
+};
+
+LossLayout loss_layout(const rnnt_shape_t& s) {
+  const size_t rows = static_cast<size_t>(s.B) * s.T_max * (s.U_max + 1);
+  const size_t cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max) * (s.U_max + 1);
+  LossLayout L{};
+  size_t o = 0;
+  L.rowinfo = o;
+  o = align256(o + rows * sizeof(RowInfo));
+  L.lp = o;
+  o = align256(o + cells * 2 * sizeof(double));
+  L.alpha = o;
+  o = align256(o + cells * sizeof(double));
+  L.beta = o;
+  o = align256(o + cells * sizeof(double));
+  L.lnp = o;
+  o = align256(o + 2 * static_cast<size_t>(s.B) * sizeof(double));
+  L.total = o;
+  return L;
+}
+
+// Workspace of rnnt_lattice_scores: alpha, beta (diagonal-indexed) and lnp.
+struct LatticeLayout {
+  size_t alpha, beta, lnp, total;
+};
+
+LatticeLayout lattice_layout(const rnnt_shape_t& s) {
+  const size_t cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max) * (s.U_max + 1);
+  LatticeLayout L{};
+  size_t o = 0;
+  L.alpha = o;
+  o = align256(o + cells * sizeof(double));
+  L.beta = o;
+  o = align256(o + cells * sizeof(double));
+  L.lnp = o;
+  o = align256(o + 2 * static_cast<size_t>(s.B) * sizeof(double));
+  L.total = o;
+  return L;
+}
+
+// ---- kernel 1 ---------------------------------------------------------------
+
+template <typename T>
+int k1_group_lanes(int V) {
+  constexpr int EPC = ElemTraits<T>::kPerChunk;
+  const int max_chunks = (EPC - 1 + V + EPC - 1) / EPC;
+  int want = (max_chunks + 3) / 4;  // about four chunks per lane
+  int g = 8;
+  while (g < want && g < 64) g <<= 1;
+  return g;
+}
+
+template <typename T, int G>
+hipError_t launch_k1_g(PopulateParams p, hipStream_t stream) {
+  constexpr int groups = 256 / G;
+  p.rows_per_block = groups * 4;
+  p.n_ublk = (p.U_max + 1 + p.rows_per_block - 1) / p.rows_per_block;
+  const int64_t blocks = static_cast<int64_t>(p.B) * p.T_max * p.n_ublk;
+  if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL((k1_populate<T, G>), dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_k1(PopulateParams p, hipStream_t stream) {
+  switch (k1_group_lanes<T>(p.V)) {
+    case 8: return launch_k1_g<T, 8>(p, stream);
+    case 16: return launch_k1_g<T, 16>(p, stream);
+    case 32: return launch_k1_g<T, 32>(p, stream);
+    default: return launch_k1_g<T, 64>(p, stream);
+  }
+}
+
+hipError_t launch_k1_dtype(rnnt_dtype_t dt, const PopulateParams& p, hipStream_t stream) {
+  switch (dt) {
+    case RNNT_DTYPE_F32: return launch_k1<float>(p, stream);
+    case RNNT_DTYPE_BF16: return launch_k1<bf16_t>(p, stream);
+    default: return launch_k1<f16_t>(p, stream);
+  }
+}
+
+// ---- kernel 2 ---------------------------------------------------------------
+
+template <int K, int MODE, bool IL>
+hipError_t launch_k2_k(const LatticeParams& p, hipStream_t stream) {
+  constexpr int PF = (K >= 16) ? 1 : (32 / K);  // weights of PF diagonals in flight per lane
+  const int threads = (MODE == kLossOnly) ? 64 : 512;
+  hipLaunchKernelGGL((k2_lattice<K, PF, MODE, IL>), dim3(p.B), dim3(threads), 0, stream, p);
+  return hipGetLastError();
+}
+
+template <int MODE, bool IL>
+hipError_t launch_k2(const LatticeParams& p, hipStream_t stream) {
+  const int units1 = p.U_max + 1;
+  if (units1 <= 64) return launch_k2_k<1, MODE, IL>(p, stream);
+  if (units1 <= 128) return launch_k2_k<2, MODE, IL>(p, stream);
+  if (units1 <= 256) return launch_k2_k<4, MODE, IL>(p, stream);
+  if (units1 <= 512) return launch_k2_k<8, MODE, IL>(p, stream);
+  return launch_k2_k<16, MODE, IL>(p, stream);
+}
+
+// ---- kernel 3 ---------------------------------------------------------------
+
+template <typename T>
+hipError_t launch_k3(const GradParams& p, hipStream_t stream) {
+  constexpr int EPC = ElemTraits<T>::kPerChunk;
+  const int64_t chunks = (p.n_elem + EPC - 1) / EPC;
+  const int64_t blocks = (chunks + kGradTileChunks - 1) / kGradTileChunks;
+  if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+  if (p.V < EPC)
+    hipLaunchKernelGGL((k3_grad<T, true>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL((k3_grad<T, false>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_k3_dtype(rnnt_dtype_t dt, const GradParams& p, hipStream_t stream) {
+  switch (dt) {
+    case RNNT_DTYPE_F32: return launch_k3<float>(p, stream);
+    case RNNT_DTYPE_BF16: return launch_k3<bf16_t>(p, stream);
+    default: return launch_k3<f16_t>(p, stream);
+  }
+}
+
+bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
+
+// Stream-ordered scratch when the caller passes no workspace.
+struct Scratch {
+  void* ptr = nullptr;
+  hipStream_t stream = nullptr;
+  ~Scratch() {
+    if (ptr) (void)hipFreeAsync(ptr, stream);
+  }
+};
+
+}  // namespace
+}  // namespace rnnt
+
+using namespace rnnt;
+
+extern "C" {
+
+const char* rnnt_status_string(rnnt_status_t status) {
+  switch (status) {
+    case RNNT_OK: return "ok";
+    case RNNT_ERR_NULL_PTR: return "a required pointer is NULL";
+    case RNNT_ERR_BAD_SHAPE: return "bad shape (need B >= 1, T_max >= 1, U_max >= 0, V >= 2, sizes in range)";
+    case RNNT_ERR_BAD_BLANK: return "blank outside [0, V)";
+    case RNNT_ERR_BAD_DTYPE: return "unknown dtype";
+    case RNNT_ERR_BAD_VARIANT: return "unknown variant";
+    case RNNT_ERR_WORKSPACE: return "workspace smaller than required";
+    case RNNT_ERR_ALIGNMENT: return "logits / grad must be 16-byte aligned";
+    case RNNT_ERR_HIP: return "HIP runtime error";
+    case RNNT_ERR_UNSUPPORTED: return "unsupported shape (U_max + 1 > 1024)";
+  }
+  return "unknown status";
+}
+
+const char* rnnt_version(void) { return "rnnt_mi355x 0.1.0 gfx950"; }
+
+size_t rnnt_loss_workspace_bytes(rnnt_shape_t shape) {
+  if (check_shape(shape) != RNNT_OK) return 0;
+  return loss_layout(shape).total;
+}
+
+size_t rnnt_lattice_workspace_bytes(rnnt_shape_t shape) {
+  rnnt_shape_t s = shape;
+  s.dtype = RNNT_DTYPE_F32;
+  if (check_shape(s) != RNNT_OK) return 0;
+  return lattice_layout(s).total;
+}
+
+rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int32_t* labels,
+                              const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
+                              rnnt_variant_t variant, float* loss_out, void* grad_out, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream, hipEvent_t* events) {
+  rnnt_status_t st = check_shape(shape);
+  if (st != RNNT_OK) return st;
+  if (!logits || !logit_lens || !label_lens || !loss_out || (!labels && shape.U_max > 0))
+    return RNNT_ERR_NULL_PTR;
+  if (blank < 0 || blank >= shape.V) return RNNT_ERR_BAD_BLANK;
+  if (variant != RNNT_VARIANT_RNNT && variant != RNNT_VARIANT_WRNNT && variant != RNNT_VARIANT_WRNNT_ALLOW_IGNORE)
+    return RNNT_ERR_BAD_VARIANT;
+  if (!aligned16(logits) || (grad_out && !aligned16(grad_out))) return RNNT_ERR_ALIGNMENT;
+  if (shape.U_max + 1 > kMaxUnits1) return RNNT_ERR_UNSUPPORTED;
+  const LossLayout L = loss_layout(shape);
+  if (workspace && workspace_bytes < L.total) return RNNT_ERR_WORKSPACE;
+  if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u)) return RNNT_ERR_ALIGNMENT;
+
+  Scratch scratch;
+  char* ws = static_cast<char*>(workspace);
+  if (!ws) {
+    if (hipMallocAsync(&scratch.ptr, L.total, stream) != hipSuccess) return RNNT_ERR_HIP;
+    scratch.stream = stream;
+    ws = static_cast<char*>(scratch.ptr);
+  }
+  RowInfo* rowinfo = reinterpret_cast<RowInfo*>(ws + L.rowinfo);
+  double* lp = reinterpret_cast<double*>(ws + L.lp);
+  const int64_t U1 = shape.U_max + 1;
+  const int64_t n_rows = static_cast<int64_t>(shape.B) * shape.T_max * U1;
+  const int64_t n_elem = n_rows * shape.V;
+  const bool need_grad = grad_out != nullptr;
+
+  auto mark = [&](int i) { return events ? hipEventRecord(events[i], stream) : hipSuccess; };
+  if (mark(0) != hipSuccess) return RNNT_ERR_HIP;
+
+  // kernel 1: lse and arc weights; lp is stored by diagonal, interleaved
+  PopulateParams p1{};
+  p1.logits = logits;
+  p1.B = shape.B;
+  p1.T_max = shape.T_max;
+  p1.U_max = shape.U_max;
+  p1.V = shape.V;
+  p1.blank = blank;
+  p1.labels = labels;
+  p1.logit_lens = logit_lens;
+  p1.label_lens = label_lens;
+  p1.n_elem = n_elem;
+  p1.rowinfo = need_grad ? rowinfo : nullptr;
+  p1.lp_blank = lp;
+  p1.lp_label = lp + 1;
+  p1.sb = 2 * static_cast<int64_t>(shape.T_max + shape.U_max) * U1;
+  p1.st = 2 * U1;        // (t, u) -> diagonal (t+u), unit u: (t+u)*U1 + u
+  p1.su = 2 * (U1 + 1);
+  p1.lse_out = nullptr;
+  if (launch_k1_dtype(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (mark(1) != hipSuccess) return RNNT_ERR_HIP;
+
+  // kernel 2: forward / backward scores and arc posteriors
+  LatticeParams p2{};
+  p2.B = shape.B;
+  p2.T_max = shape.T_max;
+  p2.U_max = shape.U_max;
+  p2.V = shape.V;
+  p2.blank = blank;
+  p2.variant = static_cast<int32_t>(variant);
+  p2.labels = labels;
+  p2.logit_lens = logit_lens;
+  p2.label_lens = label_lens;
+  p2.lp_blank = lp;
+  p2.lp_label = lp + 1;
+  p2.sb = p1.sb;
+  p2.st = p1.st;
+  p2.su = p1.su;
+  p2.alpha = reinterpret_cast<double*>(ws + L.alpha);
+  p2.beta = reinterpret_cast<double*>(ws + L.beta);
+  p2.sab = static_cast<int64_t>(shape.T_max + shape.U_max) * U1;
+  p2.lnp_fwd = reinterpret_cast<double*>(ws + L.lnp);
+  p2.lnp_bwd = p2.lnp_fwd + shape.B;
+  p2.loss_f32 = loss_out;
+  p2.rowinfo = rowinfo;
+  hipError_t e = need_grad ? launch_k2<kRowRecords, true>(p2, stream) : launch_k2<kLossOnly, true>(p2, stream);
+  if (e != hipSuccess) return RNNT_ERR_HIP;
+  if (mark(2) != hipSuccess) return RNNT_ERR_HIP;
+
+  // kernel 3: gradient
+  if (need_grad) {
+    GradParams p3{};
+    p3.logits = logits;
+    p3.grad = grad_out;
+    p3.rowinfo = rowinfo;
+    p3.n_elem = n_elem;
+    p3.n_rows = n_rows;
+    p3.V = shape.V;
+    p3.blank = blank;
+    if (launch_k3_dtype(shape.dtype, p3, stream) != hipSuccess) return RNNT_ERR_HIP;
+  }
+  if (mark(3) != hipSuccess) return RNNT_ERR_HIP;
+  return RNNT_OK;
+}
+
+rnnt_status_t rnnt_loss(const void* logits, rnnt_shape_t shape, const int32_t* labels,
+                        const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
+                        rnnt_variant_t variant, float* loss_out, void* grad_out, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
+  return rnnt_loss_timed(logits, shape, labels, logit_lens, label_lens, blank, variant, loss_out, grad_out,
+                         workspace, workspace_bytes, stream, nullptr);
+}
+
+rnnt_status_t rnnt_log_softmax_gather(const void* logits, rnnt_shape_t shape, const int32_t* labels,
+                                      const int32_t* logit_lens, const int32_t* label_lens,
+                                      int32_t blank, double* lse_out, double* lp_blank_out,
+                                      double* lp_label_out, hipStream_t stream) {
+  rnnt_status_t st = check_shape(shape);
+  if (st != RNNT_OK) return st;
+  if (!logits || !logit_lens || !label_lens || !lp_blank_out || !lp_label_out || (!labels && shape.U_max > 0))
+    return RNNT_ERR_NULL_PTR;
+  if (blank < 0 || blank >= shape.V) return RNNT_ERR_BAD_BLANK;
+  if (!aligned16(logits)) return RNNT_ERR_ALIGNMENT;
+  const int64_t U1 = shape.U_max + 1;
+  PopulateParams p1{};
+  p1.logits = logits;
+  p1.B = shape.B;
+  p1.T_max = shape.T_max;
+  p1.U_max = shape.U_max;
+  p1.V = shape.V;
+  p1.blank = blank;
+  p1.labels = labels;
+  p1.logit_lens = logit_lens;
+  p1.label_lens = label_lens;
+  p1.n_elem = static_cast<int64_t>(shape.B) * shape.T_max * U1 * shape.V;
+  p1.rowinfo = nullptr;
+  p1.lp_blank = lp_blank_out;
+  p1.lp_label = lp_label_out;
+  p1.sb = static_cast<int64_t>(shape.T_max) * U1;
+  p1.st = U1;
+  p1.su = 1;
+  p1.lse_out = lse_out;
+  return launch_k1_dtype(shape.dtype, p1, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
+}
+
+rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label, rnnt_shape_t shape,
+                                  const int32_t* logit_lens, const int32_t* label_lens,
+                                  rnnt_variant_t variant, double* alpha_out, double* beta_out,
+                                  double* loss_out, double* loss_bwd_out, double* occ_blank_out,
+                                  double* occ_label_out, void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream) {
+  rnnt_shape_t s = shape;
+  s.dtype = RNNT_DTYPE_F32;
+  rnnt_status_t st = check_shape(s);
+  if (st != RNNT_OK) return st;
+  if (!lp_blank || !lp_label || !logit_lens || !label_lens) return RNNT_ERR_NULL_PTR;
+  if (variant != RNNT_VARIANT_RNNT && variant != RNNT_VARIANT_WRNNT && variant != RNNT_VARIANT_WRNNT_ALLOW_IGNORE)
+    return RNNT_ERR_BAD_VARIANT;
+  if (s.U_max + 1 > kMaxUnits1) return RNNT_ERR_UNSUPPORTED;
+  const LatticeLayout L = lattice_layout(s);
+  if (workspace && workspace_bytes < L.total) return RNNT_ERR_WORKSPACE;
+  if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u)) return RNNT_ERR_ALIGNMENT;
+  Scratch scratch;
+  char* ws = static_cast<char*>(workspace);
+  if (!ws) {
+    if (hipMallocAsync(&scratch.ptr, L.total, stream) != hipSuccess) return RNNT_ERR_HIP;
+    scratch.stream = stream;
+    ws = static_cast<char*>(scratch.ptr);
+  }
+  const int64_t U1 = s.U_max + 1;
+  LatticeParams p2{};
+  p2.B = s.B;
+  p2.T_max = s.T_max;
+  p2.U_max = s.U_max;
+  p2.V = s.V;
+  p2.blank = 0;
+  p2.variant = static_cast<int32_t>(variant);
+  p2.labels = nullptr;
+  p2.logit_lens = logit_lens;
+  p2.label_lens = label_lens;
+  p2.lp_blank = lp_blank;
+  p2.lp_label = lp_label;
+  p2.sb = static_cast<int64_t>(s.T_max) * U1;
+  p2.st = U1;
+  p2.su = 1;
+  p2.alpha = reinterpret_cast<double*>(ws + L.alpha);
+  p2.beta = reinterpret_cast<double*>(ws + L.beta);
+  p2.sab = static_cast<int64_t>(s.T_max + s.U_max) * U1;
+  p2.lnp_fwd = reinterpret_cast<double*>(ws + L.lnp);
+  p2.lnp_bwd = p2.lnp_fwd + s.B;
+  p2.loss_f32 = nullptr;
+  p2.alpha_out = alpha_out;
+  p2.beta_out = beta_out;
+  p2.occ_blank_out = occ_blank_out;
+  p2.occ_label_out = occ_label_out;
+  p2.loss_out = loss_out;
+  p2.loss_bwd_out = loss_bwd_out;
+  return launch_k2<kDenseOut, false>(p2, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
+}
+
+}  // extern "C"

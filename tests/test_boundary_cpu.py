@@ -1,0 +1,136 @@
+"""The C-ABI library without a GPU: it loads, exports every declared symbol,
+sizes its workspace as documented, and rejects bad arguments with the right
+status before touching the device (no compute call is made here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rnnt_mi355x.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2303_10384_amd import binding
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2303_10384_amd import build
+        build.build(verbose=False)
+    return binding.load_library()
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(rnnt_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_header_declares_the_documented_entry_points():
+    names = declared_functions()
+    assert names == sorted(["rnnt_loss_workspace_bytes", "rnnt_loss", "rnnt_loss_timed", "rnnt_log_softmax_gather",
+                            "rnnt_lattice_workspace_bytes", "rnnt_lattice_scores", "rnnt_status_string",
+                            "rnnt_version"])
+
+
+def test_every_declared_symbol_is_exported(lib):
+    from paper_2303_10384_amd import binding
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    assert sorted(binding.EXPORTED) == declared_functions()
+
+
+def test_status_strings_and_version(lib):
+    from paper_2303_10384_amd import binding
+    for code in range(10):
+        assert binding.status_string(code)
+    assert binding.status_string(0) == "ok"
+    assert "gfx950" in binding.version()
+
+
+def shape(B=2, T=5, U=3, V=7, dt=0):
+    from paper_2303_10384_amd.binding import Shape
+    return Shape(B, T, U, V, dt)
+
+
+def expected_workspace(B, T, U, V):
+    a = lambda x: (x + 255) // 256 * 256  # noqa: E731
+    rows = B * T * (U + 1)
+    cells = B * (T + U) * (U + 1)
+    o = a(rows * 16)
+    o = a(o + cells * 16)
+    o = a(o + cells * 8)
+    o = a(o + cells * 8)
+    return a(o + 2 * B * 8)
+
+
+@pytest.mark.parametrize("B,T,U,V", [(1, 1, 0, 2), (2, 20, 8, 16), (32, 250, 80, 1025), (64, 500, 150, 1025)])
+def test_workspace_size(lib, B, T, U, V):
+    assert lib.rnnt_loss_workspace_bytes(shape(B, T, U, V)) == expected_workspace(B, T, U, V)
+
+
+def test_workspace_size_of_bad_shape_is_zero(lib):
+    assert lib.rnnt_loss_workspace_bytes(shape(B=0)) == 0
+    assert lib.rnnt_loss_workspace_bytes(shape(V=1)) == 0
+    assert lib.rnnt_loss_workspace_bytes(shape(dt=7)) == 0
+
+
+FAKE = 1 << 20  # aligned, never dereferenced: every call below fails validation first
+
+
+def call_loss(lib, sh, logits=FAKE, labels=FAKE, tl=FAKE, ul=FAKE, blank=0, variant=0, loss=FAKE, grad=FAKE,
+              ws=0, ws_bytes=0):
+    vp = ctypes.c_void_p
+    return lib.rnnt_loss(vp(logits), sh, vp(labels), vp(tl), vp(ul), blank, variant, vp(loss), vp(grad), vp(ws),
+                         ws_bytes, vp(0))
+
+
+def test_rnnt_loss_host_errors(lib):
+    assert call_loss(lib, shape(B=0)) == 2
+    assert call_loss(lib, shape(T=0)) == 2
+    assert call_loss(lib, shape(U=-1)) == 2
+    assert call_loss(lib, shape(V=1)) == 2
+    assert call_loss(lib, shape(dt=3)) == 4
+    assert call_loss(lib, shape(), logits=0) == 1
+    assert call_loss(lib, shape(), labels=0) == 1
+    assert call_loss(lib, shape(), tl=0) == 1
+    assert call_loss(lib, shape(), ul=0) == 1
+    assert call_loss(lib, shape(), loss=0) == 1
+    assert call_loss(lib, shape(), blank=-1) == 3
+    assert call_loss(lib, shape(), blank=7) == 3
+    assert call_loss(lib, shape(), variant=3) == 5
+    assert call_loss(lib, shape(), logits=FAKE + 4) == 7
+    assert call_loss(lib, shape(), grad=FAKE + 8) == 7
+    assert call_loss(lib, shape(U=1024)) == 9
+    need = lib.rnnt_loss_workspace_bytes(shape())
+    assert call_loss(lib, shape(), ws=FAKE, ws_bytes=need - 1) == 6
+    assert call_loss(lib, shape(), ws=FAKE + 16, ws_bytes=need) == 7
+
+
+def test_other_entry_points_host_errors(lib):
+    vp = ctypes.c_void_p
+    st = lib.rnnt_log_softmax_gather(vp(FAKE), shape(), vp(FAKE), vp(FAKE), vp(FAKE), 9, vp(FAKE), vp(FAKE),
+                                     vp(FAKE), vp(0))
+    assert st == 3
+    st = lib.rnnt_log_softmax_gather(vp(FAKE), shape(), vp(FAKE), vp(FAKE), vp(FAKE), 0, vp(FAKE), vp(0),
+                                     vp(FAKE), vp(0))
+    assert st == 1
+    st = lib.rnnt_lattice_scores(vp(FAKE), vp(FAKE), shape(), vp(FAKE), vp(FAKE), 4, vp(0), vp(0), vp(0), vp(0),
+                                 vp(0), vp(0), vp(0), 0, vp(0))
+    assert st == 5
+    st = lib.rnnt_lattice_scores(vp(0), vp(FAKE), shape(), vp(FAKE), vp(FAKE), 0, vp(0), vp(0), vp(0), vp(0),
+                                 vp(0), vp(0), vp(0), 0, vp(0))
+    assert st == 1
+    need = lib.rnnt_lattice_workspace_bytes(shape())
+    st = lib.rnnt_lattice_scores(vp(FAKE), vp(FAKE), shape(), vp(FAKE), vp(FAKE), 0, vp(0), vp(0), vp(0), vp(0),
+                                 vp(0), vp(0), vp(FAKE), need - 1, vp(0))
+    assert st == 6
+
+
+def test_binding_refuses_cpu_tensors(lib):
+    import torch
+    from paper_2303_10384_amd import rnnt_loss
+    x = torch.zeros(1, 2, 2, 3)
+    with pytest.raises(ValueError, match="GPU"):
+        rnnt_loss(x, torch.zeros(1, 1, dtype=torch.int32), torch.ones(1, dtype=torch.int32),
+                  torch.ones(1, dtype=torch.int32))

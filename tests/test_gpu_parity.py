@@ -1,0 +1,320 @@
+"""GPU parity: the HIP path (through the C-ABI) against the float64 oracle.
+
+Tolerances (fp32 logits): per-utterance |L - L_ref| <= 1e-5 |L_ref| and every
+gradient element |g - g_ref| <= 1e-5.  bf16 / fp16 logits: |L - L_ref| <=
+2e-3 |L_ref| and |g - g_ref| <= 2e-3 |g_ref| + 1e-5, with g_ref computed from
+the same half-precision values upcast exactly (the output rounding alone is
+up to 2^-9 relative for bf16).  Padding rows must be exactly 0 and NaN logits
+in the padding must not leak.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from figures import allow_ignore_from_fig4, grid_weights, load_figure
+from oracle import rnnt_ref as R
+from paper_2303_10384_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+VARIANTS = ("rnnt", "wrnnt", "wrnnt_allow_ignore")
+
+
+@pytest.fixture(autouse=True)
+def announce(request):
+    sys.__stderr__.write("\n[gpu-test] %s\n" % request.node.nodeid)
+    sys.__stderr__.flush()
+    yield
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as _t
+    assert _t.cuda.is_available(), "GPU tests need a GPU"
+    return _t
+
+
+@pytest.fixture(scope="module")
+def pkg(torch):
+    import paper_2303_10384_amd as P
+    P.load_library()
+    return P
+
+
+def to_dev(torch, x, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(x)).to("cuda:0")
+    return t.to(dtype) if dtype is not None else t
+
+
+def tol_check(loss, grad, loss_ref, grad_ref, half, tl=None, ul=None):
+    """Assert the stated tolerances; returns (max loss rel err, max grad abs err)."""
+    good = np.isfinite(loss_ref)
+    assert np.array_equal(np.isnan(loss), ~good), (loss, loss_ref)
+    rel = np.abs(loss[good] - loss_ref[good]) / np.maximum(np.abs(loss_ref[good]), 1e-30)
+    lrt = 2e-3 if half else 1e-5
+    assert np.all(rel <= lrt), ("loss", rel.max(), loss[good], loss_ref[good])
+    gerr = 0.0
+    if grad is not None:
+        err = np.abs(grad.astype(np.float64) - grad_ref)
+        bound = (2e-3 * np.abs(grad_ref) + 1e-5) if half else 1e-5
+        bad = err > bound
+        assert not bad.any(), ("grad", err.max(), np.argwhere(bad)[:5])
+        gerr = float(err.max())
+        if tl is not None:
+            for b in range(len(tl)):
+                if not good[b]:
+                    assert np.all(grad[b] == 0)
+                    continue
+                assert np.all(grad[b, tl[b]:] == 0)
+                assert np.all(grad[b, :, ul[b] + 1:] == 0)
+    return float(rel.max()) if rel.size else 0.0, gerr
+
+
+def run_case(torch, pkg, logits_np, tl, ul, labels, blank=0, variant="rnnt", dtype="f32", poison=True,
+             need_grad=True):
+    """GPU call on the given inputs (logits rounded to dtype on the device);
+    returns (loss, grad as float64 numpy or None, the exact logits the GPU saw as float64)."""
+    lg = to_dev(torch, logits_np).to(W.torch_dtype(dtype))
+    if poison:
+        W.poison_padding(lg, tl, ul)
+    loss, grad = pkg.rnnt_loss(lg, to_dev(torch, labels), to_dev(torch, tl), to_dev(torch, ul), blank=blank,
+                               variant=variant, need_grad=need_grad)
+    torch.cuda.synchronize()
+    seen = lg.float().cpu().numpy().astype(np.float64)
+    g = grad.float().cpu().numpy().astype(np.float64) if grad is not None else None
+    return loss.cpu().numpy().astype(np.float64), g, seen
+
+
+# ---------------------------------------------------------------------------
+# the library that runs is the in-tree HIP build
+# ---------------------------------------------------------------------------
+
+def test_native_library_loaded(torch, pkg):
+    logits, tl, ul, labels = W.small_case(1, 3, 2, 5, seed=1)
+    run_case(torch, pkg, logits, tl, ul, labels)
+    maps = open("/proc/self/maps").read()
+    assert "librnnt_mi355x.so" in maps
+    assert "gfx950" in pkg.version()
+
+
+# ---------------------------------------------------------------------------
+# lattice kernel on the paper's printed lattices
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("variant,loader,ref", [
+    ("rnnt", lambda: load_figure("fig1_rnnt_lattice.txt"), 4.2574511041),
+    ("wrnnt", lambda: load_figure("fig4_wrnnt_lattice.txt"), 2.2070452674),
+    ("wrnnt_allow_ignore", lambda: allow_ignore_from_fig4(load_figure("fig4_wrnnt_lattice.txt")), 1.9385100266),
+])
+def test_lattice_kernel_on_printed_figures(torch, pkg, variant, loader, ref):
+    fig = loader()
+    lp_b, lp_l = map(np.array, grid_weights(fig))
+    lp_l[:, -1] = np.nan  # never read
+    T, U1 = lp_b.shape
+    out = pkg.lattice_scores(to_dev(torch, lp_b[None]), to_dev(torch, lp_l[None]),
+                             to_dev(torch, np.array([T], np.int32)), to_dev(torch, np.array([U1 - 1], np.int32)),
+                             variant)
+    loss = float(out["loss"][0])
+    assert abs(loss - ref) <= 1e-6 * ref
+    assert abs(float(out["loss_bwd"][0]) - ref) <= 1e-6 * ref
+    alpha, lnP = R.forward_scores(lp_b, np.where(np.isnan(lp_l), -np.inf, lp_l), variant)
+    beta, _ = R.backward_scores(lp_b, np.where(np.isnan(lp_l), -np.inf, lp_l), variant)
+    ob, ol = R.arc_posteriors(alpha, beta, lp_b, np.where(np.isnan(lp_l), -np.inf, lp_l), lnP)
+    np.testing.assert_allclose(out["alpha"][0].cpu().numpy(), alpha, atol=1e-6)
+    np.testing.assert_allclose(out["beta"][0].cpu().numpy(), beta, atol=1e-6)
+    np.testing.assert_allclose(out["occ_blank"][0].cpu().numpy(), ob, atol=1e-6)
+    np.testing.assert_allclose(out["occ_label"][0].cpu().numpy(), ol, atol=1e-6)
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("B,T,U", [(3, 7, 5), (2, 40, 70), (2, 6, 200), (1, 3, 300), (1, 2, 700), (4, 1, 0), (3, 9, 0)])
+def test_lattice_kernel_random_weights(torch, pkg, variant, B, T, U):
+    rng = np.random.default_rng(B * 1000 + T * 10 + U)
+    lp_b = -rng.exponential(1.0, size=(B, T, U + 1))
+    lp_l = -rng.exponential(1.5, size=(B, T, U + 1))
+    tl = rng.integers(1, T, size=B, endpoint=True).astype(np.int32)
+    ul = rng.integers(0, U, size=B, endpoint=True).astype(np.int32)
+    tl[0], ul[0] = T, U
+    out = pkg.lattice_scores(to_dev(torch, lp_b), to_dev(torch, lp_l), to_dev(torch, tl), to_dev(torch, ul), variant)
+    for b in range(B):
+        Tb, Ub = tl[b], ul[b]
+        pb = lp_b[b, :Tb, :Ub + 1]
+        pl = lp_l[b, :Tb, :Ub + 1].copy()
+        pl[:, Ub] = -np.inf
+        alpha, lnP = R.forward_scores(pb, pl, variant)
+        beta, lnPb = R.backward_scores(pb, pl, variant)
+        ob, ol = R.arc_posteriors(alpha, beta, pb, pl, lnP)
+        scale = max(1.0, abs(lnP))
+        assert abs(float(out["loss"][b]) + lnP) <= 1e-9 * scale + 2e-6 * np.sqrt(Tb + Ub), (b, lnP)
+        assert abs(float(out["loss_bwd"][b]) + lnPb) <= 1e-9 * scale + 2e-6 * np.sqrt(Tb + Ub)
+        np.testing.assert_allclose(out["occ_blank"][b, :Tb, :Ub + 1].cpu().numpy(), ob, atol=1e-5)
+        np.testing.assert_allclose(out["occ_label"][b, :Tb, :Ub + 1].cpu().numpy(), ol, atol=1e-5)
+
+
+# ---------------------------------------------------------------------------
+# populate kernel (lse and gathered log-probs), tested on its own
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("V,blank", [(2, 0), (3, 2), (5, 1), (16, 0), (29, 0), (257, 100), (1025, 0), (4100, 4099)])
+def test_populate_kernel(torch, pkg, dtype, V, blank):
+    logits, tl, ul, labels = W.small_case(3, 6, 5, V, seed=V + blank, sigma=3.0, blank=blank)
+    lg = to_dev(torch, logits).to(W.torch_dtype(dtype))
+    W.poison_padding(lg, tl, ul)
+    lse, lpb, lpl = pkg.log_softmax_gather(lg, to_dev(torch, labels), to_dev(torch, tl), to_dev(torch, ul), blank)
+    torch.cuda.synchronize()
+    z = lg.float().cpu().numpy().astype(np.float64)
+    for b in range(3):
+        T_b, U_b = tl[b], ul[b]
+        lse_r, pb_r, pl_r = R.lattice_weights(z[b, :T_b, :U_b + 1], labels[b, :U_b], blank)
+        np.testing.assert_allclose(lse[b, :T_b, :U_b + 1].cpu().numpy(), lse_r, rtol=0, atol=1e-6)
+        np.testing.assert_allclose(lpb[b, :T_b, :U_b + 1].cpu().numpy(), pb_r, rtol=0, atol=1e-6)
+        np.testing.assert_allclose(lpl[b, :T_b, :U_b].cpu().numpy(), pl_r[:, :U_b], rtol=0, atol=1e-6)
+        assert np.all(np.isneginf(lpl[b, :T_b, U_b].cpu().numpy()))
+        # rows outside the utterance are not written
+        assert np.all(np.isnan(lse[b, T_b:].cpu().numpy()))
+        assert np.all(np.isnan(lse[b, :, U_b + 1:].cpu().numpy()))
+
+
+# ---------------------------------------------------------------------------
+# end to end: rnnt_loss against the oracle
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("variant", VARIANTS)
+def test_tiny_workload(torch, pkg, variant):
+    w = W.WORKLOADS["tiny"]
+    tl, ul, labels = W.make_lengths_labels(w)
+    logits = W.make_logits(w, "cuda:0").cpu().numpy()
+    loss, grad, seen = run_case(torch, pkg, logits, tl, ul, labels, variant=variant)
+    loss_ref, grad_ref = R.rnnt_loss_grad(seen, labels, tl, ul, 0, variant)
+    tol_check(loss, grad, loss_ref, grad_ref, False, tl, ul)
+
+
+@pytest.mark.parametrize("variant", ["rnnt", "wrnnt"])
+def test_char_workload(torch, pkg, variant):
+    w = W.WORKLOADS["char"]
+    tl, ul, labels = W.make_lengths_labels(w)
+    logits = W.make_logits(w, "cuda:0").cpu().numpy()
+    loss, grad, seen = run_case(torch, pkg, logits, tl, ul, labels, variant=variant)
+    loss_ref, grad_ref = R.rnnt_loss_grad(seen, labels, tl, ul, 0, variant)
+    tol_check(loss, grad, loss_ref, grad_ref, False, tl, ul)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("B,T,U,V,blank,seed", [
+    (4, 9, 6, 7, 0, 1), (3, 17, 70, 33, 5, 2), (2, 5, 130, 11, 10, 3), (5, 13, 3, 1030, 1029, 4),
+    (2, 4, 2, 3, 1, 5), (3, 6, 4, 2, 0, 6), (1, 1, 5, 9, 0, 7), (2, 11, 0, 6, 2, 8)])
+def test_random_shapes(torch, pkg, dtype, variant, B, T, U, V, blank, seed):
+    logits, tl, ul, labels = W.small_case(B, T, U, V, seed=seed, sigma=2.0, blank=blank)
+    loss, grad, seen = run_case(torch, pkg, logits, tl, ul, labels, blank=blank, variant=variant, dtype=dtype)
+    loss_ref, grad_ref = R.rnnt_loss_grad(seen, labels, tl, ul, blank, variant)
+    tol_check(loss, grad, loss_ref, grad_ref, dtype != "f32", tl, ul)
+
+
+def test_loss_only_matches_fused(torch, pkg):
+    logits, tl, ul, labels = W.small_case(4, 12, 9, 40, seed=11)
+    a, _, _ = run_case(torch, pkg, logits, tl, ul, labels, need_grad=False)
+    b, g, _ = run_case(torch, pkg, logits, tl, ul, labels, need_grad=True)
+    assert g is not None
+    np.testing.assert_array_equal(a, b)
+
+
+def test_bad_data_is_isolated(torch, pkg):
+    logits, tl, ul, labels = W.small_case(6, 8, 5, 12, seed=12)
+    tl[1] = 0          # no frames
+    ul[2] = 6          # more units than U_max
+    labels[3, 1] = 0   # a unit equal to blank
+    labels[4, 0] = 12  # a unit outside the vocabulary
+    tl[5] = 9          # more frames than T_max
+    loss, grad, seen = run_case(torch, pkg, logits, tl, ul, labels, poison=False)
+    assert np.isfinite(loss[0])
+    assert np.all(np.isnan(loss[1:]))
+    assert np.all(grad[1:] == 0)
+    loss_ref, grad_ref = R.rnnt_loss_grad(seen, labels, tl, ul, 0, "rnnt")
+    tol_check(loss, grad, loss_ref, grad_ref, False)
+
+
+def test_batch_permutation_and_determinism(torch, pkg):
+    logits, tl, ul, labels = W.small_case(5, 10, 7, 50, seed=13)
+    l1, g1, _ = run_case(torch, pkg, logits, tl, ul, labels)
+    l2, g2, _ = run_case(torch, pkg, logits, tl, ul, labels)
+    np.testing.assert_array_equal(l1, l2)
+    np.testing.assert_array_equal(g1, g2)
+    perm = np.array([3, 0, 4, 2, 1])
+    lp, gp, _ = run_case(torch, pkg, logits[perm], tl[perm], ul[perm], labels[perm])
+    np.testing.assert_array_equal(lp, l1[perm])
+    np.testing.assert_array_equal(gp, g1[perm])
+
+
+def test_no_write_past_gradient(torch, pkg):
+    logits, tl, ul, labels = W.small_case(3, 7, 4, 13, seed=14)
+    lg = to_dev(torch, logits)
+    n = lg.numel()
+    buf = torch.full((n + 4096,), 12345.0, dtype=torch.float32, device="cuda:0")
+    grad = buf[:n].view(lg.shape)
+    pkg.rnnt_loss(lg, to_dev(torch, labels), to_dev(torch, tl), to_dev(torch, ul), grad_out=grad)
+    torch.cuda.synchronize()
+    assert torch.all(buf[n:] == 12345.0)
+
+
+def test_preallocated_workspace_and_autograd(torch, pkg):
+    logits, tl, ul, labels = W.small_case(3, 8, 5, 21, seed=15)
+    lg = to_dev(torch, logits)
+    nbytes = pkg.loss_workspace_bytes(3, 8, 5, 21)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    l1, g1 = pkg.rnnt_loss(lg, to_dev(torch, labels), to_dev(torch, tl), to_dev(torch, ul), workspace=ws)
+    l2, g2 = pkg.rnnt_loss(lg, to_dev(torch, labels), to_dev(torch, tl), to_dev(torch, ul))
+    assert torch.equal(l1, l2) and torch.equal(g1, g2)
+    x = lg.clone().requires_grad_(True)
+    out = pkg.rnnt_loss_autograd(x, to_dev(torch, labels), to_dev(torch, tl), to_dev(torch, ul), reduction="mean")
+    out.backward()
+    assert torch.allclose(out, l2.mean())
+    assert torch.allclose(x.grad, g2 / 3, atol=1e-7)
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads (the sizes the benchmark times), sampled utterances
+# ---------------------------------------------------------------------------
+
+def full_size_case(torch, pkg, name, loss_utts, grad_utts):
+    w = W.WORKLOADS[name]
+    tl, ul, labels = W.make_lengths_labels(w)
+    lg = W.make_logits(w, "cuda:0")
+    loss, grad = pkg.rnnt_loss(lg, to_dev(torch, labels), to_dev(torch, tl), to_dev(torch, ul), variant=w.variant)
+    torch.cuda.synchronize()
+    loss = loss.cpu().numpy().astype(np.float64)
+    half = w.dtype != "f32"
+    for b in sorted(set(loss_utts) | set(grad_utts)):
+        T_b, U_b = int(tl[b]), int(ul[b])
+        z = lg[b, :T_b, :U_b + 1].float().cpu().numpy().astype(np.float64)
+        r = R.utterance_loss_grad(z, labels[b, :U_b], 0, w.variant, need_grad=b in grad_utts)
+        lref = np.array([r["loss"]])
+        if b in grad_utts:
+            g = grad[b].float().cpu().numpy()
+            gref = np.zeros(g.shape)
+            gref[:T_b, :U_b + 1] = r["grad"]
+            tol_check(loss[b:b + 1], g[None], lref, gref[None], half, tl[b:b + 1], ul[b:b + 1])
+        else:
+            tol_check(loss[b:b + 1], None, lref, None, half)
+    # properties that hold at any size, on every utterance
+    rs = grad.float().sum(dim=-1)
+    assert float(rs.abs().max()) < (2e-3 if half else 2e-5)
+    for b in range(w.B):
+        assert torch.all(grad[b, int(tl[b]):] == 0)
+        assert torch.all(grad[b, :, int(ul[b]) + 1:] == 0)
+    assert np.all(np.isfinite(loss)) and np.all(loss > 0)
+
+
+def test_bpe_workload_full_size(torch, pkg):
+    full_size_case(torch, pkg, "bpe", loss_utts=range(0, 32, 3), grad_utts=[0, 17])
+
+
+def test_wrnnt_workload_full_size(torch, pkg):
+    full_size_case(torch, pkg, "wrnnt", loss_utts=range(0, 32, 4), grad_utts=[0, 9])
+
+
+def test_large_bf16_workload_full_size(torch, pkg):
+    full_size_case(torch, pkg, "large", loss_utts=[0, 31, 63], grad_utts=[0, 40])

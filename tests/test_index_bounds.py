@@ -1,0 +1,100 @@
+"""Host-side model of the kernels' grids and index arithmetic (no GPU).
+
+Before any launch, this checks for every workload shape that each block of
+each kernel only addresses memory inside the buffers it is given, that the
+gradient kernel's chunk -> (row, column) mapping reproduces the flat index
+exactly, and that 32-bit intermediates cannot overflow.  The formulas mirror
+the launch code in csrc/rnnt_api.hip and the kernels' index expressions.
+"""
+import numpy as np
+import pytest
+
+from paper_2303_10384_amd.workloads import WORKLOADS
+
+EPC = {"f32": 4, "bf16": 8, "f16": 8}
+SHAPES = [(w.B, w.T_max, w.U_max, w.V, w.dtype) for w in WORKLOADS.values()] + [
+    (3, 7, 0, 2, "f32"), (2, 5, 4, 3, "bf16"), (1, 1, 1023, 5, "f32"), (4, 9, 63, 4097, "f16"),
+    (5, 3, 64, 7, "bf16"), (2, 2, 127, 8, "f32")]
+
+
+def k1_group_lanes(V, epc):
+    max_chunks = (epc - 1 + V + epc - 1) // epc
+    want = (max_chunks + 3) // 4
+    g = 8
+    while g < want and g < 64:
+        g <<= 1
+    return g
+
+
+@pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
+def test_populate_kernel_addresses(B, T, U, V, dt):
+    epc = EPC[dt]
+    n_elem = B * T * (U + 1) * V
+    G = k1_group_lanes(V, epc)
+    rows_per_block = (256 // G) * 4
+    n_ublk = -(-(U + 1) // rows_per_block)
+    blocks = B * T * n_ublk
+    assert blocks < 2**31
+    # every row a block can touch (u < U+1 always, the lengths bound it further)
+    seg = np.arange(B * T, dtype=np.int64)
+    for u in (0, U):
+        row = seg * (U + 1) + u
+        e0 = row * V
+        c0 = e0 // epc
+        mis = e0 - c0 * epc
+        nch = (mis + V + epc - 1) // epc
+        last_chunk = c0 + nch - 1
+        # whole-chunk loads only when the chunk ends inside the tensor
+        assert np.all(last_chunk * epc < n_elem)
+        assert np.all(e0 + V <= n_elem)
+    # lp written by diagonal: (b, t, u) -> 2*((t+u)*(U+1)+u) (+1) inside B*(T+U)*(U+1) double2
+    sb, st, su = 2 * (T + U) * (U + 1), 2 * (U + 1), 2 * (U + 2)
+    hi = (B - 1) * sb + (T - 1) * st + U * su + 1
+    assert hi < 2 * B * (T + U) * (U + 1)
+
+
+@pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
+def test_gradient_kernel_chunk_mapping(B, T, U, V, dt):
+    epc = EPC[dt]
+    n_elem = B * T * (U + 1) * V
+    n_rows = B * T * (U + 1)
+    tile = 256 * 4
+    chunks = -(-n_elem // epc)
+    blocks = -(-chunks // tile)
+    assert blocks < 2**31
+    rng = np.random.default_rng(0)
+    blk = np.unique(np.concatenate([np.arange(min(blocks, 64)), np.arange(max(0, blocks - 64), blocks),
+                                    rng.integers(0, blocks, size=256)])).astype(np.int64)
+    tile0 = blk * tile
+    e_tile = tile0 * epc
+    r_tile = e_tile // V
+    v_tile = e_tile - r_tile * V
+    assert np.all(v_tile < V)
+    for cl in (0, 1, 255, 256, tile - 1):
+        c = tile0 + cl
+        e0 = c * epc
+        live = e0 < n_elem
+        off = v_tile + cl * epc
+        assert np.all(off < 2**32)
+        dr = off // V
+        r = r_tile + dr
+        v = off - dr * V
+        assert np.all((r * V + v)[live] == e0[live])
+        assert np.all(r[live] < n_rows)
+        if V >= epc:
+            split = v + epc > V
+            # the second row of a split chunk exists unless the chunk runs past the end
+            assert np.all(((r + 1 < n_rows) | (e0 + epc > n_elem))[live & split])
+
+
+@pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
+def test_lattice_kernel_addresses(B, T, U, V, dt):
+    U1 = U + 1
+    K = next(k for k in (1, 2, 4, 8, 16) if U1 <= 64 * k)
+    assert 64 * K >= U1
+    sab = (T + U) * U1
+    # alpha / beta at (b, d, u): d <= T-1+U, u <= U; beta also reads d+1 only for valid neighbours
+    hi = (B - 1) * sab + (T - 1 + U) * U1 + U
+    assert hi < B * sab
+    # the epilogue reads beta(t+1, u) for t < T-1 and beta(t, u+1) for u < U: diagonal <= T-1+U
+    assert (T - 2 + 1 + U) <= T - 1 + U
