@@ -53,7 +53,7 @@ typedef enum {
   RNNT_ERR_NULL_PTR = 1,     /* a required pointer is NULL                       */
   RNNT_ERR_BAD_SHAPE = 2,    /* B < 1, T_max < 1, U_max < 0, V < 2, or too large */
   RNNT_ERR_BAD_BLANK = 3,    /* blank outside [0, V)                             */
-  RNNT_ERR_BAD_DTYPE = 4,    /* unknown rnnt_dtype_t                             */
+  RNNT_ERR_BAD_DTYPE = 4,    /* unknown dtype, or grad_dtype not dtype / F32     */
   RNNT_ERR_BAD_VARIANT = 5,  /* unknown rnnt_variant_t                           */
   RNNT_ERR_WORKSPACE = 6,    /* workspace given but smaller than required        */
   RNNT_ERR_ALIGNMENT = 7,    /* logits or grad not 16-byte aligned               */
@@ -75,13 +75,18 @@ typedef enum {
                         /* inside (the half-precision lattice of Section 4.2)      */
 } rnnt_dtype_t;
 
-/* Padded problem shape: logits are (B, T_max, U_max+1, V) of `dtype`. */
+/* Padded problem shape: logits are (B, T_max, U_max+1, V) of `dtype`; the
+ * gradient has the same shape and element type `grad_dtype`, which must be
+ * `dtype` itself or RNNT_DTYPE_F32 (a float32 gradient of half-precision
+ * logits: the gradient is computed in float32 either way, this only decides
+ * how it is stored). */
 typedef struct {
   int32_t B;
   int32_t T_max;
   int32_t U_max;
   int32_t V;
   rnnt_dtype_t dtype;
+  rnnt_dtype_t grad_dtype;
 } rnnt_shape_t;
 
 /* Bytes of device workspace that rnnt_loss needs for `shape` (0 if the shape
@@ -99,7 +104,7 @@ size_t rnnt_loss_workspace_bytes(rnnt_shape_t shape);
  *   blank       index of the blank symbol in [0, V).
  *   variant     rnnt_variant_t.
  *   loss_out    (B) float32: loss_b, no reduction (NaN for bad data).
- *   grad_out    NULL (loss only) or (B, T_max, U_max+1, V) of shape.dtype:
+ *   grad_out    NULL (loss only) or (B, T_max, U_max+1, V) of shape.grad_dtype:
  *               every element is written; rows outside t < T_b, u <= U_b and
  *               all rows of a bad utterance are exactly 0.  The gradient of
  *               row (t, u) is softmax * (g_blank + g_label) - g_blank at
@@ -162,8 +167,8 @@ rnnt_status_t rnnt_log_softmax_gather(const void* logits, rnnt_shape_t shape, co
  *   occ_blank_out       posterior of the blank arc leaving each node (0 where
  *                       absent)
  *   occ_label_out       posterior of the label arc leaving each node
- * label_lens/logit_lens as in rnnt_loss; shape.V and shape.dtype are ignored
- * (pass V >= 2).  A bad utterance (lengths out of range) gets NaN losses and
+ * label_lens/logit_lens as in rnnt_loss; shape.V, shape.dtype and
+ * shape.grad_dtype are ignored (pass V >= 2).  A bad utterance (lengths out of range) gets NaN losses and
  * no other output.  Needs a workspace of rnnt_lattice_workspace_bytes(shape)
  * bytes or NULL (then allocated stream-ordered).
  */

@@ -26,7 +26,7 @@ EXPORTED = ("rnnt_loss_workspace_bytes", "rnnt_loss", "rnnt_loss_timed", "rnnt_l
 
 class Shape(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("T_max", ctypes.c_int32), ("U_max", ctypes.c_int32),
-                ("V", ctypes.c_int32), ("dtype", ctypes.c_int)]
+                ("V", ctypes.c_int32), ("dtype", ctypes.c_int), ("grad_dtype", ctypes.c_int)]
 
 
 class RNNTError(RuntimeError):
@@ -107,23 +107,25 @@ def _stream_handle(device):
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
-def shape_of(logits):
+def shape_of(logits, grad_dtype=None):
     B, T, U1, V = logits.shape
-    return Shape(B, T, U1 - 1, V, dtype_code(logits.dtype))
+    dt = dtype_code(logits.dtype)
+    return Shape(B, T, U1 - 1, V, dt, dt if grad_dtype is None else dtype_code(grad_dtype))
 
 
 def loss_workspace_bytes(B, T_max, U_max, V, dtype_code_=DTYPE_F32):
-    return load_library().rnnt_loss_workspace_bytes(Shape(B, T_max, U_max, V, dtype_code_))
+    return load_library().rnnt_loss_workspace_bytes(Shape(B, T_max, U_max, V, dtype_code_, dtype_code_))
 
 
 def rnnt_loss(logits, labels, logit_lens, label_lens, blank=0, variant="rnnt", need_grad=True,
-              workspace=None, grad_out=None, loss_out=None, events=None):
+              workspace=None, grad_out=None, loss_out=None, events=None, grad_dtype=None):
     """Per-utterance loss (float32, shape (B,)) and gradient (logits' shape and dtype, or None).
 
     logits (B, T_max, U_max+1, V) float32/bfloat16/float16 on the GPU; labels (B, U_max) int32;
     logit_lens, label_lens (B,) int32.  workspace: optional uint8 GPU tensor of at least
     loss_workspace_bytes(...) bytes; grad_out / loss_out: optional preallocated outputs;
-    events: optional ctypes array of 4 hipEvent_t recorded around the three kernels.
+    events: optional ctypes array of 4 hipEvent_t recorded around the three kernels;
+    grad_dtype: None (the logits' dtype) or torch.float32.
     """
     torch = _torch()
     lib = load_library()
@@ -133,7 +135,9 @@ def rnnt_loss(logits, labels, logit_lens, label_lens, blank=0, variant="rnnt", n
     _check_gpu("label_lens", label_lens, torch.int32)
     if logits.dim() != 4:
         raise ValueError("logits must be (B, T_max, U_max+1, V)")
-    shape = shape_of(logits)
+    if grad_out is not None and grad_dtype is None:
+        grad_dtype = grad_out.dtype
+    shape = shape_of(logits, grad_dtype)
     if labels.shape != (shape.B, shape.U_max) or logit_lens.shape != (shape.B,) or label_lens.shape != (shape.B,):
         raise ValueError("labels must be (B, U_max) and the length vectors (B,)")
     if variant not in VARIANTS:
@@ -143,8 +147,9 @@ def rnnt_loss(logits, labels, logit_lens, label_lens, blank=0, variant="rnnt", n
     _check_gpu("loss_out", loss, torch.float32)
     grad = None
     if need_grad:
-        grad = grad_out if grad_out is not None else torch.empty_like(logits)
-        _check_gpu("grad_out", grad, logits.dtype)
+        gdt = logits.dtype if grad_dtype is None else grad_dtype
+        grad = grad_out if grad_out is not None else torch.empty(logits.shape, dtype=gdt, device=dev)
+        _check_gpu("grad_out", grad, gdt)
         if grad.shape != logits.shape:
             raise ValueError("grad_out must have the logits' shape")
     ws_ptr, ws_bytes = ctypes.c_void_p(0), 0
@@ -190,7 +195,7 @@ def lattice_scores(lp_blank, lp_label, logit_lens, label_lens, variant="rnnt"):
     for n, t in (("lp_blank", lp_blank), ("lp_label", lp_label)):
         _check_gpu(n, t, torch.float64)
     B, T, U1 = lp_blank.shape
-    shape = Shape(B, T, U1 - 1, 2, DTYPE_F32)
+    shape = Shape(B, T, U1 - 1, 2, DTYPE_F32, DTYPE_F32)
     dev = lp_blank.device
     nan = float("nan")
     out = {k: torch.full((B, T, U1), nan, dtype=torch.float64, device=dev)

@@ -30,6 +30,7 @@ rnnt_status_t check_shape(const rnnt_shape_t& s) {
   if (static_cast<int64_t>(s.B) * rows_per_utt > (int64_t{1} << 40)) return RNNT_ERR_BAD_SHAPE;
   if (s.V > (1 << 30)) return RNNT_ERR_BAD_SHAPE;
   if (!dtype_known(s.dtype)) return RNNT_ERR_BAD_DTYPE;
+  if (s.grad_dtype != s.dtype && s.grad_dtype != RNNT_DTYPE_F32) return RNNT_ERR_BAD_DTYPE;
   return RNNT_OK;
 }
 
@@ -144,24 +145,27 @@ hipError_t launch_k2(const LatticeParams& p, hipStream_t stream) {
 
 // ---- kernel 3 ---------------------------------------------------------------
 
-template <typename T>
+template <typename Tin, typename Tout>
 hipError_t launch_k3(const GradParams& p, hipStream_t stream) {
-  constexpr int EPC = ElemTraits<T>::kPerChunk;
+  constexpr int EPC = ElemTraits<Tin>::kPerChunk;
   const int64_t chunks = (p.n_elem + EPC - 1) / EPC;
   const int64_t blocks = (chunks + kGradTileChunks - 1) / kGradTileChunks;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   if (p.V < EPC)
-    hipLaunchKernelGGL((k3_grad<T, true>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads), 0, stream, p);
+    hipLaunchKernelGGL((k3_grad<Tin, Tout, true>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads), 0,
+                       stream, p);
   else
-    hipLaunchKernelGGL((k3_grad<T, false>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads), 0, stream, p);
+    hipLaunchKernelGGL((k3_grad<Tin, Tout, false>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads), 0,
+                       stream, p);
   return hipGetLastError();
 }
 
-hipError_t launch_k3_dtype(rnnt_dtype_t dt, const GradParams& p, hipStream_t stream) {
+hipError_t launch_k3_dtype(rnnt_dtype_t dt, rnnt_dtype_t gdt, const GradParams& p, hipStream_t stream) {
+  const bool f32_out = gdt == RNNT_DTYPE_F32;
   switch (dt) {
-    case RNNT_DTYPE_F32: return launch_k3<float>(p, stream);
-    case RNNT_DTYPE_BF16: return launch_k3<bf16_t>(p, stream);
-    default: return launch_k3<f16_t>(p, stream);
+    case RNNT_DTYPE_F32: return launch_k3<float, float>(p, stream);
+    case RNNT_DTYPE_BF16: return f32_out ? launch_k3<bf16_t, float>(p, stream) : launch_k3<bf16_t, bf16_t>(p, stream);
+    default: return f32_out ? launch_k3<f16_t, float>(p, stream) : launch_k3<f16_t, f16_t>(p, stream);
   }
 }
 
@@ -189,7 +193,7 @@ const char* rnnt_status_string(rnnt_status_t status) {
     case RNNT_ERR_NULL_PTR: return "a required pointer is NULL";
     case RNNT_ERR_BAD_SHAPE: return "bad shape (need B >= 1, T_max >= 1, U_max >= 0, V >= 2, sizes in range)";
     case RNNT_ERR_BAD_BLANK: return "blank outside [0, V)";
-    case RNNT_ERR_BAD_DTYPE: return "unknown dtype";
+    case RNNT_ERR_BAD_DTYPE: return "unknown dtype, or grad_dtype neither dtype nor F32";
     case RNNT_ERR_BAD_VARIANT: return "unknown variant";
     case RNNT_ERR_WORKSPACE: return "workspace smaller than required";
     case RNNT_ERR_ALIGNMENT: return "logits / grad must be 16-byte aligned";
@@ -209,6 +213,7 @@ size_t rnnt_loss_workspace_bytes(rnnt_shape_t shape) {
 size_t rnnt_lattice_workspace_bytes(rnnt_shape_t shape) {
   rnnt_shape_t s = shape;
   s.dtype = RNNT_DTYPE_F32;
+  s.grad_dtype = RNNT_DTYPE_F32;
   if (check_shape(s) != RNNT_OK) return 0;
   return lattice_layout(s).total;
 }
@@ -306,7 +311,7 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
     p3.n_rows = n_rows;
     p3.V = shape.V;
     p3.blank = blank;
-    if (launch_k3_dtype(shape.dtype, p3, stream) != hipSuccess) return RNNT_ERR_HIP;
+    if (launch_k3_dtype(shape.dtype, shape.grad_dtype, p3, stream) != hipSuccess) return RNNT_ERR_HIP;
   }
   if (mark(3) != hipSuccess) return RNNT_ERR_HIP;
   return RNNT_OK;
@@ -360,6 +365,7 @@ rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label
                                   hipStream_t stream) {
   rnnt_shape_t s = shape;
   s.dtype = RNNT_DTYPE_F32;
+  s.grad_dtype = RNNT_DTYPE_F32;
   rnnt_status_t st = check_shape(s);
   if (st != RNNT_OK) return st;
   if (!lp_blank || !lp_label || !logit_lens || !label_lens) return RNNT_ERR_NULL_PTR;

@@ -36,9 +36,22 @@ __device__ __forceinline__ float grad_elem(float z, int v, const RowInfo& ri, in
   return (ri.label == kZeroRow) ? 0.f : g;
 }
 
+// Gradient elements of one 16-byte input chunk, stored as Tout (one or two
+// aligned 16-byte stores).
+template <typename Tout, int EPC>
+__device__ __forceinline__ void store_chunk(void* dst, int64_t e0, const float* out) {
+  constexpr int PER = ElemTraits<Tout>::kPerChunk;
+  static_assert(EPC % PER == 0, "input chunk must cover whole output chunks");
+  uint4* d = reinterpret_cast<uint4*>(static_cast<Tout*>(dst) + e0);
+#pragma unroll
+  for (int i = 0; i < EPC / PER; ++i) d[i] = ElemTraits<Tout>::pack(out + i * PER);
+}
+
+// Tin: logits element type; Tout: gradient element type (Tin or float).
 // SMALLV: V < elements per chunk, so one chunk may cover several rows.
-template <typename T, bool SMALLV>
+template <typename Tin, typename Tout, bool SMALLV>
 __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
+  using T = Tin;
   constexpr int EPC = ElemTraits<T>::kPerChunk;
   const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kGradTileChunks;
   const int64_t e_tile = tile0 * EPC;
@@ -46,9 +59,8 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
   const uint32_t v_tile = static_cast<uint32_t>(e_tile - r_tile * p.V);
   const uint32_t uV = static_cast<uint32_t>(p.V);
   const uint4* __restrict__ src = static_cast<const uint4*>(p.logits);
-  uint4* __restrict__ dst = static_cast<uint4*>(p.grad);
   const T* __restrict__ src_e = static_cast<const T*>(p.logits);
-  T* __restrict__ dst_e = static_cast<T*>(p.grad);
+  Tout* __restrict__ dst_e = static_cast<Tout*>(p.grad);
 
 #pragma unroll
   for (int q = 0; q < kGradChunksPerThread; ++q) {
@@ -109,11 +121,11 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
       }
     }
     if (full) {
-      dst[c] = ElemTraits<T>::pack(out);
+      store_chunk<Tout, EPC>(p.grad, e0, out);
     } else {
 #pragma unroll
       for (int j = 0; j < EPC; ++j)
-        if (e0 + j < p.n_elem) ElemTraits<T>::store1(dst_e + e0 + j, out[j]);
+        if (e0 + j < p.n_elem) ElemTraits<Tout>::store1(dst_e + e0 + j, out[j]);
     }
   }
 }

@@ -48,9 +48,9 @@ def test_status_strings_and_version(lib):
     assert "gfx950" in binding.version()
 
 
-def shape(B=2, T=5, U=3, V=7, dt=0):
+def shape(B=2, T=5, U=3, V=7, dt=0, gdt=None):
     from paper_2303_10384_amd.binding import Shape
-    return Shape(B, T, U, V, dt)
+    return Shape(B, T, U, V, dt, dt if gdt is None else gdt)
 
 
 def expected_workspace(B, T, U, V):
@@ -91,6 +91,8 @@ def test_rnnt_loss_host_errors(lib):
     assert call_loss(lib, shape(U=-1)) == 2
     assert call_loss(lib, shape(V=1)) == 2
     assert call_loss(lib, shape(dt=3)) == 4
+    assert call_loss(lib, shape(dt=0, gdt=1)) == 4   # fp32 logits, bf16 gradient: not offered
+    assert call_loss(lib, shape(dt=1, gdt=2)) == 4
     assert call_loss(lib, shape(), logits=0) == 1
     assert call_loss(lib, shape(), labels=0) == 1
     assert call_loss(lib, shape(), tl=0) == 1
