@@ -89,9 +89,13 @@ def tol_check(loss, grad, loss_ref, grad_ref, logits_dtype="f32", tl=None, ul=No
         assert not bad.any(), ("grad", err.max(), np.argwhere(bad)[:5])
         gerr = float(err.max())
         if grad_dtype == "bf16":
-            # float32 arithmetic: the stored value is the correctly rounded g_ref except next to a tie
-            differ = grad != bf16_round(grad_ref)
-            assert differ.mean() <= 1e-2, differ.mean()
+            # float32 arithmetic: the stored value is the correctly rounded g_ref, or its
+            # neighbour where g_ref sits next to a tie or is a cancelling small difference
+            rn = bf16_round(grad_ref)
+            differ = grad != rn
+            assert np.all(np.abs(grad - rn)[differ] <= 2.0 ** -7 * np.abs(rn[differ]) + 1e-5)
+            if differ.size >= 10000:
+                assert differ.mean() <= 1e-2, differ.mean()
         if tl is not None:
             for b in range(len(tl)):
                 if not good[b]:
