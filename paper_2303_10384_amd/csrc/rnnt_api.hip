@@ -37,7 +37,7 @@ rnnt_status_t check_shape(const rnnt_shape_t& s) {
 // Workspace of rnnt_loss, all pieces 256-byte aligned:
 //   rowinfo  (B*T_max*(U_max+1)) RowInfo
 //   lp       (B, T_max+U_max, U_max+1) double2 {lp_blank, lp_label}, indexed by diagonal
-//   alpha    (B, T_max+U_max, U_max+1) double, indexed by diagonal
+//   alpha    (B, T_max+U_max+1, U_max+1) double, indexed by diagonal (last row: scratch)
 //   beta     same
 //   lnp      2*B double
 struct LossLayout {
@@ -47,6 +47,7 @@ struct LossLayout {
 LossLayout loss_layout(const rnnt_shape_t& s) {
   const size_t rows = static_cast<size_t>(s.B) * s.T_max * (s.U_max + 1);
   const size_t cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max) * (s.U_max + 1);
+  const size_t score_cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max + 1) * (s.U_max + 1);
   LossLayout L{};
   size_t o = 0;
   L.rowinfo = o;
@@ -54,9 +55,9 @@ LossLayout loss_layout(const rnnt_shape_t& s) {
   L.lp = o;
   o = align256(o + cells * 2 * sizeof(double));
   L.alpha = o;
-  o = align256(o + cells * sizeof(double));
+  o = align256(o + score_cells * sizeof(double));
   L.beta = o;
-  o = align256(o + cells * sizeof(double));
+  o = align256(o + score_cells * sizeof(double));
   L.lnp = o;
   o = align256(o + 2 * static_cast<size_t>(s.B) * sizeof(double));
   L.total = o;
@@ -69,7 +70,7 @@ struct LatticeLayout {
 };
 
 LatticeLayout lattice_layout(const rnnt_shape_t& s) {
-  const size_t cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max) * (s.U_max + 1);
+  const size_t cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max + 1) * (s.U_max + 1);
   LatticeLayout L{};
   size_t o = 0;
   L.alpha = o;
@@ -84,34 +85,61 @@ LatticeLayout lattice_layout(const rnnt_shape_t& s) {
 
 // ---- kernel 1 ---------------------------------------------------------------
 
+// Lanes per row G and chunks per lane NB for kernel 1: the smallest G*NB
+// that covers a row's chunks (NB <= 5 keeps the batch in registers); rows
+// longer than 64*5 chunks take several batches.
+struct K1Shape {
+  int G, NB;
+};
+
 template <typename T>
-int k1_group_lanes(int V) {
+K1Shape k1_shape(int V) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
   const int max_chunks = (EPC - 1 + V + EPC - 1) / EPC;
-  int want = (max_chunks + 3) / 4;  // about four chunks per lane
-  int g = 8;
-  while (g < want && g < 64) g <<= 1;
-  return g;
+  K1Shape best{64, 5};
+  int best_slots = 1 << 30;
+  for (int g : {64, 32, 16, 8}) {
+    for (int nb = 1; nb <= 5; ++nb) {
+      const int slots = g * nb;
+      if (slots >= max_chunks && slots < best_slots) {
+        best = K1Shape{g, nb};
+        best_slots = slots;
+      }
+    }
+  }
+  return best;
 }
 
-template <typename T, int G>
+template <typename T, int G, int NB>
 hipError_t launch_k1_g(PopulateParams p, hipStream_t stream) {
   constexpr int groups = 256 / G;
   p.rows_per_block = groups * 4;
   p.n_ublk = (p.U_max + 1 + p.rows_per_block - 1) / p.rows_per_block;
   const int64_t blocks = static_cast<int64_t>(p.B) * p.T_max * p.n_ublk;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((k1_populate<T, G>), dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, stream, p);
+  hipLaunchKernelGGL((k1_populate<T, G, NB>), dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 
+template <typename T, int G>
+hipError_t launch_k1_nb(int nb, const PopulateParams& p, hipStream_t stream) {
+  switch (nb) {
+    case 1: return launch_k1_g<T, G, 1>(p, stream);
+    case 2: return launch_k1_g<T, G, 2>(p, stream);
+    case 3: return launch_k1_g<T, G, 3>(p, stream);
+    case 4: return launch_k1_g<T, G, 4>(p, stream);
+    default: return launch_k1_g<T, G, 5>(p, stream);
+  }
+}
+
 template <typename T>
-hipError_t launch_k1(PopulateParams p, hipStream_t stream) {
-  switch (k1_group_lanes<T>(p.V)) {
-    case 8: return launch_k1_g<T, 8>(p, stream);
-    case 16: return launch_k1_g<T, 16>(p, stream);
-    case 32: return launch_k1_g<T, 32>(p, stream);
-    default: return launch_k1_g<T, 64>(p, stream);
+hipError_t launch_k1(const PopulateParams& p, hipStream_t stream) {
+  const K1Shape ks = k1_shape<T>(p.V);
+  switch (ks.G) {
+    case 8: return launch_k1_nb<T, 8>(ks.NB, p, stream);
+    case 16: return launch_k1_nb<T, 16>(ks.NB, p, stream);
+    case 32: return launch_k1_nb<T, 32>(ks.NB, p, stream);
+    default: return launch_k1_nb<T, 64>(ks.NB, p, stream);
   }
 }
 
@@ -292,7 +320,7 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
   p2.su = p1.su;
   p2.alpha = reinterpret_cast<double*>(ws + L.alpha);
   p2.beta = reinterpret_cast<double*>(ws + L.beta);
-  p2.sab = static_cast<int64_t>(shape.T_max + shape.U_max) * U1;
+  p2.sab = static_cast<int64_t>(shape.T_max + shape.U_max + 1) * U1;
   p2.lnp_fwd = reinterpret_cast<double*>(ws + L.lnp);
   p2.lnp_bwd = p2.lnp_fwd + shape.B;
   p2.loss_f32 = loss_out;
@@ -400,7 +428,7 @@ rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label
   p2.su = 1;
   p2.alpha = reinterpret_cast<double*>(ws + L.alpha);
   p2.beta = reinterpret_cast<double*>(ws + L.beta);
-  p2.sab = static_cast<int64_t>(s.T_max + s.U_max) * U1;
+  p2.sab = static_cast<int64_t>(s.T_max + s.U_max + 1) * U1;
   p2.lnp_fwd = reinterpret_cast<double*>(ws + L.lnp);
   p2.lnp_bwd = p2.lnp_fwd + s.B;
   p2.loss_f32 = nullptr;

@@ -9,10 +9,14 @@
 // for the gradient kernel.  Padding rows are never touched.
 //
 // Mapping: a block owns `rows_per_block` consecutive rows u of one (b, t)
-// segment; a group of G lanes (G = 8..64, chosen from V) reads one row with
-// aligned 16-byte loads (the chunks straddling the row's ends are masked, the
-// tensor's last partial chunk is read element-wise), reduces max then sum
-// within the group, and its lane 0 writes the row's outputs.
+// segment; a group of G lanes reads one row as aligned 16-byte chunks, NB
+// chunks per lane per batch (G and NB are picked from V so that G*NB just
+// covers a row).  All loads of a batch are issued unconditionally (chunk index
+// clamped into the row) before any value is touched, and the elements outside
+// the row are masked afterwards, so a row's loads are in flight together.  The
+// group reduces max, then sum of exp in float32 per lane and float64 across
+// lanes.  A row whose last chunk runs past the end of the tensor (only the
+// tensor's last row can) takes an element-wise path.
 #pragma once
 
 #include "rnnt_device.h"
@@ -35,12 +39,39 @@ struct PopulateParams {
   double* lse_out;         // dense (B, T_max, U_max+1) or null
 };
 
-template <typename T, int G>
+// (max, sum of exp) of one batch of register-held values, merged into the
+// lane's running pair.
+template <int N>
+__device__ __forceinline__ void merge_batch(const float (&x)[N], float& mloc, float& sloc) {
+  const float kNegInf = -__builtin_inff();
+  float bm = kNegInf;
+#pragma unroll
+  for (int i = 0; i < N; ++i) bm = fmaxf(bm, x[i]);
+  const float mn = fmaxf(mloc, bm);
+  const float sh = (mn == kNegInf) ? 0.f : mn;
+  float acc = 0.f;
+#pragma unroll
+  for (int i = 0; i < N; ++i) acc += fast_exp2((x[i] - sh) * kLog2eF);
+  sloc = (mloc == kNegInf) ? acc : fmaf(sloc, fast_exp2((mloc - sh) * kLog2eF), acc);
+  mloc = mn;
+}
+
+// Value of element `idx` of a register array (select chain, no dynamic index).
+template <int N>
+__device__ __forceinline__ float pick_reg(const float (&x)[N], int idx) {
+  float r = x[0];
+#pragma unroll
+  for (int i = 1; i < N; ++i) r = (idx == i) ? x[i] : r;
+  return r;
+}
+
+template <typename T, int G, int NB>
 __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
-  constexpr int NB = 32 / EPC;      // chunks per lane per register batch
-  constexpr int GROUPS = 256 / G;   // rows in flight per block
+  constexpr int GROUPS = 256 / G;      // rows in flight per block
+  constexpr int MAX_ROWS = GROUPS * 4; // rows_per_block set by the launcher
   const float kNegInf = -__builtin_inff();
+  __shared__ int s_label[MAX_ROWS];
 
   const int seg = blockIdx.x / p.n_ublk;  // b * T_max + t
   const int ublk = blockIdx.x - seg * p.n_ublk;
@@ -54,8 +85,16 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   const int grp = threadIdx.x / G;
   const int u_begin = ublk * p.rows_per_block;
   const int u_end = min(u_begin + p.rows_per_block, Ub + 1);
+  // the block's labels go through LDS, so no label load waits inside the row loop
+  if (threadIdx.x < MAX_ROWS) {
+    const int u = u_begin + threadIdx.x;
+    s_label[threadIdx.x] = (u < Ub) ? p.labels[static_cast<int64_t>(b) * p.U_max + u] : kNoLabel;
+  }
+  __syncthreads();
+
   const T* __restrict__ base = static_cast<const T*>(p.logits);
   const uint4* __restrict__ cbase = reinterpret_cast<const uint4*>(base);
+  const int64_t full_chunks = p.n_elem / EPC;
 
   for (int u = u_begin + grp; u < u_end; u += GROUPS) {
     const int64_t row = static_cast<int64_t>(seg) * (p.U_max + 1) + u;
@@ -63,59 +102,56 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
     const int64_t c0 = e0 / EPC;
     const int mis = static_cast<int>(e0 - c0 * EPC);
     const int nch = (mis + p.V + EPC - 1) / EPC;
-
-    // the two gathered logits, issued before the streaming loads
-    float zb = 0.f, zy = 0.f;
-    int y = kNoLabel;
-    if (lg == 0) {
-      zb = ElemTraits<T>::load1(base + e0 + p.blank);
-      if (u < Ub) {
-        y = p.labels[static_cast<int64_t>(b) * p.U_max + u];
-        if (y >= 0 && y < p.V) zy = ElemTraits<T>::load1(base + e0 + y);
-      }
-    }
+    const int y = s_label[u - u_begin];
+    const bool y_ok = (y >= 0 && y < p.V);
+    // chunk / lane / register slot holding z[blank] and z[y]
+    const int kb_blank = (p.blank + mis) / EPC, kb_y = ((y_ok ? y : 0) + mis) / EPC;
+    float zb_loc = 0.f, zy_loc = 0.f;
 
     float mloc = kNegInf, sloc = 0.f;
-    for (int kb = 0; kb < nch; kb += G * NB) {
-      float x[NB * EPC];
+    if (c0 + nch <= full_chunks) {
+      for (int kb = 0; kb < nch; kb += G * NB) {
+        uint4 raw[NB];
 #pragma unroll
-      for (int q = 0; q < NB; ++q) {
-        const int k = kb + q * G + lg;
-        float f[EPC];
-        if (k < nch) {
-          const int64_t ck = c0 + k;
-          if ((ck + 1) * EPC <= p.n_elem) {
-            ElemTraits<T>::unpack(cbase[ck], f);
-          } else {
+        for (int q = 0; q < NB; ++q) {
+          const int k = min(kb + q * G + lg, nch - 1);
+          raw[q] = cbase[c0 + k];
+        }
+        float x[NB * EPC];
 #pragma unroll
-            for (int j = 0; j < EPC; ++j) {
-              const int64_t e = ck * EPC + j;
-              f[j] = (e < p.n_elem) ? ElemTraits<T>::load1(base + e) : kNegInf;
-            }
-          }
+        for (int q = 0; q < NB; ++q) {
+          float f[EPC];
+          ElemTraits<T>::unpack(raw[q], f);
+          const int k = kb + q * G + lg;
 #pragma unroll
           for (int j = 0; j < EPC; ++j) {
             const int v = k * EPC + j - mis;
-            if (v < 0 || v >= p.V) f[j] = kNegInf;
+            x[q * EPC + j] = (k < nch && v >= 0 && v < p.V) ? f[j] : kNegInf;
           }
-        } else {
-#pragma unroll
-          for (int j = 0; j < EPC; ++j) f[j] = kNegInf;
         }
-#pragma unroll
-        for (int j = 0; j < EPC; ++j) x[q * EPC + j] = f[j];
+        // the owner lane of this batch keeps z[blank] / z[y] (slot = chunk offset in batch)
+        if (kb_blank >= kb && kb_blank < kb + G * NB)
+          zb_loc = pick_reg<NB * EPC>(x, ((kb_blank - kb) / G) * EPC + (p.blank + mis) % EPC);
+        if (kb_y >= kb && kb_y < kb + G * NB)
+          zy_loc = pick_reg<NB * EPC>(x, ((kb_y - kb) / G) * EPC + ((y_ok ? y : 0) + mis) % EPC);
+        merge_batch<NB * EPC>(x, mloc, sloc);
       }
-      float bm = kNegInf;
+    } else {
+      // last row of the tensor, whose final chunk is partial: element loads
+      for (int k = lg; k < nch; k += G) {
+        float x[EPC];
 #pragma unroll
-      for (int i = 0; i < NB * EPC; ++i) bm = fmaxf(bm, x[i]);
-      const float mn = fmaxf(mloc, bm);
-      const float sh = (mn == kNegInf) ? 0.f : mn;
-      float acc = 0.f;
-#pragma unroll
-      for (int i = 0; i < NB * EPC; ++i) acc += fast_exp2((x[i] - sh) * kLog2eF);
-      sloc = (mloc == kNegInf) ? acc : sloc * fast_exp2((mloc - sh) * kLog2eF) + acc;
-      mloc = mn;
+        for (int j = 0; j < EPC; ++j) {
+          const int v = k * EPC + j - mis;
+          x[j] = (v >= 0 && v < p.V) ? ElemTraits<T>::load1(base + e0 + v) : kNegInf;
+        }
+        if (k == kb_blank) zb_loc = pick_reg<EPC>(x, (p.blank + mis) % EPC);
+        if (k == kb_y) zy_loc = pick_reg<EPC>(x, ((y_ok ? y : 0) + mis) % EPC);
+        merge_batch<EPC>(x, mloc, sloc);
+      }
     }
+    const float zb = __shfl(zb_loc, kb_blank % G, G);
+    const float zy = __shfl(zy_loc, kb_y % G, G);
 
     // group max, then every lane's partial sum rescaled to it and summed in float64
     float mg = mloc;
@@ -132,7 +168,7 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
                          static_cast<int64_t>(u) * p.su;
       p.lp_blank[li] = static_cast<double>(zb) - lse;
       double lpl = -__builtin_inf();
-      if (u < Ub) lpl = (y >= 0 && y < p.V) ? static_cast<double>(zy) - lse : __builtin_nan("");
+      if (u < Ub) lpl = y_ok ? static_cast<double>(zy) - lse : __builtin_nan("");
       p.lp_label[li] = lpl;
       if (p.rowinfo) p.rowinfo[row].lse2 = static_cast<float>(lse * kLog2eD);
       if (p.lse_out) p.lse_out[row] = lse;

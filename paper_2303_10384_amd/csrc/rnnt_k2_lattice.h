@@ -46,7 +46,8 @@ struct LatticeParams {
   const double* lp_blank;  // element (b,t,u) at b*sb + t*st + u*su (in doubles)
   const double* lp_label;
   int64_t sb, st, su;
-  double* alpha;  // workspace: (b, d, u) at b*sab + d*(U_max+1) + u
+  double* alpha;  // workspace: (b, d, u) at b*sab + d*(U_max+1) + u, plus one scratch row
+                  // per utterance after diagonal T_max+U_max-1 (sab >= (T_max+U_max+1)*(U_max+1))
   double* beta;
   int64_t sab;
   double* lnp_fwd;  // (B) workspace
@@ -61,6 +62,10 @@ struct LatticeParams {
   double* loss_bwd_out;  // (B) or null
 };
 
+// Arc weights of diagonal d for the lane's K cells.  The loads are issued
+// unconditionally (cells outside the utterance read its node (0,0), which is
+// always written) and nothing touches the registers here, so the loads stay in
+// flight until the step that uses them; masking happens at that use.
 template <int K, bool IL>
 __device__ __forceinline__ void load_diag(const LatticeParams& p, int64_t lp0, int d, int lane, int T, int U,
                                           double (&rb)[K], double (&rl)[K]) {
@@ -68,22 +73,36 @@ __device__ __forceinline__ void load_diag(const LatticeParams& p, int64_t lp0, i
   for (int k = 0; k < K; ++k) {
     const int u = lane * K + k;
     const int t = d - u;
-    double xb = neg_inf(), xl = neg_inf();
-    if (t >= 0 && t < T && u <= U) {
-      const int64_t idx = lp0 + static_cast<int64_t>(t) * p.st + static_cast<int64_t>(u) * p.su;
-      if (IL) {
-        const double2 w = *reinterpret_cast<const double2*>(p.lp_blank + idx);
-        xb = w.x;
-        xl = w.y;
-      } else {
-        xb = p.lp_blank[idx];
-        if (u < U) xl = p.lp_label[idx];
-      }
-      if (u == U) xl = neg_inf();
+    const bool v = (t >= 0) && (t < T) && (u <= U);
+    const int64_t idx = v ? lp0 + static_cast<int64_t>(t) * p.st + static_cast<int64_t>(u) * p.su : lp0;
+    if (IL) {
+      const double2 w = *reinterpret_cast<const double2*>(p.lp_blank + idx);
+      rb[k] = w.x;
+      rl[k] = w.y;
+    } else {
+      rb[k] = p.lp_blank[idx];
+      rl[k] = p.lp_label[idx];
     }
-    rb[k] = xb;
-    rl[k] = xl;
   }
+}
+
+// Neighbour exchange along the wavefront: lane i receives lane i-1's value
+// (lane 0 receives `fill`), or lane i+1's (lane 63 receives `fill`), by DPP
+// whole-wave shifts.
+__device__ __forceinline__ double wave_shift_up(double x, double fill) {
+  const int lo = __builtin_amdgcn_update_dpp(static_cast<int>(__double2loint(fill)),
+                                             static_cast<int>(__double2loint(x)), 0x138, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(static_cast<int>(__double2hiint(fill)),
+                                             static_cast<int>(__double2hiint(x)), 0x138, 0xf, 0xf, false);
+  return __hiloint2double(hi, lo);
+}
+
+__device__ __forceinline__ double wave_shift_down(double x, double fill) {
+  const int lo = __builtin_amdgcn_update_dpp(static_cast<int>(__double2loint(fill)),
+                                             static_cast<int>(__double2loint(x)), 0x130, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(static_cast<int>(__double2hiint(fill)),
+                                             static_cast<int>(__double2hiint(x)), 0x130, 0xf, 0xf, false);
+  return __hiloint2double(hi, lo);
 }
 
 // IL: arc weights interleaved (lp_label == lp_blank + 1), read as one 16-byte load.
@@ -128,6 +147,7 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 512) void k2_lattice(Latti
   const int64_t ab0 = static_cast<int64_t>(b) * p.sab;
   const int variant = p.variant;
   const int owner_top = U / K;  // lane owning u = U
+  const int64_t dump = static_cast<int64_t>(p.T_max + p.U_max) * U1;  // scratch row after the last diagonal
 
   if (wave == 0) {
     // ---------------- forward sweep ----------------
@@ -143,30 +163,37 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 512) void k2_lattice(Latti
 #pragma unroll
     for (int s = 0; s < PF; ++s) load_diag<K, IL>(p, lp0, s, lane, T, U, rb[s], rl[s]);
 
+    // Whole blocks of PF steps with no branch around the loads or stores (a
+    // branch would make the wait counters unknown at the join and serialise
+    // the prefetch); the up to PF-1 steps past D only see invalid nodes.
     for (int d0 = 1; d0 <= D; d0 += PF) {
 #pragma unroll
       for (int s = 0; s < PF; ++s) {
         const int d = d0 + s;  // slot s holds the weights of diagonal d-1
-        if (d <= D) {
+        {
           double eb[K], el[K];
 #pragma unroll
           for (int k = 0; k < K; ++k) {
             eb[k] = a[k] + rb[s][k];
-            el[k] = a[k] + rl[s][k];
+            el[k] = (lane * K + k < U) ? a[k] + rl[s][k] : neg_inf();
           }
-          double left = __shfl_up(el[K - 1], 1);
-          if (lane == 0) left = neg_inf();
+          const double left = wave_shift_up(el[K - 1], neg_inf());
 #pragma unroll
           for (int k = 0; k < K; ++k) {
             const int u = lane * K + k;
             const int t = d - u;
             const bool v = (t >= 0) && (t < T) && (u <= U);
             double n = log_add(eb[k], k == 0 ? left : el[k > 0 ? k - 1 : 0]);
-            if (variant != 0 && u == 0 && t >= 1) n = log_add(n, 0.0);            // (0,0)->(t,0)
-            if (variant == 1 && u == U && t == T - 1) n = log_add(n, acc_top);      // (t',U)->(T-1,U)
+            // wild-card arcs into this node: (0,0)->(t,0) and (t',U)->(T-1,U)
+            const double extra = (variant != 0 && u == 0 && t >= 1) ? 0.0
+                                 : (variant == 1 && u == U && t == T - 1) ? acc_top : neg_inf();
+            if (extra != neg_inf()) n = log_add(n, extra);
             n = v ? n : neg_inf();
             a[k] = n;
-            if (MODE != kLossOnly && v) p.alpha[ab0 + static_cast<int64_t>(d) * U1 + u] = n;
+            // every lane stores (invalid nodes store -inf in place, lanes past
+            // U_max into the dump row) so no store sits under a branch
+            if (MODE != kLossOnly)
+              p.alpha[ab0 + (u <= p.U_max && d <= D ? static_cast<int64_t>(d) * U1 + u : dump)] = n;
             if (u == U && v) a_top = n;
             if (variant != 0 && u == U && v && t <= T - 2) acc_top = log_add(acc_top, n);
           }
@@ -204,13 +231,13 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 512) void k2_lattice(Latti
 #pragma unroll
     for (int s = 0; s < PF; ++s) load_diag<K, IL>(p, lp0, D - 1 - s, lane, T, U, rb[s], rl[s]);
 
+    double b00 = bv[0];  // beta(0,0) (lane 0); already final when D == 0
     for (int d0 = D - 1; d0 >= 0; d0 -= PF) {
 #pragma unroll
       for (int s = 0; s < PF; ++s) {
-        const int d = d0 - s;  // slot s holds the weights of diagonal d
-        if (d >= 0) {
-          double right = __shfl_down(bv[0], 1);
-          if (lane == kWave - 1) right = neg_inf();
+        const int d = d0 - s;  // slot s holds the weights of diagonal d (d < 0: no node)
+        {
+          const double right = wave_shift_down(bv[0], neg_inf());
           double nb[K];
 #pragma unroll
           for (int k = 0; k < K; ++k) {
@@ -218,17 +245,18 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 512) void k2_lattice(Latti
             const int t = d - u;
             const bool v = (t >= 0) && (t < T) && (u <= U);
             const double xb = rb[s][k] + bv[k];
-            const double xl = rl[s][k] + (k == K - 1 ? right : bv[k + 1 < K ? k + 1 : k]);
+            const double xl = (u < U) ? rl[s][k] + (k == K - 1 ? right : bv[k + 1 < K ? k + 1 : k]) : neg_inf();
             double n = log_add(xb, xl);
-            if (u == U && t < T - 1) {
-              if (variant == 1) n = log_add(n, b_top);  // (t,U)->(T-1,U)
-              if (variant == 2) n = log_add(n, 0.0);    // (t,U)->final
-            }
-            if (variant != 0 && u == 0 && t == 0) n = log_add(n, acc0);  // (0,0)->(t',0)
+            // wild-card arcs out of this node: (t,U)->(T-1,U) or (t,U)->final, and (0,0)->(t',0)
+            const double extra = (u == U && t < T - 1 && variant == 1) ? b_top
+                                 : (u == U && t < T - 1 && variant == 2) ? 0.0 : neg_inf();
+            if (extra != neg_inf()) n = log_add(n, extra);
+            if (variant != 0 && u == 0 && t == 0) n = log_add(n, acc0);
             n = v ? n : neg_inf();
             nb[k] = n;
-            if (v) p.beta[ab0 + static_cast<int64_t>(d) * U1 + u] = n;
+            p.beta[ab0 + (u <= p.U_max && d >= 0 ? static_cast<int64_t>(d) * U1 + u : dump)] = n;
             if (variant != 0 && u == 0 && v && t >= 1) acc0 = log_add(acc0, n);
+            if (u == 0 && d == 0) b00 = n;
           }
 #pragma unroll
           for (int k = 0; k < K; ++k) bv[k] = nb[k];
@@ -236,58 +264,85 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 512) void k2_lattice(Latti
         }
       }
     }
-    if (lane == 0) p.lnp_bwd[b] = bv[0];
+    if (lane == 0) p.lnp_bwd[b] = b00;
   }
 
   if (MODE == kLossOnly) return;
   __syncthreads();
 
   // ---------------- arc posteriors ----------------
+  // RB rows per thread are loaded before any is used (independent loads in
+  // flight); cells outside the utterance read node (0,0) and are discarded.
+  constexpr int RB = 4;
   const double lnP = p.lnp_fwd[b];
   const int rows = p.T_max * U1;
   const int64_t row0 = static_cast<int64_t>(b) * rows;
+  const double* __restrict__ alpha = p.alpha;
+  const double* __restrict__ beta = p.beta;
+  const int32_t* __restrict__ lab_b = p.labels ? p.labels + static_cast<int64_t>(b) * p.U_max : nullptr;
   if (MODE == kDenseOut && tid == 0) {
     if (p.loss_out) p.loss_out[b] = -lnP;
     if (p.loss_bwd_out) p.loss_bwd_out[b] = -p.lnp_bwd[b];
   }
-  for (int r = tid; r < rows; r += blockDim.x) {
-    const int t = r / U1;
-    const int u = r - t * U1;
-    const bool valid = (t < T) && (u <= U);
-    if (MODE == kRowRecords && !valid) {
-      p.rowinfo[row0 + r] = RowInfo{0.f, 0.f, 0.f, kZeroRow};
-      continue;
+  for (int rb0 = tid; rb0 < rows; rb0 += blockDim.x * RB) {
+    double al[RB], be_b[RB], be_l[RB], lpb[RB], lpl[RB];
+    float l2[RB];
+    int lab[RB];
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+      const int r = rb0 + i * blockDim.x;
+      const int t = r / U1;
+      const int u = r - t * U1;
+      const bool valid = (r < rows) && (t < T) && (u <= U);
+      const int d = t + u;
+      const int64_t ai = valid ? ab0 + static_cast<int64_t>(d) * U1 + u : ab0;
+      const int64_t bi_b = (valid && t < T - 1) ? ab0 + static_cast<int64_t>(d + 1) * U1 + u : ab0;
+      const int64_t bi_l = (valid && u < U) ? ab0 + static_cast<int64_t>(d + 1) * U1 + u + 1 : ab0;
+      const int64_t li = valid ? lp0 + static_cast<int64_t>(t) * p.st + static_cast<int64_t>(u) * p.su : lp0;
+      al[i] = alpha[ai];
+      be_b[i] = beta[bi_b];
+      be_l[i] = beta[bi_l];
+      if (IL) {
+        const double2 w = *reinterpret_cast<const double2*>(p.lp_blank + li);
+        lpb[i] = w.x;
+        lpl[i] = w.y;
+      } else {
+        lpb[i] = p.lp_blank[li];
+        lpl[i] = p.lp_label[li];
+      }
+      l2[i] = (MODE == kRowRecords) ? p.rowinfo[valid ? row0 + r : row0].lse2 : 0.f;
+      lab[i] = (lab_b != nullptr && U > 0) ? lab_b[u < U ? u : U - 1] : kNoLabel;
     }
-    if (!valid) continue;
-    const int d = t + u;
-    const double al = p.alpha[ab0 + static_cast<int64_t>(d) * U1 + u];
-    const int64_t li = lp0 + static_cast<int64_t>(t) * p.st + static_cast<int64_t>(u) * p.su;
-    double lpb, lpl;
-    if (IL) {
-      const double2 w = *reinterpret_cast<const double2*>(p.lp_blank + li);
-      lpb = w.x;
-      lpl = w.y;
-    } else {
-      lpb = p.lp_blank[li];
-      lpl = (u < U) ? p.lp_label[li] : neg_inf();
-    }
-    double xb = neg_inf(), xl = neg_inf();
-    if (t < T - 1) xb = al + lpb + p.beta[ab0 + static_cast<int64_t>(d + 1) * U1 + u] - lnP;
-    else if (u == U) xb = al + lpb - lnP;
-    if (u < U) xl = al + lpl + p.beta[ab0 + static_cast<int64_t>(d + 1) * U1 + u + 1] - lnP;
-    if (MODE == kRowRecords) {
-      RowInfo o;
-      o.lse2 = p.rowinfo[row0 + r].lse2;
-      o.occ_blank = fast_exp2(static_cast<float>(xb * kLog2eD));
-      o.occ_label = fast_exp2(static_cast<float>(xl * kLog2eD));
-      o.label = (u < U) ? p.labels[static_cast<int64_t>(b) * p.U_max + u] : kNoLabel;
-      p.rowinfo[row0 + r] = o;
-    } else {
-      const int64_t o = row0 + r;
-      if (p.alpha_out) p.alpha_out[o] = al;
-      if (p.beta_out) p.beta_out[o] = p.beta[ab0 + static_cast<int64_t>(d) * U1 + u];
-      if (p.occ_blank_out) p.occ_blank_out[o] = exp(xb);
-      if (p.occ_label_out) p.occ_label_out[o] = exp(xl);
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+      const int r = rb0 + i * blockDim.x;
+      if (r >= rows) break;
+      const int t = r / U1;
+      const int u = r - t * U1;
+      const bool valid = (t < T) && (u <= U);
+      if (MODE == kRowRecords && !valid) {
+        p.rowinfo[row0 + r] = RowInfo{0.f, 0.f, 0.f, kZeroRow};
+        continue;
+      }
+      if (!valid) continue;
+      double xb = neg_inf(), xl = neg_inf();
+      if (t < T - 1) xb = al[i] + lpb[i] + be_b[i] - lnP;
+      else if (u == U) xb = al[i] + lpb[i] - lnP;
+      if (u < U) xl = al[i] + lpl[i] + be_l[i] - lnP;
+      if (MODE == kRowRecords) {
+        RowInfo o;
+        o.lse2 = l2[i];
+        o.occ_blank = fast_exp2(static_cast<float>(xb * kLog2eD));
+        o.occ_label = fast_exp2(static_cast<float>(xl * kLog2eD));
+        o.label = (u < U) ? lab[i] : kNoLabel;
+        p.rowinfo[row0 + r] = o;
+      } else {
+        const int64_t o = row0 + r;
+        if (p.alpha_out) p.alpha_out[o] = al[i];
+        if (p.beta_out) p.beta_out[o] = beta[ab0 + static_cast<int64_t>(t + u) * U1 + u];
+        if (p.occ_blank_out) p.occ_blank_out[o] = exp(xb);
+        if (p.occ_label_out) p.occ_label_out[o] = exp(xl);
+      }
     }
   }
 }

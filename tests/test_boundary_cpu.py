@@ -57,10 +57,11 @@ def expected_workspace(B, T, U, V):
     a = lambda x: (x + 255) // 256 * 256  # noqa: E731
     rows = B * T * (U + 1)
     cells = B * (T + U) * (U + 1)
+    score_cells = B * (T + U + 1) * (U + 1)  # one scratch diagonal row per utterance
     o = a(rows * 16)
     o = a(o + cells * 16)
-    o = a(o + cells * 8)
-    o = a(o + cells * 8)
+    o = a(o + score_cells * 8)
+    o = a(o + score_cells * 8)
     return a(o + 2 * B * 8)
 
 

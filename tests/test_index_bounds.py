@@ -17,20 +17,21 @@ SHAPES = [(w.B, w.T_max, w.U_max, w.V, w.dtype) for w in WORKLOADS.values()] + [
     (5, 3, 64, 7, "bf16"), (2, 2, 127, 8, "f32")]
 
 
-def k1_group_lanes(V, epc):
+def k1_shape(V, epc):
     max_chunks = (epc - 1 + V + epc - 1) // epc
-    want = (max_chunks + 3) // 4
-    g = 8
-    while g < want and g < 64:
-        g <<= 1
-    return g
+    best, best_slots = (64, 5), 1 << 30
+    for g in (64, 32, 16, 8):
+        for nb in range(1, 6):
+            if g * nb >= max_chunks and g * nb < best_slots:
+                best, best_slots = (g, nb), g * nb
+    return best
 
 
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
 def test_populate_kernel_addresses(B, T, U, V, dt):
     epc = EPC[dt]
     n_elem = B * T * (U + 1) * V
-    G = k1_group_lanes(V, epc)
+    G, NB = k1_shape(V, epc)
     rows_per_block = (256 // G) * 4
     n_ublk = -(-(U + 1) // rows_per_block)
     blocks = B * T * n_ublk
@@ -44,9 +45,14 @@ def test_populate_kernel_addresses(B, T, U, V, dt):
         mis = e0 - c0 * epc
         nch = (mis + V + epc - 1) // epc
         last_chunk = c0 + nch - 1
-        # whole-chunk loads only when the chunk ends inside the tensor
         assert np.all(last_chunk * epc < n_elem)
         assert np.all(e0 + V <= n_elem)
+        # the chunk-load path runs only when every chunk of the row is whole; its
+        # clamped indices stay in [c0, c0 + nch)
+        fast = c0 + nch <= n_elem // epc
+        assert np.all(((c0 + nch) * epc <= n_elem)[fast])
+        # only the tensor's last row can take the element-wise path
+        assert np.all(row[~fast] == B * T * (U + 1) - 1)
     # lp written by diagonal: (b, t, u) -> 2*((t+u)*(U+1)+u) (+1) inside B*(T+U)*(U+1) double2
     sb, st, su = 2 * (T + U) * (U + 1), 2 * (U + 1), 2 * (U + 2)
     hi = (B - 1) * sb + (T - 1) * st + U * su + 1
@@ -92,9 +98,11 @@ def test_lattice_kernel_addresses(B, T, U, V, dt):
     U1 = U + 1
     K = next(k for k in (1, 2, 4, 8, 16) if U1 <= 64 * k)
     assert 64 * K >= U1
-    sab = (T + U) * U1
-    # alpha / beta at (b, d, u): d <= T-1+U, u <= U; beta also reads d+1 only for valid neighbours
+    sab = (T + U + 1) * U1
+    # alpha / beta at (b, d, u): d <= T-1+U, u <= U; lanes past U_max store to the scratch row
     hi = (B - 1) * sab + (T - 1 + U) * U1 + U
     assert hi < B * sab
+    dump = (B - 1) * sab + (T + U) * U1
+    assert dump < B * sab
     # the epilogue reads beta(t+1, u) for t < T-1 and beta(t, u+1) for u < U: diagonal <= T-1+U
     assert (T - 2 + 1 + U) <= T - 1 + U
