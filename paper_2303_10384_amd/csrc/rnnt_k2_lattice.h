@@ -185,8 +185,9 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 512) void k2_lattice(Latti
             const bool v = (t >= 0) && (t < T) && (u <= U);
             double n = log_add(eb[k], k == 0 ? left : el[k > 0 ? k - 1 : 0]);
             // wild-card arcs into this node: (0,0)->(t,0) and (t',U)->(T-1,U)
-            const double extra = (variant != 0 && u == 0 && t >= 1) ? 0.0
-                                 : (variant == 1 && u == U && t == T - 1) ? acc_top : neg_inf();
+            // (with U = 0 both reach (T-1, 0) and both count)
+            double extra = (variant != 0 && u == 0 && t >= 1) ? 0.0 : neg_inf();
+            if (variant == 1 && u == U && t == T - 1) extra = log_add(extra, acc_top);
             if (extra != neg_inf()) n = log_add(n, extra);
             n = v ? n : neg_inf();
             a[k] = n;
