@@ -56,15 +56,6 @@ __device__ __forceinline__ void merge_batch(const float (&x)[N], float& mloc, fl
   mloc = mn;
 }
 
-// Value of element `idx` of a register array (select chain, no dynamic index).
-template <int N>
-__device__ __forceinline__ float pick_reg(const float (&x)[N], int idx) {
-  float r = x[0];
-#pragma unroll
-  for (int i = 1; i < N; ++i) r = (idx == i) ? x[i] : r;
-  return r;
-}
-
 template <typename T, int G, int NB>
 __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
@@ -104,9 +95,10 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
     const int nch = (mis + p.V + EPC - 1) / EPC;
     const int y = s_label[u - u_begin];
     const bool y_ok = (y >= 0 && y < p.V);
-    // chunk / lane / register slot holding z[blank] and z[y]
-    const int kb_blank = (p.blank + mis) / EPC, kb_y = ((y_ok ? y : 0) + mis) / EPC;
-    float zb_loc = 0.f, zy_loc = 0.f;
+    // z[blank], z[y]: the same address in every lane of the group (one request,
+    // the line the row's chunk loads bring in), issued ahead of them
+    const float zb = ElemTraits<T>::load1(base + e0 + p.blank);
+    const float zy = ElemTraits<T>::load1(base + e0 + (y_ok ? y : 0));
 
     float mloc = kNegInf, sloc = 0.f;
     if (c0 + nch <= full_chunks) {
@@ -129,11 +121,6 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
             x[q * EPC + j] = (k < nch && v >= 0 && v < p.V) ? f[j] : kNegInf;
           }
         }
-        // the owner lane of this batch keeps z[blank] / z[y] (slot = chunk offset in batch)
-        if (kb_blank >= kb && kb_blank < kb + G * NB)
-          zb_loc = pick_reg<NB * EPC>(x, ((kb_blank - kb) / G) * EPC + (p.blank + mis) % EPC);
-        if (kb_y >= kb && kb_y < kb + G * NB)
-          zy_loc = pick_reg<NB * EPC>(x, ((kb_y - kb) / G) * EPC + ((y_ok ? y : 0) + mis) % EPC);
         merge_batch<NB * EPC>(x, mloc, sloc);
       }
     } else {
@@ -145,13 +132,9 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
           const int v = k * EPC + j - mis;
           x[j] = (v >= 0 && v < p.V) ? ElemTraits<T>::load1(base + e0 + v) : kNegInf;
         }
-        if (k == kb_blank) zb_loc = pick_reg<EPC>(x, (p.blank + mis) % EPC);
-        if (k == kb_y) zy_loc = pick_reg<EPC>(x, ((y_ok ? y : 0) + mis) % EPC);
         merge_batch<EPC>(x, mloc, sloc);
       }
     }
-    const float zb = __shfl(zb_loc, kb_blank % G, G);
-    const float zy = __shfl(zy_loc, kb_y % G, G);
 
     // group max, then every lane's partial sum rescaled to it and summed in float64
     float mg = mloc;
