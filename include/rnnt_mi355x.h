@@ -125,11 +125,12 @@ rnnt_status_t rnnt_loss(const void* logits, rnnt_shape_t shape, const int32_t* l
 /*
  * rnnt_loss that also records timing events on `stream`: events[0] before the
  * first kernel, events[1] after kernel 1 (log-normaliser and gather),
- * events[2] after kernel 2 (lattice scores and arc posteriors), events[3]
- * after kernel 3 (gradient; recorded right after events[2] when grad_out is
- * NULL).  `events` is a HOST array of 4 events created by the caller (for
- * example with hipEventCreate); NULL behaves exactly like rnnt_loss.  Used to
- * time each kernel in place (hipEventElapsedTime between consecutive events).
+ * events[2] after kernel 2 (forward / backward sweeps), events[3] after
+ * kernel 2b (arc posteriors), events[4] after kernel 3 (gradient); without a
+ * gradient, events[3] and events[4] follow events[2] directly.  `events` is a
+ * HOST array of 5 events created by the caller (for example with
+ * hipEventCreate); NULL behaves exactly like rnnt_loss.  Used to time each
+ * kernel in place (hipEventElapsedTime between consecutive events).
  */
 rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int32_t* labels,
                               const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,

@@ -124,7 +124,7 @@ def rnnt_loss(logits, labels, logit_lens, label_lens, blank=0, variant="rnnt", n
     logits (B, T_max, U_max+1, V) float32/bfloat16/float16 on the GPU; labels (B, U_max) int32;
     logit_lens, label_lens (B,) int32.  workspace: optional uint8 GPU tensor of at least
     loss_workspace_bytes(...) bytes; grad_out / loss_out: optional preallocated outputs;
-    events: optional ctypes array of 4 hipEvent_t recorded around the three kernels;
+    events: optional ctypes array of 5 hipEvent_t recorded around the kernels;
     grad_dtype: None (the logits' dtype) or torch.float32.
     """
     torch = _torch()
@@ -159,7 +159,7 @@ def rnnt_loss(logits, labels, logit_lens, label_lens, blank=0, variant="rnnt", n
     if events is None:
         st = lib.rnnt_loss(_ptr(logits), shape, _ptr(labels), _ptr(logit_lens), _ptr(label_lens), int(blank),
                            VARIANTS[variant], _ptr(loss), _ptr(grad), ws_ptr, ws_bytes, _stream_handle(dev))
-    else:  # host array of 4 hipEvent_t handles
+    else:  # host array of 5 hipEvent_t handles
         st = lib.rnnt_loss_timed(_ptr(logits), shape, _ptr(labels), _ptr(logit_lens), _ptr(label_lens),
                                  int(blank), VARIANTS[variant], _ptr(loss), _ptr(grad), ws_ptr, ws_bytes,
                                  _stream_handle(dev), events)

@@ -4,7 +4,6 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
-#include <cstring>
 
 #include "rnnt_mi355x.h"
 #include "rnnt_device.h"
@@ -19,8 +18,11 @@ constexpr int kMaxUnits1 = 1024;  // U_max + 1 handled by one wavefront (16 unit
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
-
 bool dtype_known(int dt) { return dt == RNNT_DTYPE_F32 || dt == RNNT_DTYPE_BF16 || dt == RNNT_DTYPE_F16; }
+
+bool variant_known(int v) {
+  return v == RNNT_VARIANT_RNNT || v == RNNT_VARIANT_WRNNT || v == RNNT_VARIANT_WRNNT_ALLOW_IGNORE;
+}
 
 rnnt_status_t check_shape(const rnnt_shape_t& s) {
   if (s.B < 1 || s.T_max < 1 || s.U_max < 0 || s.V < 2) return RNNT_ERR_BAD_SHAPE;
@@ -34,60 +36,51 @@ rnnt_status_t check_shape(const rnnt_shape_t& s) {
   return RNNT_OK;
 }
 
-// Workspace of rnnt_loss, all pieces 256-byte aligned:
-//   rowinfo  (B*T_max*(U_max+1)) RowInfo
-//   lp       (B, T_max+U_max, U_max+1) double2 {lp_blank, lp_label}, indexed by diagonal
-//   alpha    (B, T_max+U_max+1, U_max+1) double, indexed by diagonal (last row: scratch)
-//   beta     same
+// Workspace, all pieces 256-byte aligned (C = B * (T_max+U_max) * (U_max+1)
+// anti-diagonal cells, S = B * (T_max+U_max+1) * (U_max+1) score cells):
+//   rowinfo  B*T_max*(U_max+1) RowInfo        (rnnt_loss)
+//   lp2      C double2 {lp_blank, lp_label}    (rnnt_loss)
+//   lse2     C float                           (rnnt_loss)
+//   alpha    S double
+//   beta     S double
 //   lnp      2*B double
-struct LossLayout {
-  size_t rowinfo, lp, alpha, beta, lnp, total;
+//   status   B int32
+struct Layout {
+  size_t rowinfo, lp2, lse2, alpha, beta, lnp, status, total;
 };
 
-LossLayout loss_layout(const rnnt_shape_t& s) {
-  const size_t rows = static_cast<size_t>(s.B) * s.T_max * (s.U_max + 1);
-  const size_t cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max) * (s.U_max + 1);
-  const size_t score_cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max + 1) * (s.U_max + 1);
-  LossLayout L{};
+Layout make_layout(const rnnt_shape_t& s, bool with_populate) {
+  const size_t U1 = static_cast<size_t>(s.U_max) + 1;
+  const size_t rows = static_cast<size_t>(s.B) * s.T_max * U1;
+  const size_t cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max) * U1;
+  const size_t score_cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max + 1) * U1;
+  Layout L{};
   size_t o = 0;
-  L.rowinfo = o;
-  o = align256(o + rows * sizeof(RowInfo));
-  L.lp = o;
-  o = align256(o + cells * 2 * sizeof(double));
+  if (with_populate) {
+    L.rowinfo = o;
+    o = align256(o + rows * sizeof(RowInfo));
+    L.lp2 = o;
+    o = align256(o + cells * 2 * sizeof(double));
+    L.lse2 = o;
+    o = align256(o + cells * sizeof(float));
+  }
   L.alpha = o;
   o = align256(o + score_cells * sizeof(double));
   L.beta = o;
   o = align256(o + score_cells * sizeof(double));
   L.lnp = o;
   o = align256(o + 2 * static_cast<size_t>(s.B) * sizeof(double));
-  L.total = o;
-  return L;
-}
-
-// Workspace of rnnt_lattice_scores: alpha, beta (diagonal-indexed) and lnp.
-struct LatticeLayout {
-  size_t alpha, beta, lnp, total;
-};
-
-LatticeLayout lattice_layout(const rnnt_shape_t& s) {
-  const size_t cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max + 1) * (s.U_max + 1);
-  LatticeLayout L{};
-  size_t o = 0;
-  L.alpha = o;
-  o = align256(o + cells * sizeof(double));
-  L.beta = o;
-  o = align256(o + cells * sizeof(double));
-  L.lnp = o;
-  o = align256(o + 2 * static_cast<size_t>(s.B) * sizeof(double));
+  L.status = o;
+  o = align256(o + static_cast<size_t>(s.B) * sizeof(int32_t));
   L.total = o;
   return L;
 }
 
 // ---- kernel 1 ---------------------------------------------------------------
 
-// Lanes per row G and chunks per lane NB for kernel 1: the smallest G*NB
-// that covers a row's chunks (NB <= 5 keeps the batch in registers); rows
-// longer than 64*5 chunks take several batches.
+// Lanes per row G and chunks per lane NB: the smallest G*NB that covers a
+// row's chunks (NB <= 5 keeps the batch in registers); rows longer than 64*5
+// chunks take several batches.
 struct K1Shape {
   int G, NB;
 };
@@ -110,65 +103,84 @@ K1Shape k1_shape(int V) {
   return best;
 }
 
-template <typename T, int G, int NB>
+template <typename T, int G, int NB, bool LATTICE>
 hipError_t launch_k1_g(PopulateParams p, hipStream_t stream) {
   constexpr int groups = 256 / G;
   p.rows_per_block = groups * 4;
   p.n_ublk = (p.U_max + 1 + p.rows_per_block - 1) / p.rows_per_block;
-  const int64_t blocks = static_cast<int64_t>(p.B) * p.T_max * p.n_ublk;
+  const int64_t blocks = static_cast<int64_t>(p.B) * (p.T_max + p.U_max) * p.n_ublk;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((k1_populate<T, G, NB>), dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, stream, p);
+  hipLaunchKernelGGL((k1_populate<T, G, NB, LATTICE>), dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, stream,
+                     p);
   return hipGetLastError();
 }
 
-template <typename T, int G>
+template <typename T, int G, bool LATTICE>
 hipError_t launch_k1_nb(int nb, const PopulateParams& p, hipStream_t stream) {
   switch (nb) {
-    case 1: return launch_k1_g<T, G, 1>(p, stream);
-    case 2: return launch_k1_g<T, G, 2>(p, stream);
-    case 3: return launch_k1_g<T, G, 3>(p, stream);
-    case 4: return launch_k1_g<T, G, 4>(p, stream);
-    default: return launch_k1_g<T, G, 5>(p, stream);
+    case 1: return launch_k1_g<T, G, 1, LATTICE>(p, stream);
+    case 2: return launch_k1_g<T, G, 2, LATTICE>(p, stream);
+    case 3: return launch_k1_g<T, G, 3, LATTICE>(p, stream);
+    case 4: return launch_k1_g<T, G, 4, LATTICE>(p, stream);
+    default: return launch_k1_g<T, G, 5, LATTICE>(p, stream);
   }
 }
 
-template <typename T>
+template <typename T, bool LATTICE>
 hipError_t launch_k1(const PopulateParams& p, hipStream_t stream) {
   const K1Shape ks = k1_shape<T>(p.V);
   switch (ks.G) {
-    case 8: return launch_k1_nb<T, 8>(ks.NB, p, stream);
-    case 16: return launch_k1_nb<T, 16>(ks.NB, p, stream);
-    case 32: return launch_k1_nb<T, 32>(ks.NB, p, stream);
-    default: return launch_k1_nb<T, 64>(ks.NB, p, stream);
+    case 8: return launch_k1_nb<T, 8, LATTICE>(ks.NB, p, stream);
+    case 16: return launch_k1_nb<T, 16, LATTICE>(ks.NB, p, stream);
+    case 32: return launch_k1_nb<T, 32, LATTICE>(ks.NB, p, stream);
+    default: return launch_k1_nb<T, 64, LATTICE>(ks.NB, p, stream);
   }
 }
 
+template <bool LATTICE>
 hipError_t launch_k1_dtype(rnnt_dtype_t dt, const PopulateParams& p, hipStream_t stream) {
   switch (dt) {
-    case RNNT_DTYPE_F32: return launch_k1<float>(p, stream);
-    case RNNT_DTYPE_BF16: return launch_k1<bf16_t>(p, stream);
-    default: return launch_k1<f16_t>(p, stream);
+    case RNNT_DTYPE_F32: return launch_k1<float, LATTICE>(p, stream);
+    case RNNT_DTYPE_BF16: return launch_k1<bf16_t, LATTICE>(p, stream);
+    default: return launch_k1<f16_t, LATTICE>(p, stream);
   }
 }
 
 // ---- kernel 2 ---------------------------------------------------------------
 
-template <int K, int MODE, bool IL>
+template <int K, int VAR, int MODE, bool DENSE_IN>
 hipError_t launch_k2_k(const LatticeParams& p, hipStream_t stream) {
-  constexpr int PF = (K >= 16) ? 1 : (32 / K);  // weights of PF diagonals in flight per lane
-  const int threads = (MODE == kLossOnly) ? 64 : 512;
-  hipLaunchKernelGGL((k2_lattice<K, PF, MODE, IL>), dim3(p.B), dim3(threads), 0, stream, p);
+  constexpr int PF = (K >= 16) ? 2 : (48 / K > 24 ? 24 : 48 / K);  // diagonals of weights in flight
+  const int threads = (MODE == kLossOnly) ? 64 : 128;
+  hipLaunchKernelGGL((k2_lattice<K, PF, VAR, MODE, DENSE_IN>), dim3(p.B), dim3(threads), 0, stream, p);
   return hipGetLastError();
 }
 
-template <int MODE, bool IL>
-hipError_t launch_k2(const LatticeParams& p, hipStream_t stream) {
+template <int VAR, int MODE, bool DENSE_IN>
+hipError_t launch_k2_v(const LatticeParams& p, hipStream_t stream) {
   const int units1 = p.U_max + 1;
-  if (units1 <= 64) return launch_k2_k<1, MODE, IL>(p, stream);
-  if (units1 <= 128) return launch_k2_k<2, MODE, IL>(p, stream);
-  if (units1 <= 256) return launch_k2_k<4, MODE, IL>(p, stream);
-  if (units1 <= 512) return launch_k2_k<8, MODE, IL>(p, stream);
-  return launch_k2_k<16, MODE, IL>(p, stream);
+  if (units1 <= 64) return launch_k2_k<1, VAR, MODE, DENSE_IN>(p, stream);
+  if (units1 <= 128) return launch_k2_k<2, VAR, MODE, DENSE_IN>(p, stream);
+  if (units1 <= 256) return launch_k2_k<4, VAR, MODE, DENSE_IN>(p, stream);
+  if (units1 <= 512) return launch_k2_k<8, VAR, MODE, DENSE_IN>(p, stream);
+  return launch_k2_k<16, VAR, MODE, DENSE_IN>(p, stream);
+}
+
+template <int MODE, bool DENSE_IN>
+hipError_t launch_k2(int variant, const LatticeParams& p, hipStream_t stream) {
+  switch (variant) {
+    case RNNT_VARIANT_RNNT: return launch_k2_v<0, MODE, DENSE_IN>(p, stream);
+    case RNNT_VARIANT_WRNNT: return launch_k2_v<1, MODE, DENSE_IN>(p, stream);
+    default: return launch_k2_v<2, MODE, DENSE_IN>(p, stream);
+  }
+}
+
+template <bool DENSE>
+hipError_t launch_k2b(const PostParams& p, hipStream_t stream) {
+  const int64_t blocks = (p.n_rows + kPostThreads - 1) / kPostThreads;
+  if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL((k2b_posteriors<DENSE>), dim3(static_cast<uint32_t>(blocks)), dim3(kPostThreads), 0, stream, p);
+  return hipGetLastError();
 }
 
 // ---- kernel 3 ---------------------------------------------------------------
@@ -208,6 +220,19 @@ struct Scratch {
   }
 };
 
+rnnt_status_t take_workspace(void* workspace, size_t workspace_bytes, size_t need, hipStream_t stream,
+                             Scratch& scratch, char** ws) {
+  if (workspace && workspace_bytes < need) return RNNT_ERR_WORKSPACE;
+  if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u)) return RNNT_ERR_ALIGNMENT;
+  *ws = static_cast<char*>(workspace);
+  if (!*ws) {
+    if (hipMallocAsync(&scratch.ptr, need, stream) != hipSuccess) return RNNT_ERR_HIP;
+    scratch.stream = stream;
+    *ws = static_cast<char*>(scratch.ptr);
+  }
+  return RNNT_OK;
+}
+
 }  // namespace
 }  // namespace rnnt
 
@@ -224,18 +249,18 @@ const char* rnnt_status_string(rnnt_status_t status) {
     case RNNT_ERR_BAD_DTYPE: return "unknown dtype, or grad_dtype neither dtype nor F32";
     case RNNT_ERR_BAD_VARIANT: return "unknown variant";
     case RNNT_ERR_WORKSPACE: return "workspace smaller than required";
-    case RNNT_ERR_ALIGNMENT: return "logits / grad must be 16-byte aligned";
+    case RNNT_ERR_ALIGNMENT: return "logits / grad must be 16-byte aligned, workspace 256-byte aligned";
     case RNNT_ERR_HIP: return "HIP runtime error";
     case RNNT_ERR_UNSUPPORTED: return "unsupported shape (U_max + 1 > 1024)";
   }
   return "unknown status";
 }
 
-const char* rnnt_version(void) { return "rnnt_mi355x 0.1.0 gfx950"; }
+const char* rnnt_version(void) { return "rnnt_mi355x 0.2.0 gfx950"; }
 
 size_t rnnt_loss_workspace_bytes(rnnt_shape_t shape) {
   if (check_shape(shape) != RNNT_OK) return 0;
-  return loss_layout(shape).total;
+  return make_layout(shape, true).total;
 }
 
 size_t rnnt_lattice_workspace_bytes(rnnt_shape_t shape) {
@@ -243,7 +268,7 @@ size_t rnnt_lattice_workspace_bytes(rnnt_shape_t shape) {
   s.dtype = RNNT_DTYPE_F32;
   s.grad_dtype = RNNT_DTYPE_F32;
   if (check_shape(s) != RNNT_OK) return 0;
-  return lattice_layout(s).total;
+  return make_layout(s, false).total;
 }
 
 rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int32_t* labels,
@@ -255,32 +280,23 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
   if (!logits || !logit_lens || !label_lens || !loss_out || (!labels && shape.U_max > 0))
     return RNNT_ERR_NULL_PTR;
   if (blank < 0 || blank >= shape.V) return RNNT_ERR_BAD_BLANK;
-  if (variant != RNNT_VARIANT_RNNT && variant != RNNT_VARIANT_WRNNT && variant != RNNT_VARIANT_WRNNT_ALLOW_IGNORE)
-    return RNNT_ERR_BAD_VARIANT;
+  if (!variant_known(variant)) return RNNT_ERR_BAD_VARIANT;
   if (!aligned16(logits) || (grad_out && !aligned16(grad_out))) return RNNT_ERR_ALIGNMENT;
   if (shape.U_max + 1 > kMaxUnits1) return RNNT_ERR_UNSUPPORTED;
-  const LossLayout L = loss_layout(shape);
-  if (workspace && workspace_bytes < L.total) return RNNT_ERR_WORKSPACE;
-  if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u)) return RNNT_ERR_ALIGNMENT;
-
+  const Layout L = make_layout(shape, true);
   Scratch scratch;
-  char* ws = static_cast<char*>(workspace);
-  if (!ws) {
-    if (hipMallocAsync(&scratch.ptr, L.total, stream) != hipSuccess) return RNNT_ERR_HIP;
-    scratch.stream = stream;
-    ws = static_cast<char*>(scratch.ptr);
-  }
-  RowInfo* rowinfo = reinterpret_cast<RowInfo*>(ws + L.rowinfo);
-  double* lp = reinterpret_cast<double*>(ws + L.lp);
+  char* ws = nullptr;
+  st = take_workspace(workspace, workspace_bytes, L.total, stream, scratch, &ws);
+  if (st != RNNT_OK) return st;
+
   const int64_t U1 = shape.U_max + 1;
   const int64_t n_rows = static_cast<int64_t>(shape.B) * shape.T_max * U1;
   const int64_t n_elem = n_rows * shape.V;
   const bool need_grad = grad_out != nullptr;
-
   auto mark = [&](int i) { return events ? hipEventRecord(events[i], stream) : hipSuccess; };
   if (mark(0) != hipSuccess) return RNNT_ERR_HIP;
 
-  // kernel 1: lse and arc weights; lp is stored by diagonal, interleaved
+  // kernel 1: lse and arc weights in the lattice form
   PopulateParams p1{};
   p1.logits = logits;
   p1.B = shape.B;
@@ -292,56 +308,68 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
   p1.logit_lens = logit_lens;
   p1.label_lens = label_lens;
   p1.n_elem = n_elem;
-  p1.rowinfo = need_grad ? rowinfo : nullptr;
-  p1.lp_blank = lp;
-  p1.lp_label = lp + 1;
-  p1.sb = 2 * static_cast<int64_t>(shape.T_max + shape.U_max) * U1;
-  p1.st = 2 * U1;        // (t, u) -> diagonal (t+u), unit u: (t+u)*U1 + u
-  p1.su = 2 * (U1 + 1);
-  p1.lse_out = nullptr;
-  if (launch_k1_dtype(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
+  p1.lp2 = reinterpret_cast<double2*>(ws + L.lp2);
+  p1.lse2 = reinterpret_cast<float*>(ws + L.lse2);
+  if (launch_k1_dtype<true>(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(1) != hipSuccess) return RNNT_ERR_HIP;
 
-  // kernel 2: forward / backward scores and arc posteriors
+  // kernel 2: forward / backward sweeps
   LatticeParams p2{};
   p2.B = shape.B;
   p2.T_max = shape.T_max;
   p2.U_max = shape.U_max;
   p2.V = shape.V;
   p2.blank = blank;
-  p2.variant = static_cast<int32_t>(variant);
   p2.labels = labels;
   p2.logit_lens = logit_lens;
   p2.label_lens = label_lens;
-  p2.lp_blank = lp;
-  p2.lp_label = lp + 1;
-  p2.sb = p1.sb;
-  p2.st = p1.st;
-  p2.su = p1.su;
+  p2.lp2 = p1.lp2;
   p2.alpha = reinterpret_cast<double*>(ws + L.alpha);
   p2.beta = reinterpret_cast<double*>(ws + L.beta);
-  p2.sab = static_cast<int64_t>(shape.T_max + shape.U_max + 1) * U1;
-  p2.lnp_fwd = reinterpret_cast<double*>(ws + L.lnp);
-  p2.lnp_bwd = p2.lnp_fwd + shape.B;
+  p2.lnp2_fwd = reinterpret_cast<double*>(ws + L.lnp);
+  p2.lnp2_bwd = p2.lnp2_fwd + shape.B;
+  p2.status = reinterpret_cast<int32_t*>(ws + L.status);
   p2.loss_f32 = loss_out;
-  p2.rowinfo = rowinfo;
-  hipError_t e = need_grad ? launch_k2<kRowRecords, true>(p2, stream) : launch_k2<kLossOnly, true>(p2, stream);
-  if (e != hipSuccess) return RNNT_ERR_HIP;
+  const hipError_t e2 = need_grad ? launch_k2<kScores, false>(variant, p2, stream)
+                                  : launch_k2<kLossOnly, false>(variant, p2, stream);
+  if (e2 != hipSuccess) return RNNT_ERR_HIP;
   if (mark(2) != hipSuccess) return RNNT_ERR_HIP;
 
-  // kernel 3: gradient
   if (need_grad) {
+    // kernel 2b: arc posteriors -> row records
+    PostParams pb{};
+    pb.B = shape.B;
+    pb.T_max = shape.T_max;
+    pb.U_max = shape.U_max;
+    pb.labels = labels;
+    pb.logit_lens = logit_lens;
+    pb.label_lens = label_lens;
+    pb.status = p2.status;
+    pb.lp2 = p1.lp2;
+    pb.lse2 = p1.lse2;
+    pb.alpha = p2.alpha;
+    pb.beta = p2.beta;
+    pb.lnp2_fwd = p2.lnp2_fwd;
+    pb.lnp2_bwd = p2.lnp2_bwd;
+    pb.n_rows = n_rows;
+    pb.rowinfo = reinterpret_cast<RowInfo*>(ws + L.rowinfo);
+    if (launch_k2b<false>(pb, stream) != hipSuccess) return RNNT_ERR_HIP;
+  }
+  if (mark(3) != hipSuccess) return RNNT_ERR_HIP;
+
+  if (need_grad) {
+    // kernel 3: gradient
     GradParams p3{};
     p3.logits = logits;
     p3.grad = grad_out;
-    p3.rowinfo = rowinfo;
+    p3.rowinfo = reinterpret_cast<RowInfo*>(ws + L.rowinfo);
     p3.n_elem = n_elem;
     p3.n_rows = n_rows;
     p3.V = shape.V;
     p3.blank = blank;
     if (launch_k3_dtype(shape.dtype, shape.grad_dtype, p3, stream) != hipSuccess) return RNNT_ERR_HIP;
   }
-  if (mark(3) != hipSuccess) return RNNT_ERR_HIP;
+  if (mark(4) != hipSuccess) return RNNT_ERR_HIP;
   return RNNT_OK;
 }
 
@@ -375,14 +403,10 @@ rnnt_status_t rnnt_log_softmax_gather(const void* logits, rnnt_shape_t shape, co
   p1.logit_lens = logit_lens;
   p1.label_lens = label_lens;
   p1.n_elem = static_cast<int64_t>(shape.B) * shape.T_max * U1 * shape.V;
-  p1.rowinfo = nullptr;
-  p1.lp_blank = lp_blank_out;
-  p1.lp_label = lp_label_out;
-  p1.sb = static_cast<int64_t>(shape.T_max) * U1;
-  p1.st = U1;
-  p1.su = 1;
   p1.lse_out = lse_out;
-  return launch_k1_dtype(shape.dtype, p1, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
+  p1.lp_blank_out = lp_blank_out;
+  p1.lp_label_out = lp_label_out;
+  return launch_k1_dtype<false>(shape.dtype, p1, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
 }
 
 rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label, rnnt_shape_t shape,
@@ -397,48 +421,55 @@ rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label
   rnnt_status_t st = check_shape(s);
   if (st != RNNT_OK) return st;
   if (!lp_blank || !lp_label || !logit_lens || !label_lens) return RNNT_ERR_NULL_PTR;
-  if (variant != RNNT_VARIANT_RNNT && variant != RNNT_VARIANT_WRNNT && variant != RNNT_VARIANT_WRNNT_ALLOW_IGNORE)
-    return RNNT_ERR_BAD_VARIANT;
+  if (!variant_known(variant)) return RNNT_ERR_BAD_VARIANT;
   if (s.U_max + 1 > kMaxUnits1) return RNNT_ERR_UNSUPPORTED;
-  const LatticeLayout L = lattice_layout(s);
-  if (workspace && workspace_bytes < L.total) return RNNT_ERR_WORKSPACE;
-  if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u)) return RNNT_ERR_ALIGNMENT;
+  const Layout L = make_layout(s, false);
   Scratch scratch;
-  char* ws = static_cast<char*>(workspace);
-  if (!ws) {
-    if (hipMallocAsync(&scratch.ptr, L.total, stream) != hipSuccess) return RNNT_ERR_HIP;
-    scratch.stream = stream;
-    ws = static_cast<char*>(scratch.ptr);
-  }
-  const int64_t U1 = s.U_max + 1;
+  char* ws = nullptr;
+  st = take_workspace(workspace, workspace_bytes, L.total, stream, scratch, &ws);
+  if (st != RNNT_OK) return st;
+
   LatticeParams p2{};
   p2.B = s.B;
   p2.T_max = s.T_max;
   p2.U_max = s.U_max;
   p2.V = s.V;
   p2.blank = 0;
-  p2.variant = static_cast<int32_t>(variant);
   p2.labels = nullptr;
   p2.logit_lens = logit_lens;
   p2.label_lens = label_lens;
   p2.lp_blank = lp_blank;
   p2.lp_label = lp_label;
-  p2.sb = static_cast<int64_t>(s.T_max) * U1;
-  p2.st = U1;
-  p2.su = 1;
   p2.alpha = reinterpret_cast<double*>(ws + L.alpha);
   p2.beta = reinterpret_cast<double*>(ws + L.beta);
-  p2.sab = static_cast<int64_t>(s.T_max + s.U_max + 1) * U1;
-  p2.lnp_fwd = reinterpret_cast<double*>(ws + L.lnp);
-  p2.lnp_bwd = p2.lnp_fwd + s.B;
+  p2.lnp2_fwd = reinterpret_cast<double*>(ws + L.lnp);
+  p2.lnp2_bwd = p2.lnp2_fwd + s.B;
+  p2.status = reinterpret_cast<int32_t*>(ws + L.status);
   p2.loss_f32 = nullptr;
-  p2.alpha_out = alpha_out;
-  p2.beta_out = beta_out;
-  p2.occ_blank_out = occ_blank_out;
-  p2.occ_label_out = occ_label_out;
-  p2.loss_out = loss_out;
-  p2.loss_bwd_out = loss_bwd_out;
-  return launch_k2<kDenseOut, false>(p2, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
+  if (launch_k2<kScores, true>(variant, p2, stream) != hipSuccess) return RNNT_ERR_HIP;
+
+  PostParams pb{};
+  pb.B = s.B;
+  pb.T_max = s.T_max;
+  pb.U_max = s.U_max;
+  pb.labels = nullptr;
+  pb.logit_lens = logit_lens;
+  pb.label_lens = label_lens;
+  pb.status = p2.status;
+  pb.lp_blank = lp_blank;
+  pb.lp_label = lp_label;
+  pb.alpha = p2.alpha;
+  pb.beta = p2.beta;
+  pb.lnp2_fwd = p2.lnp2_fwd;
+  pb.lnp2_bwd = p2.lnp2_bwd;
+  pb.n_rows = static_cast<int64_t>(s.B) * s.T_max * (s.U_max + 1);
+  pb.alpha_out = alpha_out;
+  pb.beta_out = beta_out;
+  pb.occ_blank_out = occ_blank_out;
+  pb.occ_label_out = occ_label_out;
+  pb.loss_out = loss_out;
+  pb.loss_bwd_out = loss_bwd_out;
+  return launch_k2b<true>(pb, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
 }
 
 }  // extern "C"

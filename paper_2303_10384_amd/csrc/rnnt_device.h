@@ -12,7 +12,7 @@ constexpr float kLn2F = 0.6931471805599453f;
 constexpr double kLog2eD = 1.4426950408889634;
 constexpr int kWave = 64;
 
-// Per-row record handed from the lattice kernel to the gradient kernel.
+// Per-row record handed from the posterior kernel to the gradient kernel.
 // lse2 = ln(sum_v exp z_v) * log2(e); occ_* are the blank / label arc
 // posteriors leaving the row's node; label is y_{u+1}, or kNoLabel on the top
 // row, or kZeroRow for rows whose gradient is identically zero (padding, bad
@@ -26,25 +26,25 @@ struct __attribute__((aligned(16))) RowInfo {
 constexpr int32_t kNoLabel = -1;
 constexpr int32_t kZeroRow = -2;
 
-__device__ __forceinline__ double neg_inf() { return -__builtin_inf(); }
+// Lattice scores are kept in log2 units (x * log2 e).  An absent arc, and a
+// node that no path reaches, carry kNoArc: finite, so sums and maxima never
+// meet -inf - -inf, and so far below any real score that it is exactly
+// absorbed by them (kNoArc + any score of magnitude < 1e284 == kNoArc).
+constexpr double kNoArc = -0x1p+1000;
 
 // exp2 / log2 on the transcendental unit (v_exp_f32 / v_log_f32, ~1 ulp).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
-// ln(e^x + e^y) with float64 operands and result.  The correction term
-// ln(1 + e^-|x-y|) lies in [0, ln 2] and is formed in float32 (absolute error
-// ~1e-7), so long chains of additions keep float64 accuracy on the large
-// magnitudes.  Two -inf operands give -inf; a NaN operand gives NaN.
-__device__ __forceinline__ double log_add(double x, double y) {
-  const bool xg = x > y;
-  const double m = xg ? x : y;
-  const double n = xg ? y : x;
-  const float d = static_cast<float>(n - m);          // <= 0, -inf or NaN
-  const float e = fast_exp2(d * kLog2eF);             // e^{n-m} in [0, 1]
-  const float c = fast_log2(1.0f + e) * kLn2F;        // ln(1 + e)
-  const double r = m + static_cast<double>(c);
-  return (m == neg_inf()) ? m : r;
+// log2(2^x + 2^y) with float64 operands and result.  The correction term
+// log2(1 + 2^-|x-y|) lies in [0, 1] and is formed in float32 (absolute error
+// ~1e-7), so the long chains of float64 additions keep their accuracy.  A NaN
+// operand gives NaN (|x-y| is NaN); two kNoArc operands give kNoArc.
+__device__ __forceinline__ double log_add2(double x, double y) {
+  const double m = __builtin_fmax(x, y);
+  const float d = static_cast<float>(x - y);
+  const float c = fast_log2(1.0f + fast_exp2(-__builtin_fabsf(d)));
+  return m + static_cast<double>(c);
 }
 
 // ---- element types: 16-byte chunks of logits / gradient -------------------

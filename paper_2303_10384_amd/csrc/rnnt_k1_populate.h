@@ -3,20 +3,29 @@
 // Populate (Section 2.2) selects every arc weight of the grid lattice (Fig. 1)
 // from X = log_softmax(logits) by (time, unit_idx, label).  One pass over each
 // valid logits row (t < T_b, u <= U_b) computes lse = ln sum_v exp z_v and
-// emits only what the lattice needs:
-//   lp_blank(t, u) = z[blank] - lse,  lp_label(t, u) = z[y_{u+1}] - lse
-// (float64, formed from the exact input value), plus lse * log2(e) as float32
-// for the gradient kernel.  Padding rows are never touched.
+// emits only what the lattice needs, formed in float64 from the exact input:
+//   lp_blank(t, u) = z[blank] - lse,  lp_label(t, u) = z[y_{u+1}] - lse.
+// Padding rows are never touched.
 //
-// Mapping: a block owns `rows_per_block` consecutive rows u of one (b, t)
-// segment; a group of G lanes reads one row as aligned 16-byte chunks, NB
-// chunks per lane per batch (G and NB are picked from V so that G*NB just
+// Two output forms:
+//  * LATTICE (the fused loss): arc weights in log2 units, stored as
+//    {lp_blank, lp_label} pairs by anti-diagonal (cell (t, u) of utterance b at
+//    (b*(T_max+U_max) + t+u)*(U_max+1) + u), where the lattice kernel reads a
+//    diagonal as one contiguous run; absent arcs (the label arc of the top row,
+//    the blank arcs of the last frame below the top row) carry kNoArc; plus
+//    lse * log2(e) as float32 at the same index.
+//  * dense natural-log lse / lp_blank / lp_label, (B, T_max, U_max+1) float64
+//    (the populate step on its own).
+//
+// Mapping: a block owns up to `rows_per_block` consecutive units u of one
+// anti-diagonal d of one utterance, so the lattice-form writes of a block are
+// one contiguous run; a group of G lanes reads one row as aligned 16-byte
+// chunks, NB chunks per lane per batch (G, NB picked from V so that G*NB just
 // covers a row).  All loads of a batch are issued unconditionally (chunk index
-// clamped into the row) before any value is touched, and the elements outside
-// the row are masked afterwards, so a row's loads are in flight together.  The
-// group reduces max, then sum of exp in float32 per lane and float64 across
-// lanes.  A row whose last chunk runs past the end of the tensor (only the
-// tensor's last row can) takes an element-wise path.
+// clamped into the row) before any value is touched, and elements outside the
+// row are masked afterwards.  The group reduces max, then sum of exp in
+// float32 per lane and float64 across lanes.  A row whose last chunk runs past
+// the end of the tensor (only the tensor's last row can) reads element-wise.
 #pragma once
 
 #include "rnnt_device.h"
@@ -30,13 +39,15 @@ struct PopulateParams {
   const int32_t* logit_lens;
   const int32_t* label_lens;
   int64_t n_elem;          // B * T_max * (U_max+1) * V
-  int32_t n_ublk;          // blocks per (b, t) segment
-  int32_t rows_per_block;  // consecutive rows u per block
-  RowInfo* rowinfo;        // row records (lse2 filled here) or null
-  double* lp_blank;        // element (b,t,u) at b*sb + t*st + u*su (in doubles)
-  double* lp_label;
-  int64_t sb, st, su;
-  double* lse_out;         // dense (B, T_max, U_max+1) or null
+  int32_t n_ublk;          // blocks per anti-diagonal
+  int32_t rows_per_block;  // consecutive units u per block
+  // lattice form
+  double2* lp2;            // (B, T_max+U_max, U_max+1) {lp_blank, lp_label} * log2(e)
+  float* lse2;             // same index: lse * log2(e)
+  // dense form
+  double* lse_out;         // (B, T_max, U_max+1) or null
+  double* lp_blank_out;
+  double* lp_label_out;
 };
 
 // (max, sum of exp) of one batch of register-held values, merged into the
@@ -56,7 +67,9 @@ __device__ __forceinline__ void merge_batch(const float (&x)[N], float& mloc, fl
   mloc = mn;
 }
 
-template <typename T, int G, int NB>
+__device__ __forceinline__ double clamp_no_arc(double x) { return x < kNoArc ? kNoArc : x; }  // NaN stays NaN
+
+template <typename T, int G, int NB, bool LATTICE>
 __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
   constexpr int GROUPS = 256 / G;      // rows in flight per block
@@ -64,21 +77,24 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   const float kNegInf = -__builtin_inff();
   __shared__ int s_label[MAX_ROWS];
 
-  const int seg = blockIdx.x / p.n_ublk;  // b * T_max + t
-  const int ublk = blockIdx.x - seg * p.n_ublk;
-  const int b = seg / p.T_max;
-  const int t = seg - b * p.T_max;
+  const int ND = p.T_max + p.U_max;  // anti-diagonals per utterance
+  const int diag = blockIdx.x / p.n_ublk;  // b * ND + d
+  const int ublk = blockIdx.x - diag * p.n_ublk;
+  const int b = diag / ND;
+  const int d = diag - b * ND;
   const int Tb = p.logit_lens[b];
   const int Ub = p.label_lens[b];
-  if (Tb < 1 || Tb > p.T_max || Ub < 0 || Ub > p.U_max || t >= Tb) return;
+  if (Tb < 1 || Tb > p.T_max || Ub < 0 || Ub > p.U_max) return;
+  const int u_first = ublk * p.rows_per_block;
+  const int u_lo = max(u_first, d - (Tb - 1));           // t = d - u <= T_b - 1
+  const int u_hi = min(u_first + p.rows_per_block, min(d, Ub) + 1);
+  if (u_lo >= u_hi) return;
 
   const int lg = threadIdx.x % G;  // lane inside the row group
   const int grp = threadIdx.x / G;
-  const int u_begin = ublk * p.rows_per_block;
-  const int u_end = min(u_begin + p.rows_per_block, Ub + 1);
   // the block's labels go through LDS, so no label load waits inside the row loop
   if (threadIdx.x < MAX_ROWS) {
-    const int u = u_begin + threadIdx.x;
+    const int u = u_first + threadIdx.x;
     s_label[threadIdx.x] = (u < Ub) ? p.labels[static_cast<int64_t>(b) * p.U_max + u] : kNoLabel;
   }
   __syncthreads();
@@ -87,16 +103,18 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   const uint4* __restrict__ cbase = reinterpret_cast<const uint4*>(base);
   const int64_t full_chunks = p.n_elem / EPC;
 
-  for (int u = u_begin + grp; u < u_end; u += GROUPS) {
-    const int64_t row = static_cast<int64_t>(seg) * (p.U_max + 1) + u;
+  for (int u = u_first + grp; u < u_hi; u += GROUPS) {
+    if (u < u_lo) continue;  // group-uniform
+    const int t = d - u;
+    const int64_t row = (static_cast<int64_t>(b) * p.T_max + t) * (p.U_max + 1) + u;
     const int64_t e0 = row * p.V;
     const int64_t c0 = e0 / EPC;
     const int mis = static_cast<int>(e0 - c0 * EPC);
     const int nch = (mis + p.V + EPC - 1) / EPC;
-    const int y = s_label[u - u_begin];
+    const int y = s_label[u - u_first];
     const bool y_ok = (y >= 0 && y < p.V);
     // z[blank], z[y]: the same address in every lane of the group (one request,
-    // the line the row's chunk loads bring in), issued ahead of them
+    // a line the row's chunk loads bring in anyway), issued ahead of them
     const float zb = ElemTraits<T>::load1(base + e0 + p.blank);
     const float zy = ElemTraits<T>::load1(base + e0 + (y_ok ? y : 0));
 
@@ -147,14 +165,21 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
 
     if (lg == 0) {
       const double lse = static_cast<double>(mg) + log(sd);
-      const int64_t li = static_cast<int64_t>(b) * p.sb + static_cast<int64_t>(t) * p.st +
-                         static_cast<int64_t>(u) * p.su;
-      p.lp_blank[li] = static_cast<double>(zb) - lse;
-      double lpl = -__builtin_inf();
-      if (u < Ub) lpl = y_ok ? static_cast<double>(zy) - lse : __builtin_nan("");
-      p.lp_label[li] = lpl;
-      if (p.rowinfo) p.rowinfo[row].lse2 = static_cast<float>(lse * kLog2eD);
-      if (p.lse_out) p.lse_out[row] = lse;
+      const double lpb = static_cast<double>(zb) - lse;
+      const double lpl = (u < Ub) ? (y_ok ? static_cast<double>(zy) - lse : __builtin_nan("")) : -__builtin_inf();
+      if (LATTICE) {
+        const int64_t sc = static_cast<int64_t>(diag) * (p.U_max + 1) + u;
+        const bool blank_arc = (t < Tb - 1) || (u == Ub);  // absent: last frame below the top row
+        double2 w;
+        w.x = blank_arc ? clamp_no_arc(lpb * kLog2eD) : kNoArc;
+        w.y = (u < Ub) ? clamp_no_arc(lpl * kLog2eD) : kNoArc;
+        p.lp2[sc] = w;
+        p.lse2[sc] = static_cast<float>(lse * kLog2eD);
+      } else {
+        if (p.lse_out) p.lse_out[row] = lse;
+        p.lp_blank_out[row] = lpb;
+        p.lp_label_out[row] = lpl;
+      }
     }
   }
 }

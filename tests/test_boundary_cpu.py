@@ -56,13 +56,15 @@ def shape(B=2, T=5, U=3, V=7, dt=0, gdt=None):
 def expected_workspace(B, T, U, V):
     a = lambda x: (x + 255) // 256 * 256  # noqa: E731
     rows = B * T * (U + 1)
-    cells = B * (T + U) * (U + 1)
-    score_cells = B * (T + U + 1) * (U + 1)  # one scratch diagonal row per utterance
-    o = a(rows * 16)
-    o = a(o + cells * 16)
-    o = a(o + score_cells * 8)
-    o = a(o + score_cells * 8)
-    return a(o + 2 * B * 8)
+    cells = B * (T + U) * (U + 1)            # anti-diagonal cells
+    score_cells = B * (T + U + 1) * (U + 1)  # plus one scratch diagonal per utterance
+    o = a(rows * 16)               # row records
+    o = a(o + cells * 16)          # {lp_blank, lp_label}
+    o = a(o + cells * 4)           # lse * log2 e
+    o = a(o + score_cells * 8)     # alpha
+    o = a(o + score_cells * 8)     # beta
+    o = a(o + 2 * B * 8)           # log P forward / backward
+    return a(o + B * 4)            # status
 
 
 @pytest.mark.parametrize("B,T,U,V", [(1, 1, 0, 2), (2, 20, 8, 16), (32, 250, 80, 1025), (64, 500, 150, 1025)])

@@ -34,29 +34,28 @@ def test_populate_kernel_addresses(B, T, U, V, dt):
     G, NB = k1_shape(V, epc)
     rows_per_block = (256 // G) * 4
     n_ublk = -(-(U + 1) // rows_per_block)
-    blocks = B * T * n_ublk
+    ND = T + U
+    blocks = B * ND * n_ublk
     assert blocks < 2**31
-    # every row a block can touch (u < U+1 always, the lengths bound it further)
-    seg = np.arange(B * T, dtype=np.int64)
-    for u in (0, U):
-        row = seg * (U + 1) + u
-        e0 = row * V
-        c0 = e0 // epc
-        mis = e0 - c0 * epc
-        nch = (mis + V + epc - 1) // epc
-        last_chunk = c0 + nch - 1
-        assert np.all(last_chunk * epc < n_elem)
-        assert np.all(e0 + V <= n_elem)
-        # the chunk-load path runs only when every chunk of the row is whole; its
-        # clamped indices stay in [c0, c0 + nch)
-        fast = c0 + nch <= n_elem // epc
-        assert np.all(((c0 + nch) * epc <= n_elem)[fast])
-        # only the tensor's last row can take the element-wise path
-        assert np.all(row[~fast] == B * T * (U + 1) - 1)
-    # lp written by diagonal: (b, t, u) -> 2*((t+u)*(U+1)+u) (+1) inside B*(T+U)*(U+1) double2
-    sb, st, su = 2 * (T + U) * (U + 1), 2 * (U + 1), 2 * (U + 2)
-    hi = (B - 1) * sb + (T - 1) * st + U * su + 1
-    assert hi < 2 * B * (T + U) * (U + 1)
+    # every (b, d, u) a block can reach with full lengths: t = d - u in [0, T), u in [0, U]
+    b, d, u = np.meshgrid(np.arange(B), np.arange(ND), np.arange(U + 1), indexing="ij")
+    t = d - u
+    ok = (t >= 0) & (t < T)
+    b, d, u, t = b[ok], d[ok], u[ok], t[ok]
+    row = (b.astype(np.int64) * T + t) * (U + 1) + u
+    e0 = row * V
+    c0 = e0 // epc
+    mis = e0 - c0 * epc
+    nch = (mis + V + epc - 1) // epc
+    assert np.all((c0 + nch - 1) * epc < n_elem)
+    assert np.all(e0 + V <= n_elem)
+    fast = c0 + nch <= n_elem // epc
+    assert np.all(((c0 + nch) * epc <= n_elem)[fast])
+    # only rows reaching into the tensor's final partial chunk read element-wise
+    assert np.all((e0 + V > (n_elem // epc) * epc)[~fast])
+    # lattice-form writes at (b*ND + d)*(U+1) + u inside the C-cell arrays
+    sc = (b.astype(np.int64) * ND + d) * (U + 1) + u
+    assert sc.max() < B * ND * (U + 1) and sc.min() >= 0
 
 
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
@@ -96,13 +95,21 @@ def test_gradient_kernel_chunk_mapping(B, T, U, V, dt):
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
 def test_lattice_kernel_addresses(B, T, U, V, dt):
     U1 = U + 1
+    ND = T + U
     K = next(k for k in (1, 2, 4, 8, 16) if U1 <= 64 * k)
     assert 64 * K >= U1
-    sab = (T + U + 1) * U1
-    # alpha / beta at (b, d, u): d <= T-1+U, u <= U; lanes past U_max store to the scratch row
+    sab = (ND + 1) * U1
+    # stores: node (d, u) with d <= D <= T-1+U, u <= U; everything else to the scratch row
     hi = (B - 1) * sab + (T - 1 + U) * U1 + U
     assert hi < B * sab
-    dump = (B - 1) * sab + (T + U) * U1
-    assert dump < B * sab
-    # the epilogue reads beta(t+1, u) for t < T-1 and beta(t, u+1) for u < U: diagonal <= T-1+U
-    assert (T - 2 + 1 + U) <= T - 1 + U
+    assert (B - 1) * sab + ND * U1 < B * sab
+    # weight loads are clamped into the utterance: d in [0, D], u in [max(0, d-T+1), min(d, U)]
+    for Tb, Ub in [(T, U), (1, 0), (max(1, T // 2), U // 2), (1, U), (T, 0)]:
+        D = Tb - 1 + Ub
+        for d in range(-20, D + 40):
+            dc = min(max(d, 0), D)
+            for u in range(0, 64 * K):
+                uc = min(max(u, dc - (Tb - 1)), min(dc, Ub))
+                assert 0 <= dc - uc < Tb and 0 <= uc <= Ub
+    # the posterior kernel reads beta at diagonal t+u+1 <= T-1+U only for t < T-1 or u < U
+    assert (T - 2) + U + 1 <= T - 1 + U
