@@ -78,24 +78,25 @@ Layout make_layout(const rnnt_shape_t& s, bool with_populate) {
 
 // ---- kernel 1 ---------------------------------------------------------------
 
-// Lanes per row G and chunks per lane NB: the smallest G*NB that covers a
-// row's chunks (NB <= 5 keeps the batch in registers); rows longer than 64*5
-// chunks take several batches.
+// Lanes per row G and interior chunks per lane NB: the smallest G*NB that
+// covers a row's interior chunks (at most V / EPC of them) with NB <= 5; rows
+// with more take the batched path (G = 64, NB = 5).
 struct K1Shape {
   int G, NB;
+  bool fast;
 };
 
 template <typename T>
 K1Shape k1_shape(int V) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
-  const int max_chunks = (EPC - 1 + V + EPC - 1) / EPC;
-  K1Shape best{64, 5};
+  const int interior = V / EPC;
+  K1Shape best{64, 5, false};
   int best_slots = 1 << 30;
   for (int g : {64, 32, 16, 8}) {
     for (int nb = 1; nb <= 5; ++nb) {
       const int slots = g * nb;
-      if (slots >= max_chunks && slots < best_slots) {
-        best = K1Shape{g, nb};
+      if (slots >= interior && slots < best_slots) {
+        best = K1Shape{g, nb, true};
         best_slots = slots;
       }
     }
@@ -103,32 +104,33 @@ K1Shape k1_shape(int V) {
   return best;
 }
 
-template <typename T, int G, int NB, bool LATTICE>
+template <typename T, int G, int NB, bool LATTICE, bool FAST>
 hipError_t launch_k1_g(PopulateParams p, hipStream_t stream) {
   constexpr int groups = 256 / G;
   p.rows_per_block = groups * 4;
   p.n_ublk = (p.U_max + 1 + p.rows_per_block - 1) / p.rows_per_block;
   const int64_t blocks = static_cast<int64_t>(p.B) * (p.T_max + p.U_max) * p.n_ublk;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((k1_populate<T, G, NB, LATTICE>), dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, stream,
-                     p);
+  hipLaunchKernelGGL((k1_populate<T, G, NB, LATTICE, FAST>), dim3(static_cast<uint32_t>(blocks)), dim3(256), 0,
+                     stream, p);
   return hipGetLastError();
 }
 
 template <typename T, int G, bool LATTICE>
 hipError_t launch_k1_nb(int nb, const PopulateParams& p, hipStream_t stream) {
   switch (nb) {
-    case 1: return launch_k1_g<T, G, 1, LATTICE>(p, stream);
-    case 2: return launch_k1_g<T, G, 2, LATTICE>(p, stream);
-    case 3: return launch_k1_g<T, G, 3, LATTICE>(p, stream);
-    case 4: return launch_k1_g<T, G, 4, LATTICE>(p, stream);
-    default: return launch_k1_g<T, G, 5, LATTICE>(p, stream);
+    case 1: return launch_k1_g<T, G, 1, LATTICE, true>(p, stream);
+    case 2: return launch_k1_g<T, G, 2, LATTICE, true>(p, stream);
+    case 3: return launch_k1_g<T, G, 3, LATTICE, true>(p, stream);
+    case 4: return launch_k1_g<T, G, 4, LATTICE, true>(p, stream);
+    default: return launch_k1_g<T, G, 5, LATTICE, true>(p, stream);
   }
 }
 
 template <typename T, bool LATTICE>
 hipError_t launch_k1(const PopulateParams& p, hipStream_t stream) {
   const K1Shape ks = k1_shape<T>(p.V);
+  if (!ks.fast) return launch_k1_g<T, 64, 5, LATTICE, false>(p, stream);
   switch (ks.G) {
     case 8: return launch_k1_nb<T, 8, LATTICE>(ks.NB, p, stream);
     case 16: return launch_k1_nb<T, 16, LATTICE>(ks.NB, p, stream);

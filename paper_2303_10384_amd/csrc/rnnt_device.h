@@ -47,6 +47,81 @@ __device__ __forceinline__ double log_add2(double x, double y) {
   return m + static_cast<double>(c);
 }
 
+// ---- reductions over a group of G consecutive lanes (G = 1..64, a power of 2)
+// DPP moves inside each 16-lane row (pair swap, quad swap, half-row mirror,
+// row mirror), so after the in-row steps every lane holds its group's value;
+// across rows: row broadcasts, then the group's last lane is read back.
+namespace dpp {
+constexpr int kQuadSwap1 = 0xB1;    // quad_perm [1,0,3,2]
+constexpr int kQuadSwap2 = 0x4E;    // quad_perm [2,3,0,1]
+constexpr int kHalfMirror = 0x141;  // lane i <- 7-i within 8 lanes
+constexpr int kRowMirror = 0x140;   // lane i <- 15-i within 16 lanes
+constexpr int kRowBcast15 = 0x142;  // every lane of row r <- lane 15 of row r-1
+constexpr int kRowBcast31 = 0x143;  // every lane of rows 2,3 <- lane 31
+}  // namespace dpp
+
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ float dpp_f32(float x, float fill) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, fill),
+                                                               __builtin_bit_cast(int, x), CTRL, ROW_MASK, 0xf,
+                                                               false));
+}
+
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ double dpp_f64(double x, double fill) {
+  const int lo = __builtin_amdgcn_update_dpp(__double2loint(fill), __double2loint(x), CTRL, ROW_MASK, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(__double2hiint(fill), __double2hiint(x), CTRL, ROW_MASK, 0xf, false);
+  return __hiloint2double(hi, lo);
+}
+
+struct MaxOp {
+  template <typename V>
+  __device__ static V apply(V a, V b) { return a > b ? a : b; }
+};
+struct SumOp {
+  template <typename V>
+  __device__ static V apply(V a, V b) { return a + b; }
+};
+
+template <typename V, int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ V dpp_any(V x, V fill) {
+  if constexpr (sizeof(V) == 8) return dpp_f64<CTRL, ROW_MASK>(x, fill);
+  else return dpp_f32<CTRL, ROW_MASK>(x, fill);
+}
+
+template <typename V>
+__device__ __forceinline__ V readlane_any(V x, int lane) {
+  if constexpr (sizeof(V) == 8) {
+    const int lo = __builtin_amdgcn_readlane(__double2loint(x), lane);
+    const int hi = __builtin_amdgcn_readlane(__double2hiint(x), lane);
+    return __hiloint2double(hi, lo);
+  } else {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), lane));
+  }
+}
+
+// Every lane of the group receives op over the group's G lanes; `ident` is
+// the operation's identity.  All 64 lanes must be active.
+template <int G, typename Op, typename V>
+__device__ __forceinline__ V group_reduce(V x, V ident) {
+  if constexpr (G >= 2) x = Op::apply(x, dpp_any<V, dpp::kQuadSwap1>(x, ident));
+  if constexpr (G >= 4) x = Op::apply(x, dpp_any<V, dpp::kQuadSwap2>(x, ident));
+  if constexpr (G >= 8) x = Op::apply(x, dpp_any<V, dpp::kHalfMirror>(x, ident));
+  if constexpr (G >= 16) x = Op::apply(x, dpp_any<V, dpp::kRowMirror>(x, ident));
+  if constexpr (G >= 32) {
+    // rows 1 and 3 add rows 0 and 2: lanes 31 and 63 hold the 32-lane totals
+    x = Op::apply(x, dpp_any<V, dpp::kRowBcast15, 0xa>(x, ident));
+    if constexpr (G == 32) {
+      const V lo = readlane_any(x, 31), hi = readlane_any(x, 63);
+      x = (__lane_id() < 32) ? lo : hi;
+    } else {
+      x = Op::apply(x, dpp_any<V, dpp::kRowBcast31, 0xc>(x, ident));
+      x = readlane_any(x, 63);
+    }
+  }
+  return x;
+}
+
 // ---- element types: 16-byte chunks of logits / gradient -------------------
 
 template <typename T>

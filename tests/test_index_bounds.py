@@ -18,12 +18,12 @@ SHAPES = [(w.B, w.T_max, w.U_max, w.V, w.dtype) for w in WORKLOADS.values()] + [
 
 
 def k1_shape(V, epc):
-    max_chunks = (epc - 1 + V + epc - 1) // epc
-    best, best_slots = (64, 5), 1 << 30
+    interior = V // epc
+    best, best_slots = (64, 5, False), 1 << 30
     for g in (64, 32, 16, 8):
         for nb in range(1, 6):
-            if g * nb >= max_chunks and g * nb < best_slots:
-                best, best_slots = (g, nb), g * nb
+            if g * nb >= interior and g * nb < best_slots:
+                best, best_slots = (g, nb, True), g * nb
     return best
 
 
@@ -31,7 +31,7 @@ def k1_shape(V, epc):
 def test_populate_kernel_addresses(B, T, U, V, dt):
     epc = EPC[dt]
     n_elem = B * T * (U + 1) * V
-    G, NB = k1_shape(V, epc)
+    G, NB, fast = k1_shape(V, epc)
     rows_per_block = (256 // G) * 4
     n_ublk = -(-(U + 1) // rows_per_block)
     ND = T + U
@@ -49,10 +49,18 @@ def test_populate_kernel_addresses(B, T, U, V, dt):
     nch = (mis + V + epc - 1) // epc
     assert np.all((c0 + nch - 1) * epc < n_elem)
     assert np.all(e0 + V <= n_elem)
-    fast = c0 + nch <= n_elem // epc
-    assert np.all(((c0 + nch) * epc <= n_elem)[fast])
+    whole = c0 + nch <= n_elem // epc
+    assert np.all(((c0 + nch) * epc <= n_elem)[whole])
+    if fast:
+        # interior chunks [kf, kl] fit G*NB lanes-chunks; every clamped index stays in [0, nch)
+        first_partial = mis != 0
+        last_partial = (mis + V) % epc != 0
+        kf = first_partial.astype(np.int64)
+        kl = nch - 1 - last_partial.astype(np.int64)
+        assert np.all(kl - kf + 1 <= G * NB)
+        assert np.all(np.maximum(kl, 0) < nch) and np.all(kf <= nch)
     # only rows reaching into the tensor's final partial chunk read element-wise
-    assert np.all((e0 + V > (n_elem // epc) * epc)[~fast])
+    assert np.all((e0 + V > (n_elem // epc) * epc)[~whole])
     # lattice-form writes at (b*ND + d)*(U+1) + u inside the C-cell arrays
     sc = (b.astype(np.int64) * ND + d) * (U + 1) + u
     assert sc.max() < B * ND * (U + 1) and sc.min() >= 0
