@@ -8,7 +8,8 @@ import ctypes
 import os
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "librnnt_mi355x.so")
+# another build of the same library may be named by RNNT_MI355X_LIBRARY
+LIB_PATH = os.environ.get("RNNT_MI355X_LIBRARY") or os.path.join(PKG, "librnnt_mi355x.so")
 
 RNNT_OK = 0
 STATUS_NAMES = {

@@ -92,7 +92,8 @@ K1Shape k1_shape(int V) {
   const int interior = V / EPC;
   K1Shape best{64, 5, false};
   int best_slots = 1 << 30;
-  for (int g : {64, 32, 16, 8}) {
+  // ties go to the smaller G: more rows per wave share each reduction
+  for (int g : {8, 16, 32, 64}) {
     for (int nb = 1; nb <= 5; ++nb) {
       const int slots = g * nb;
       if (slots >= interior && slots < best_slots) {
@@ -106,8 +107,8 @@ K1Shape k1_shape(int V) {
 
 template <typename T, int G, int NB, bool LATTICE, bool FAST>
 hipError_t launch_k1_g(PopulateParams p, hipStream_t stream) {
-  constexpr int groups = 256 / G;
-  p.rows_per_block = groups * 4;
+  // one block per anti-diagonal (split only past kMaxRowsPerBlock units)
+  p.rows_per_block = p.U_max + 1 < kMaxRowsPerBlock ? p.U_max + 1 : kMaxRowsPerBlock;
   p.n_ublk = (p.U_max + 1 + p.rows_per_block - 1) / p.rows_per_block;
   const int64_t blocks = static_cast<int64_t>(p.B) * (p.T_max + p.U_max) * p.n_ublk;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;

@@ -47,6 +47,29 @@ __device__ __forceinline__ double log_add2(double x, double y) {
   return m + static_cast<double>(c);
 }
 
+// ---- 16-byte global accesses, optionally with the nontemporal (streaming) hint
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+template <bool NT>
+__device__ __forceinline__ uint4 load16(const uint4* p) {
+  if constexpr (NT) {
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+  } else {
+    return *p;
+  }
+}
+
+template <bool NT>
+__device__ __forceinline__ void store16(uint4* p, const uint4& v) {
+  if constexpr (NT) {
+    const u32x4 w = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(p));
+  } else {
+    *p = v;
+  }
+}
+
 // ---- reductions over a group of G consecutive lanes (G = 1..64, a power of 2)
 // DPP moves inside each 16-lane row (pair swap, quad swap, half-row mirror,
 // row mirror), so after the in-row steps every lane holds its group's value;

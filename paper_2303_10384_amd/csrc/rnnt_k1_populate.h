@@ -35,7 +35,13 @@
 
 #include "rnnt_device.h"
 
+#ifndef RNNT_K1_NT_LOAD
+#define RNNT_K1_NT_LOAD 1
+#endif
+
 namespace rnnt {
+
+constexpr bool kK1StreamLoads = RNNT_K1_NT_LOAD != 0;
 
 struct PopulateParams {
   const void* logits;
@@ -45,7 +51,7 @@ struct PopulateParams {
   const int32_t* label_lens;
   int64_t n_elem;          // B * T_max * (U_max+1) * V
   int32_t n_ublk;          // blocks per anti-diagonal
-  int32_t rows_per_block;  // consecutive units u per block
+  int32_t rows_per_block;  // consecutive units u per block (<= kMaxRowsPerBlock)
   // lattice form
   double2* lp2;            // (B, T_max+U_max, U_max+1) {lp_blank, lp_label} * log2(e)
   float* lse2;             // same index: lse * log2(e)
@@ -98,9 +104,9 @@ __device__ __forceinline__ void row_stats_fast(const T* __restrict__ base, int64
 #pragma unroll
   for (int q = 0; q < NB; ++q) {
     const int k = min(max(kf + q * G + lg, kint_lo), kint_hi);
-    raw[q] = cbase[c0 + k];
+    raw[q] = load16<kK1StreamLoads>(cbase + c0 + k);
   }
-  const uint4 rawb = cbase[c0 + max(kbnd, 0)];
+  const uint4 rawb = load16<kK1StreamLoads>(cbase + c0 + max(kbnd, 0));
 
   float xb[EPC];
   {
@@ -190,12 +196,13 @@ __device__ __forceinline__ void row_stats_general(const T* __restrict__ base, in
 
 // FAST: rows take row_stats_fast (the launcher checks that NB*G covers every
 // row's interior chunks); otherwise row_stats_general.
+constexpr int kMaxRowsPerBlock = 1024;
+
 template <typename T, int G, int NB, bool LATTICE, bool FAST>
 __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
   constexpr int GROUPS = 256 / G;      // rows in flight per block
-  constexpr int MAX_ROWS = GROUPS * 4; // rows_per_block set by the launcher
-  __shared__ int s_label[MAX_ROWS];
+  __shared__ int s_label[kMaxRowsPerBlock];
 
   const int ND = p.T_max + p.U_max;  // anti-diagonals per utterance
   const int diag = blockIdx.x / p.n_ublk;  // b * ND + d
@@ -213,9 +220,9 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   const int lg = threadIdx.x % G;  // lane inside the row group
   const int grp = threadIdx.x / G;
   // the block's labels go through LDS, so no label load waits inside the row loop
-  if (threadIdx.x < MAX_ROWS) {
-    const int u = u_first + threadIdx.x;
-    s_label[threadIdx.x] = (u < Ub) ? p.labels[static_cast<int64_t>(b) * p.U_max + u] : kNoLabel;
+  for (int i = threadIdx.x; i < u_hi - u_first; i += blockDim.x) {
+    const int u = u_first + i;
+    s_label[i] = (u < Ub) ? p.labels[static_cast<int64_t>(b) * p.U_max + u] : kNoLabel;
   }
   __syncthreads();
 
@@ -224,9 +231,9 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
 
   // all lanes of a wave stay in the loop (the group reductions use every lane);
   // a group past the block's last row computes a row it does not write
-  const int n_iter = (u_hi - u_first + GROUPS - 1) / GROUPS;
+  const int n_iter = (u_hi - u_lo + GROUPS - 1) / GROUPS;
   for (int it = 0; it < n_iter; ++it) {
-    const int u_raw = u_first + it * GROUPS + grp;
+    const int u_raw = u_lo + it * GROUPS + grp;
     const bool live = u_raw >= u_lo && u_raw < u_hi;
     const int u = live ? u_raw : u_lo;  // dead groups recompute the block's first row
     const int t = d - u;

@@ -13,7 +13,17 @@
 
 #include "rnnt_device.h"
 
+#ifndef RNNT_K3_NT_LOAD
+#define RNNT_K3_NT_LOAD 1
+#endif
+#ifndef RNNT_K3_NT_STORE
+#define RNNT_K3_NT_STORE 1
+#endif
+
 namespace rnnt {
+
+constexpr bool kK3StreamLoads = RNNT_K3_NT_LOAD != 0;
+constexpr bool kK3StreamStores = RNNT_K3_NT_STORE != 0;
 
 struct GradParams {
   const void* logits;
@@ -44,7 +54,7 @@ __device__ __forceinline__ void store_chunk(void* dst, int64_t e0, const float* 
   static_assert(EPC % PER == 0, "input chunk must cover whole output chunks");
   uint4* d = reinterpret_cast<uint4*>(static_cast<Tout*>(dst) + e0);
 #pragma unroll
-  for (int i = 0; i < EPC / PER; ++i) d[i] = ElemTraits<Tout>::pack(out + i * PER);
+  for (int i = 0; i < EPC / PER; ++i) store16<kK3StreamStores>(d + i, ElemTraits<Tout>::pack(out + i * PER));
 }
 
 // Tin: logits element type; Tout: gradient element type (Tin or float).
@@ -88,7 +98,7 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
       } else {
         float f[EPC];
         if (full) {
-          ElemTraits<T>::unpack(src[c], f);
+          ElemTraits<T>::unpack(load16<kK3StreamLoads>(src + c), f);
         } else {
 #pragma unroll
           for (int j = 0; j < EPC; ++j) f[j] = (e0 + j < p.n_elem) ? ElemTraits<T>::load1(src_e + e0 + j) : 0.f;
@@ -103,7 +113,7 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
     } else {
       float f[EPC];
       if (full) {
-        ElemTraits<T>::unpack(src[c], f);
+        ElemTraits<T>::unpack(load16<kK3StreamLoads>(src + c), f);
       } else {
 #pragma unroll
         for (int j = 0; j < EPC; ++j) f[j] = (e0 + j < p.n_elem) ? ElemTraits<T>::load1(src_e + e0 + j) : 0.f;

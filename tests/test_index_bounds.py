@@ -20,7 +20,7 @@ SHAPES = [(w.B, w.T_max, w.U_max, w.V, w.dtype) for w in WORKLOADS.values()] + [
 def k1_shape(V, epc):
     interior = V // epc
     best, best_slots = (64, 5, False), 1 << 30
-    for g in (64, 32, 16, 8):
+    for g in (8, 16, 32, 64):
         for nb in range(1, 6):
             if g * nb >= interior and g * nb < best_slots:
                 best, best_slots = (g, nb, True), g * nb
@@ -32,7 +32,7 @@ def test_populate_kernel_addresses(B, T, U, V, dt):
     epc = EPC[dt]
     n_elem = B * T * (U + 1) * V
     G, NB, fast = k1_shape(V, epc)
-    rows_per_block = (256 // G) * 4
+    rows_per_block = min(U + 1, 1024)
     n_ublk = -(-(U + 1) // rows_per_block)
     ND = T + U
     blocks = B * ND * n_ublk
