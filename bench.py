@@ -12,7 +12,6 @@ MI355X peak, and the CPU oracle timed on a bounded sample.
 """
 import argparse
 import ctypes
-import hashlib
 import json
 import os
 import sys
@@ -22,7 +21,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
-ROWREC_BYTES = 16      # per-row record written by kernel 2 and read by kernel 3
+ROWREC_BYTES = 16      # per-row record written by kernel 2b and read by kernel 3
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 
 
@@ -57,25 +56,40 @@ class HipEvents:
             self.hip.hipEventDestroy(ctypes.c_void_p(h))
 
 
-def source_digest(paths):
-    h = hashlib.sha256()
-    for p in paths:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()[:16]
-
-
 def profiled_traffic(workload):
     """HBM bytes per gradient-kernel launch from the committed rocprofv3 counter
-    summary, if it was taken on the kernel sources as they are now; else None."""
+    record, if it was taken on the kernel sources as they are now; else None."""
+    from paper_2303_10384_amd.profiling import KERNEL_SOURCES, source_digest
     path = os.path.join(PROFILE_DIR, "k3_grad_%s_traffic.json" % workload)
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("source_digest") != source_digest(rec.get("sources", [])):
+    if rec.get("source_digest") != source_digest(KERNEL_SOURCES):
         return None
     return rec.get("hbm_bytes_per_launch")
+
+
+def algorithmic_bytes(w, tl, ul, s_in, s_out):
+    """Bytes each streaming kernel must move at the least, per launch.
+
+    Kernel 1 reads the logits of the valid rows (t < T_b, u <= U_b) once.
+    Kernel 3 reads the valid rows' logits and the per-row record of every padded
+    row, and writes the whole gradient (zeros in the padding rows).  The lattice
+    arrays of kernels 2 / 2b (a few MB) are left out.  The step as a whole must
+    read the valid logits twice (the arc posteriors that kernel 3 needs depend on
+    every row's normaliser) and write the whole gradient once."""
+    import numpy as np
+    r_valid = int(np.sum(tl.astype(np.int64) * (ul.astype(np.int64) + 1)))
+    r_total = w.B * w.T_max * (w.U_max + 1)
+    V = w.V
+    return {
+        "valid_rows": r_valid,
+        "padded_rows": r_total,
+        "k1_populate": r_valid * V * s_in,
+        "k3_grad": r_valid * V * s_in + r_total * V * s_out + r_total * ROWREC_BYTES,
+        "step": 2 * r_valid * V * s_in + r_total * V * s_out,
+    }
 
 
 def cpu_oracle_worker(args):
@@ -104,9 +118,10 @@ def cpu_baseline(w, tl, ul, labels, budget_s):
         t0 = time.perf_counter()
         pool.map(cpu_oracle_worker, jobs[:cores])  # one round, to size the sample
         t_round = time.perf_counter() - t0
-        rounds = max(1, min(-(-len(jobs) // cores), int(budget_s / max(t_round, 1e-3))))
-        sample = jobs[:rounds * cores]
-        log("[bench] cpu oracle: one round of %d utterances took %.1f s; timing %d utterances"
+        # cycle through the batch's utterances until about budget_s of work is queued
+        rounds = max(1, int(budget_s / max(t_round, 1e-3)))
+        sample = [jobs[i % len(jobs)] for i in range(rounds * min(cores, len(jobs)))]
+        log("[bench] cpu oracle: one round of %d utterances took %.1f s; timing %d utterance evaluations"
             % (min(cores, len(jobs)), t_round, len(sample)))
         t0 = time.perf_counter()
         pool.map(cpu_oracle_worker, sample)
@@ -117,10 +132,23 @@ def cpu_baseline(w, tl, ul, labels, budget_s):
         "unit": "joint-logit elements/s",
         "cores": min(cores, n),
         "kind": "oracle",
-        "sample": "%d of the %d utterances of the batch (their lengths and labels, N(0,%g) logits), float64 "
-                  "loss + gradient, %d worker processes, %.1f s; elements counted as padded rows x V like the "
-                  "GPU value" % (n, w.B, w.sigma, min(cores, n), dt),
+        "sample": "%d utterance evaluations cycling through the %d utterances of the batch (their lengths and "
+                  "labels, N(0,%g) logits), float64 loss + gradient, %d worker processes, %.1f s; elements "
+                  "counted as padded rows x V like the GPU value" % (n, w.B, w.sigma, min(cores, n), dt),
     }
+
+
+def copy_probe(torch, w, steps):
+    """Plain device-to-device copies of a known size (the gradient tensor's bytes):
+    the reference reading for the FETCH_SIZE / WRITE_SIZE counters."""
+    nbytes = w.B * w.T_max * (w.U_max + 1) * w.V * 4
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": nbytes, "copies": steps}), flush=True)
 
 
 def main():
@@ -130,7 +158,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="bpe", choices=["tiny", "char", "bpe", "wrnnt", "large"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work to time")
+    ap.add_argument("--cpu-budget", type=float, default=30.0, help="seconds of oracle work to time")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run --steps device-to-device copies of the workload's gradient size (the "
+                         "known-size copy that calibrates the HBM byte counters), then exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the loss has no multi-GPU path in this build "
@@ -145,6 +176,9 @@ def main():
     from paper_2303_10384_amd import workloads as W
 
     w = W.WORKLOADS[args.workload]
+    if args.copy_probe:
+        copy_probe(torch, w, args.steps)
+        return
     log("[bench] workload", w.describe())
     tl, ul, labels = W.make_lengths_labels(w)
     cpu = None
@@ -189,14 +223,10 @@ def main():
     log("[bench] per step %.4f ms (wall %.4f ms): k1 %.4f  k2 %.4f  k2b %.4f  k3 %.4f ms"
         % (ms_per_step, wall * 1e3 / args.steps, k1_ms, k2_ms, k2b_ms, k3_ms))
 
-    s = logits.element_size()
-    V = w.V
-    r_valid = int(np.sum(tl.astype(np.int64) * (ul.astype(np.int64) + 1)))
-    r_total = w.B * w.T_max * (w.U_max + 1)
+    ab = algorithmic_bytes(w, tl, ul, logits.element_size(), grad.element_size())
+    r_valid, r_total, V = ab["valid_rows"], ab["padded_rows"], w.V
     elems = r_total * V
-    k1_bytes = r_valid * V * s
-    k3_bytes = r_valid * V * s + r_total * V * s + r_total * ROWREC_BYTES
-    step_bytes = 2 * r_valid * V * s + r_total * V * s
+    k1_bytes, k3_bytes, step_bytes = ab["k1_populate"], ab["k3_grad"], ab["step"]
     k3_gbs = k3_bytes / (k3_ms * 1e-3) / 1e9
     traffic = profiled_traffic(args.workload)
     roofline = {
@@ -234,6 +264,7 @@ def main():
         "kernel_ms": {"k1_populate": round(k1_ms, 5), "k2_lattice": round(k2_ms, 5),
                       "k2b_posteriors": round(k2b_ms, 5), "k3_grad": round(k3_ms, 5)},
         "kernel_gbs": {"k1_populate": round(k1_bytes / (k1_ms * 1e-3) / 1e9, 1), "k3_grad": round(k3_gbs, 1)},
+        "algorithmic_bytes": {"k1_populate": k1_bytes, "k3_grad": k3_bytes, "step": step_bytes},
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

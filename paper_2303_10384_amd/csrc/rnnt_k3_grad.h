@@ -5,9 +5,9 @@
 // arc posteriors g_b, g_l and p = softmax(z):
 //   d loss / d z_v = p_v (g_b + g_l) - g_b [v = blank] - g_l [v = y_{u+1}]
 // The kernel streams the whole gradient tensor once: each 16-byte chunk is
-// located in its row(s) by index arithmetic, rows flagged as zero rows
-// (padding, bad utterances) are written as 0 without reading the logits, and
-// every other chunk reads the logits once and writes the gradient once.
+// located in its row(s) by index arithmetic, chunks of zero rows (padding, bad
+// utterances) are written as 0 without reading the logits, and every other
+// chunk reads the logits once and writes the gradient once.
 // p_v = exp2(z_v * log2(e) - lse2) with lse2 = lse * log2(e) from the row record.
 #pragma once
 
@@ -57,22 +57,19 @@ __device__ __forceinline__ void store_chunk(void* dst, int64_t e0, const float* 
   for (int i = 0; i < EPC / PER; ++i) store16<kK3StreamStores>(d + i, ElemTraits<Tout>::pack(out + i * PER));
 }
 
-// Tin: logits element type; Tout: gradient element type (Tin or float).
-// SMALLV: V < elements per chunk, so one chunk may cover several rows.
-template <typename Tin, typename Tout, bool SMALLV>
-__global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
-  using T = Tin;
+// The chunks of one block, one at a time (any V; the tensor's final partial
+// chunk read and written element by element).  SMALLV: V < elements per chunk,
+// so one chunk may cover several rows.  Only small-V tensors and the block
+// holding the final partial chunk come here; zero rows' logits are read too
+// (and ignored).
+template <typename T, typename Tout, bool SMALLV>
+__device__ __forceinline__ void grad_chunks_general(const GradParams& p, int64_t tile0, int64_t r_tile,
+                                                    uint32_t v_tile) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
-  const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kGradTileChunks;
-  const int64_t e_tile = tile0 * EPC;
-  const int64_t r_tile = e_tile / p.V;
-  const uint32_t v_tile = static_cast<uint32_t>(e_tile - r_tile * p.V);
   const uint32_t uV = static_cast<uint32_t>(p.V);
   const uint4* __restrict__ src = static_cast<const uint4*>(p.logits);
   const T* __restrict__ src_e = static_cast<const T*>(p.logits);
   Tout* __restrict__ dst_e = static_cast<Tout*>(p.grad);
-
-#pragma unroll
   for (int q = 0; q < kGradChunksPerThread; ++q) {
     const int cl = q * kGradThreads + static_cast<int>(threadIdx.x);
     const int64_t c = tile0 + cl;
@@ -83,52 +80,23 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
     int64_t r = r_tile + dr;
     int v = static_cast<int>(off - dr * uV);
     const bool full = e0 + EPC <= p.n_elem;
-    float out[EPC];
-
-    if (!SMALLV) {
-      const RowInfo ri0 = p.rowinfo[r];
-      const bool split = v + EPC > p.V;
-      RowInfo ri1 = ri0;
-      if (split && r + 1 < p.n_rows) ri1 = p.rowinfo[r + 1];
-      const bool zero0 = ri0.label == kZeroRow;
-      const bool zero1 = ri1.label == kZeroRow;
-      if (zero0 && (!split || zero1)) {
-#pragma unroll
-        for (int j = 0; j < EPC; ++j) out[j] = 0.f;
-      } else {
-        float f[EPC];
-        if (full) {
-          ElemTraits<T>::unpack(load16<kK3StreamLoads>(src + c), f);
-        } else {
-#pragma unroll
-          for (int j = 0; j < EPC; ++j) f[j] = (e0 + j < p.n_elem) ? ElemTraits<T>::load1(src_e + e0 + j) : 0.f;
-        }
-#pragma unroll
-        for (int j = 0; j < EPC; ++j) {
-          const int vj = v + j;
-          const bool second = vj >= p.V;
-          out[j] = second ? grad_elem(f[j], vj - p.V, ri1, p.blank) : grad_elem(f[j], vj, ri0, p.blank);
-        }
-      }
+    float f[EPC], out[EPC];
+    RowInfo ri = p.rowinfo[r];
+    if (full) {
+      ElemTraits<T>::unpack(load16<kK3StreamLoads>(src + c), f);
     } else {
-      float f[EPC];
-      if (full) {
-        ElemTraits<T>::unpack(load16<kK3StreamLoads>(src + c), f);
-      } else {
 #pragma unroll
-        for (int j = 0; j < EPC; ++j) f[j] = (e0 + j < p.n_elem) ? ElemTraits<T>::load1(src_e + e0 + j) : 0.f;
-      }
-      RowInfo ri = p.rowinfo[r];
+      for (int j = 0; j < EPC; ++j) f[j] = (e0 + j < p.n_elem) ? ElemTraits<T>::load1(src_e + e0 + j) : 0.f;
+    }
 #pragma unroll
-      for (int j = 0; j < EPC; ++j) {
-        if (v >= p.V) {
-          v -= p.V;
-          ++r;
-          if (r < p.n_rows) ri = p.rowinfo[r];
-        }
-        out[j] = grad_elem(f[j], v, ri, p.blank);
-        ++v;
+    for (int j = 0; j < EPC; ++j) {
+      if (v >= p.V) {  // next row (at most once per chunk unless SMALLV)
+        v -= p.V;
+        ++r;
+        if (r < p.n_rows) ri = p.rowinfo[r];
       }
+      out[j] = grad_elem(f[j], v, ri, p.blank);
+      ++v;
     }
     if (full) {
       store_chunk<Tout, EPC>(p.grad, e0, out);
@@ -137,6 +105,78 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
       for (int j = 0; j < EPC; ++j)
         if (e0 + j < p.n_elem) ElemTraits<Tout>::store1(dst_e + e0 + j, out[j]);
     }
+  }
+}
+
+constexpr int kBufferWord3 = 0x00020000;  // raw buffer, 32-bit format (gfx9 family)
+constexpr int kOutOfRange = static_cast<int>(0x80000000u);
+constexpr int kBufferNT = RNNT_K3_NT_LOAD ? 2 : 0;  // cache policy bits of a buffer load: nt
+
+// Tin: logits element type; Tout: gradient element type (Tin or float).
+// A block covers kGradTileChunks consecutive chunks.  Every block but the one
+// holding the tensor's final partial chunk takes the fast path, in three phases
+// that keep all of a thread's memory requests in flight together: the row
+// records of its chunks; the logits of its chunks, as buffer loads issued
+// unconditionally (a chunk whose logits are not needed gets an offset past the
+// buffer's end, which reads zero without touching memory); arithmetic and
+// stores.
+template <typename Tin, typename Tout, bool SMALLV>
+__global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
+  using T = Tin;
+  constexpr int EPC = ElemTraits<T>::kPerChunk;
+  constexpr int Q = kGradChunksPerThread;
+  const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kGradTileChunks;
+  const int64_t e_tile = tile0 * EPC;
+  const int64_t r_tile = e_tile / p.V;
+  const uint32_t v_tile = static_cast<uint32_t>(e_tile - r_tile * p.V);
+  const uint32_t uV = static_cast<uint32_t>(p.V);
+  const int64_t n_full = p.n_elem / EPC;  // chunks wholly inside the tensor
+  if (SMALLV || (p.n_elem % EPC != 0 && tile0 + kGradTileChunks > n_full)) {
+    grad_chunks_general<T, Tout, SMALLV>(p, tile0, r_tile, v_tile);
+    return;
+  }
+
+  int64_t r[Q];
+  int v[Q];
+  RowInfo ri0[Q], ri1[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const uint32_t off = v_tile + static_cast<uint32_t>(q * kGradThreads + static_cast<int>(threadIdx.x)) * EPC;
+    const uint32_t dr = off / uV;
+    r[q] = min(r_tile + dr, p.n_rows - 1);  // chunks past the end read a valid record and store nothing
+    v[q] = static_cast<int>(off - dr * uV);
+    ri0[q] = p.rowinfo[r[q]];
+    ri1[q] = p.rowinfo[min(r[q] + 1, p.n_rows - 1)];
+  }
+  __builtin_amdgcn_sched_barrier(0);  // all record loads issue before any of them is used
+  const int64_t tile_bytes = min<int64_t>(kGradTileChunks, n_full - tile0) * 16;
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint4*>(static_cast<const uint4*>(p.logits) + tile0), static_cast<short>(0),
+      static_cast<int>(tile_bytes), kBufferWord3);
+  u32x4 raw[Q];
+  bool store[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int cl = q * kGradThreads + static_cast<int>(threadIdx.x);
+    const bool live = tile0 + cl < n_full;
+    const bool split = v[q] + EPC > p.V;
+    const bool zero = ri0[q].label == kZeroRow && (!split || ri1[q].label == kZeroRow);
+    store[q] = live;
+    const int off = (live && !zero) ? cl * 16 : kOutOfRange;
+    raw[q] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, kBufferNT);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    float f[EPC], out[EPC];
+    ElemTraits<T>::unpack(make_uint4(raw[q].x, raw[q].y, raw[q].z, raw[q].w), f);
+#pragma unroll
+    for (int j = 0; j < EPC; ++j) {
+      const int vj = v[q] + j;
+      const bool second = vj >= p.V;
+      out[j] = second ? grad_elem(f[j], vj - p.V, ri1[q], p.blank) : grad_elem(f[j], vj, ri0[q], p.blank);
+    }
+    if (store[q]) store_chunk<Tout, EPC>(p.grad, (tile0 + q * kGradThreads + static_cast<int>(threadIdx.x)) * EPC, out);
   }
 }
 

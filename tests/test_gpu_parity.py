@@ -85,7 +85,7 @@ def tol_check(loss, grad, loss_ref, grad_ref, logits_dtype="f32", tl=None, ul=No
     gerr = 0.0
     if grad is not None:
         err = np.abs(grad.astype(np.float64) - grad_ref)
-        bad = err > grad_bound(grad_ref, logits_dtype, grad_dtype)
+        bad = ~(err <= grad_bound(grad_ref, logits_dtype, grad_dtype))  # NaN counts as bad
         assert not bad.any(), ("grad", err.max(), np.argwhere(bad)[:5])
         gerr = float(err.max())
         if grad_dtype == "bf16":
@@ -109,12 +109,17 @@ def tol_check(loss, grad, loss_ref, grad_ref, logits_dtype="f32", tl=None, ul=No
 def run_case(torch, pkg, logits_np, tl, ul, labels, blank=0, variant="rnnt", dtype="f32", poison=True,
              need_grad=True, grad_dtype=None):
     """GPU call on the given inputs (logits rounded to dtype on the device);
-    returns (loss, grad as float64 numpy or None, the exact logits the GPU saw as float64)."""
+    returns (loss, grad as float64 numpy or None, the exact logits the GPU saw as float64).
+    The gradient buffer starts out NaN, so an element the kernels never write shows."""
     lg = to_dev(torch, logits_np).to(W.torch_dtype(dtype))
     if poison:
         W.poison_padding(lg, tl, ul)
+    grad_out = None
+    if need_grad:
+        gdt = W.torch_dtype(grad_dtype or dtype)
+        grad_out = torch.full(lg.shape, float("nan"), dtype=gdt, device=lg.device)
     loss, grad = pkg.rnnt_loss(lg, to_dev(torch, labels), to_dev(torch, tl), to_dev(torch, ul), blank=blank,
-                               variant=variant, need_grad=need_grad,
+                               variant=variant, need_grad=need_grad, grad_out=grad_out,
                                grad_dtype=None if grad_dtype is None else W.torch_dtype(grad_dtype))
     torch.cuda.synchronize()
     seen = lg.float().cpu().numpy().astype(np.float64)
@@ -321,8 +326,10 @@ def full_size_case(torch, pkg, name, loss_utts, grad_utts, grad_dtype=None):
     tl, ul, labels = W.make_lengths_labels(w)
     lg = W.make_logits(w, "cuda:0")
     gdt = grad_dtype or w.dtype
+    # NaN everywhere first: every element must be written (padding rows by the fill blocks)
+    grad_out = torch.full(lg.shape, float("nan"), dtype=W.torch_dtype(gdt), device=lg.device)
     loss, grad = pkg.rnnt_loss(lg, to_dev(torch, labels), to_dev(torch, tl), to_dev(torch, ul), variant=w.variant,
-                               grad_dtype=W.torch_dtype(gdt))
+                               grad_out=grad_out, grad_dtype=W.torch_dtype(gdt))
     torch.cuda.synchronize()
     loss = loss.cpu().numpy().astype(np.float64)
     for b in sorted(set(loss_utts) | set(grad_utts)):

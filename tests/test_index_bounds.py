@@ -121,3 +121,34 @@ def test_lattice_kernel_addresses(B, T, U, V, dt):
                 assert 0 <= dc - uc < Tb and 0 <= uc <= Ub
     # the posterior kernel reads beta at diagonal t+u+1 <= T-1+U only for t < T-1 or u < U
     assert (T - 2) + U + 1 <= T - 1 + U
+
+
+@pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
+def test_gradient_kernel_fast_path_buffer(B, T, U, V, dt):
+    """Blocks on the buffer-load path: no partial chunk inside, a per-block buffer of at
+    most one tile (offsets fit 32 bits), every live chunk's offset inside it, dead chunks
+    past its end; the row-record indices of dead chunks are clamped into the records."""
+    epc = EPC[dt]
+    n_elem = B * T * (U + 1) * V
+    n_rows = B * T * (U + 1)
+    tile = 256 * 4
+    n_chunks = -(-n_elem // epc)
+    n_full = n_elem // epc
+    blocks = -(-n_chunks // tile)
+    for blk in sorted(b for b in {0, 1, blocks // 2, blocks - 2, blocks - 1} if 0 <= b < blocks):
+        tile0 = blk * tile
+        general = V < epc or (n_elem % epc != 0 and tile0 + tile > n_full)
+        if general:
+            # at most the last block holds the partial chunk
+            assert V < epc or blk == blocks - 1
+            continue
+        tile_bytes = min(tile, n_full - tile0) * 16
+        assert 0 < tile_bytes <= tile * 16 < 2**31
+        cl = np.arange(tile)
+        live = tile0 + cl < n_full
+        assert np.all((cl * 16 < tile_bytes) == live)
+        e_tile = tile0 * epc
+        r_tile, v_tile = e_tile // V, e_tile % V
+        r = np.minimum(r_tile + (v_tile + cl * epc) // V, n_rows - 1)
+        assert np.all(r >= 0) and np.all(np.minimum(r + 1, n_rows - 1) < n_rows)
+    assert 0x80000000 > tile * 16  # the out-of-range offset lies past every block's buffer
