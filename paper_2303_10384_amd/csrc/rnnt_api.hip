@@ -105,14 +105,20 @@ K1Shape k1_shape(int V) {
   return best;
 }
 
-template <typename T, int G, int NB, bool LATTICE, bool FAST>
-hipError_t launch_k1_g(PopulateParams p, hipStream_t stream) {
-  // one block per anti-diagonal (split only past kMaxRowsPerBlock units)
+// one block per anti-diagonal (split only past kMaxRowsPerBlock units)
+void k1_blocking(PopulateParams& p) {
   p.rows_per_block = p.U_max + 1 < kMaxRowsPerBlock ? p.U_max + 1 : kMaxRowsPerBlock;
   p.n_ublk = (p.U_max + 1 + p.rows_per_block - 1) / p.rows_per_block;
+}
+
+template <typename T, int G, int NB, bool LATTICE, bool FAST>
+hipError_t launch_k1_g(PopulateParams p, hipStream_t stream) {
+  k1_blocking(p);
   const int64_t blocks = static_cast<int64_t>(p.B) * (p.T_max + p.U_max) * p.n_ublk;
-  if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((k1_populate<T, G, NB, LATTICE, FAST>), dim3(static_cast<uint32_t>(blocks)), dim3(256), 0,
+  const int64_t runs = (blocks + kXcdRun - 1) / kXcdRun;  // whole rounds of the XCD-major numbering
+  const int64_t grid = (runs + kXcds - 1) / kXcds * kXcds * kXcdRun;
+  if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL((k1_populate<T, G, NB, LATTICE, FAST>), dim3(static_cast<uint32_t>(grid)), dim3(256), 0,
                      stream, p);
   return hipGetLastError();
 }
@@ -128,10 +134,18 @@ hipError_t launch_k1_nb(int nb, const PopulateParams& p, hipStream_t stream) {
   }
 }
 
+// A block's rows on one diagonal lie U_max rows apart; the fast path addresses
+// them through one buffer resource with 32-bit offsets.
+bool k1_span_fits(PopulateParams p, int elem_bytes) {
+  k1_blocking(p);
+  const int64_t rows = static_cast<int64_t>(p.rows_per_block - 1) * p.U_max + 1;
+  return rows * p.V * elem_bytes + 64 < 0x7fffffffLL;
+}
+
 template <typename T, bool LATTICE>
 hipError_t launch_k1(const PopulateParams& p, hipStream_t stream) {
   const K1Shape ks = k1_shape<T>(p.V);
-  if (!ks.fast) return launch_k1_g<T, 64, 5, LATTICE, false>(p, stream);
+  if (!ks.fast || !k1_span_fits(p, static_cast<int>(sizeof(T)))) return launch_k1_g<T, 64, 5, LATTICE, false>(p, stream);
   switch (ks.G) {
     case 8: return launch_k1_nb<T, 8, LATTICE>(ks.NB, p, stream);
     case 16: return launch_k1_nb<T, 16, LATTICE>(ks.NB, p, stream);

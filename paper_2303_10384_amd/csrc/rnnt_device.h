@@ -164,6 +164,7 @@ struct ElemTraits<float> {
                       __float_as_uint(f[3]));
   }
   __device__ static __forceinline__ float load1(const float* p) { return *p; }
+  __device__ static __forceinline__ float from_bits(uint32_t b) { return __uint_as_float(b); }
   __device__ static __forceinline__ void store1(float* p, float v) { *p = v; }
 };
 
@@ -199,6 +200,7 @@ struct ElemTraits<bf16_t> {
     return make_uint4(w[0], w[1], w[2], w[3]);
   }
   __device__ static __forceinline__ float load1(const bf16_t* p) { return bf16_to_f32(p->bits); }
+  __device__ static __forceinline__ float from_bits(uint32_t b) { return bf16_to_f32(b & 0xffffu); }
   __device__ static __forceinline__ void store1(bf16_t* p, float v) {
     p->bits = static_cast<uint16_t>(f32_to_bf16_rne(v));
   }
@@ -241,7 +243,36 @@ struct ElemTraits<f16_t> {
     return make_uint4(w[0], w[1], w[2], w[3]);
   }
   __device__ static __forceinline__ float load1(const f16_t* p) { return f16_to_f32(p->bits); }
+  __device__ static __forceinline__ float from_bits(uint32_t b) { return f16_to_f32(b & 0xffffu); }
   __device__ static __forceinline__ void store1(f16_t* p, float v) { p->bits = static_cast<uint16_t>(f32_to_f16(v)); }
 };
+
+// ---- raw buffer loads ------------------------------------------------------
+// A buffer resource covers [base, base + bytes); a load at an offset at or past
+// `bytes` returns zero without a memory access.  Loads issued unconditionally
+// with such offsets for lanes that need nothing keep the compiler's wait counts
+// exact (a load under a branch makes every later wait a full drain).
+constexpr int kBufferWord3 = 0x00020000;               // raw buffer, 32-bit data format (gfx9 family)
+constexpr int kOutOfRange = static_cast<int>(0x80000000u);  // past any buffer made here (< 2^31 bytes)
+constexpr int kBufferNT = 2;                           // cache-policy bits: nontemporal
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_buffer(const void* base, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0), static_cast<int>(bytes),
+                                           kBufferWord3);
+}
+
+template <bool NT>
+__device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, NT ? kBufferNT : 0);
+}
+
+// One element of type T (4 or 2 bytes) at byte offset `off`, widened to float.
+template <typename T>
+__device__ __forceinline__ float buffer_load_elem(__amdgpu_buffer_rsrc_t r, int off) {
+  if constexpr (sizeof(T) == 4)
+    return ElemTraits<T>::from_bits(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+  else
+    return ElemTraits<T>::from_bits(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
+}
 
 }  // namespace rnnt

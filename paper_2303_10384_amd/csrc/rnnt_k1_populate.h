@@ -18,19 +18,30 @@
 //    (the populate step on its own).
 //
 // Mapping: a block owns up to `rows_per_block` consecutive units u of one
-// anti-diagonal d of one utterance, so the lattice-form writes of a block are
-// one contiguous run.  A group of G lanes reads one row as aligned 16-byte
-// chunks.  The chunks entirely inside the row ("interior") are spread NB per
-// lane (G and NB picked from V so that G*NB just covers them) and need no
-// element masks: a lane with no chunk of its own reloads an interior chunk,
-// which cannot raise the maximum, and drops it from the sum with one select.
-// The at most two chunks that straddle the row's ends go to lanes 0 and 1 with
-// element masks.  All loads are issued, unconditionally, before any value is
-// used.  Then two passes over the registers: the group maximum (DPP
-// reduction), then the sum of 2^(z*log2 e - max*log2 e) per lane in float32
-// and across the group in float64.  Rows longer than 64 * 5 interior chunks
-// take a batched path with a running (max, sum) per lane; a row whose last
-// chunk runs past the end of the tensor reads element-wise.
+// anti-diagonal d of one utterance; blocks are numbered so that consecutive
+// diagonals of an utterance run on the same XCD (dispatch deals blocks to the 8
+// XCDs round robin), where rows (t, u) and (t, u+1), adjacent in memory but on
+// diagonals d and d+1, share the L2 copy of the line between them.  A group of
+// G lanes reads one row as aligned 16-byte chunks.  The chunks entirely inside
+// the row ("interior") are spread NB per lane (G and NB picked from V so that
+// G*NB just covers them) and need no element masks: a lane with no chunk of its
+// own reloads an interior chunk, which cannot raise the maximum, and drops it
+// from the sum with one select.  The at most two chunks that straddle the
+// row's ends go to lanes 0 and 1 with element masks.  Then two passes over the
+// registers: the group maximum (DPP reduction), then the sum of
+// 2^(z*log2 e - max*log2 e) per lane in float32 and across the group in
+// float64.
+//
+// Fast path (every block whose rows lie in whole chunks): the loads of a
+// group's next row are issued before its current row is reduced, as buffer
+// loads on a per-block buffer resource; a row past the block's last gets
+// offsets past the buffer's end (zeros, no memory access), so every load is
+// issued unconditionally and the compiler's wait counts stay exact.  Results
+// go to LDS and leave the block in one contiguous copy at its end, so no
+// global store sits in the row loop either.  Otherwise (rows longer than
+// 64 * 5 interior chunks, a block reaching the tensor's final partial chunk,
+// or a block spanning 2 GB or more) a general loop with a running (max, sum)
+// per lane and element masks.
 #pragma once
 
 #include "rnnt_device.h"
@@ -80,48 +91,85 @@ __device__ __forceinline__ void merge_batch(const float (&x)[N], float& mloc, fl
 
 __device__ __forceinline__ double clamp_no_arc(double x) { return x < kNoArc ? kNoArc : x; }  // NaN stays NaN
 
-// Row statistics of the common case: the row's interior chunks fit NB per
-// lane.  Returns (group max, group sum of exp(z - max)) in every lane.
-template <typename T, int G, int NB>
-__device__ __forceinline__ void row_stats_fast(const T* __restrict__ base, int64_t c0, int mis, int nch, int V,
-                                               int lg, float& mg, double& sg) {
-  constexpr int EPC = ElemTraits<T>::kPerChunk;
-  const float kNegInf = -__builtin_inff();
-  const uint4* __restrict__ cbase = reinterpret_cast<const uint4*>(base);
-  const bool first_partial = mis != 0;
-  const bool last_partial = ((mis + V) % EPC) != 0;
-  const int kf = first_partial ? 1 : 0;                    // first interior chunk
-  const int kl = nch - 1 - (last_partial ? 1 : 0);         // last interior chunk
-  const int n_int = kl - kf + 1;                           // may be <= 0 for tiny rows
-  // boundary chunks: lane 0 takes the first, lane 1 the last (once if they coincide)
-  const int kb0 = first_partial ? 0 : -1;
-  const int kb1 = (last_partial && nch - 1 != kb0) ? nch - 1 : -1;
-  const int kbnd = (lg == 0) ? kb0 : (lg == 1 ? kb1 : -1);
+// Geometry of the row a group handles in one iteration of the fast path.
+struct RowGeom {
+  bool live;   // a row of the block (else: every load is out of range)
+  int j;       // number of the row in the block (0 if not live)
+  int u;       // unit of the row
+  int mis;     // elements of the row's first chunk before the row starts
+  int nch;     // chunks touched by the row
+  int off0;    // byte offset of the row's first chunk in the block's buffer
+  int y;       // label y_{u+1}, or kNoLabel
+};
 
-  uint4 raw[NB];
-  const int kint_hi = n_int > 0 ? kl : 0;
-  const int kint_lo = n_int > 0 ? kf : 0;
+template <typename T, int NB>
+struct RowRegs {
+  u32x4 raw[NB];  // interior chunks
+  u32x4 rawb;     // boundary chunk (lanes 0 and 1)
+  float zb, zy;   // z[blank], z[y]
+};
+
+// Issue every load of one row (all lanes, unconditionally).  Offsets are
+// unsigned: a row that is not live starts at kOutOfRange, and every offset
+// derived from it stays at or above 2^31, past the buffer.
+template <typename T, int G, int NB>
+__device__ __forceinline__ void issue_row(__amdgpu_buffer_rsrc_t rsrc, const RowGeom& g, int V, int blank, int lg,
+                                          RowRegs<T, NB>& R) {
+  constexpr int EPC = ElemTraits<T>::kPerChunk;
+  constexpr uint32_t S = sizeof(T);
+  const bool first_partial = g.mis != 0;
+  const bool last_partial = ((g.mis + V) % EPC) != 0;
+  const int kf = first_partial ? 1 : 0;
+  const int kl = g.nch - 1 - (last_partial ? 1 : 0);
+  const int kint_lo = kl >= kf ? kf : 0;
+  const int kint_hi = kl >= kf ? kl : 0;
+  const uint32_t rb = g.live ? static_cast<uint32_t>(g.off0) : static_cast<uint32_t>(kOutOfRange);
 #pragma unroll
   for (int q = 0; q < NB; ++q) {
     const int k = min(max(kf + q * G + lg, kint_lo), kint_hi);
-    raw[q] = load16<kK1StreamLoads>(cbase + c0 + k);
+    R.raw[q] = buffer_load16<kK1StreamLoads>(rsrc, static_cast<int>(rb + static_cast<uint32_t>(k) * 16u));
   }
-  const uint4 rawb = load16<kK1StreamLoads>(cbase + c0 + max(kbnd, 0));
+  const int kb0 = first_partial ? 0 : -1;
+  const int kb1 = (last_partial && g.nch - 1 != kb0) ? g.nch - 1 : -1;
+  const int kbnd = (lg == 0) ? kb0 : (lg == 1 ? kb1 : -1);
+  const uint32_t ob = kbnd >= 0 ? rb + static_cast<uint32_t>(kbnd) * 16u : static_cast<uint32_t>(kOutOfRange);
+  R.rawb = buffer_load16<kK1StreamLoads>(rsrc, static_cast<int>(ob));
+  // the same address in every lane of the group: one request, a line the chunk loads bring in
+  R.zb = buffer_load_elem<T>(rsrc, static_cast<int>(rb + static_cast<uint32_t>(g.mis + blank) * S));
+  const bool y_ok = g.y >= 0 && g.y < V;
+  const uint32_t oy = y_ok ? rb + static_cast<uint32_t>(g.mis + g.y) * S : static_cast<uint32_t>(kOutOfRange);
+  R.zy = buffer_load_elem<T>(rsrc, static_cast<int>(oy));
+}
+
+// (group max, group sum of exp(z - max)) of a row from its registers, in every lane.
+template <typename T, int G, int NB>
+__device__ __forceinline__ void reduce_row(const RowRegs<T, NB>& R, const RowGeom& g, int V, int lg, float& mg,
+                                           double& sg) {
+  constexpr int EPC = ElemTraits<T>::kPerChunk;
+  const float kNegInf = -__builtin_inff();
+  const bool first_partial = g.mis != 0;
+  const bool last_partial = ((g.mis + V) % EPC) != 0;
+  const int kf = first_partial ? 1 : 0;
+  const int kl = g.nch - 1 - (last_partial ? 1 : 0);
+  const int n_int = kl - kf + 1;  // may be <= 0 for tiny rows
+  const int kb0 = first_partial ? 0 : -1;
+  const int kb1 = (last_partial && g.nch - 1 != kb0) ? g.nch - 1 : -1;
+  const int kbnd = (lg == 0) ? kb0 : (lg == 1 ? kb1 : -1);
 
   float xb[EPC];
   {
     float f[EPC];
-    ElemTraits<T>::unpack(rawb, f);
+    ElemTraits<T>::unpack(make_uint4(R.rawb.x, R.rawb.y, R.rawb.z, R.rawb.w), f);
 #pragma unroll
     for (int j = 0; j < EPC; ++j) {
-      const int v = kbnd * EPC + j - mis;
+      const int v = kbnd * EPC + j - g.mis;
       xb[j] = (kbnd >= 0 && v >= 0 && v < V) ? f[j] : kNegInf;
     }
   }
   float x[NB * EPC];
 #pragma unroll
-  for (int q = 0; q < NB; ++q) ElemTraits<T>::unpack(raw[q], x + q * EPC);
-
+  for (int q = 0; q < NB; ++q) ElemTraits<T>::unpack(make_uint4(R.raw[q].x, R.raw[q].y, R.raw[q].z, R.raw[q].w),
+                                                     x + q * EPC);
   // pass 1: maximum (interior duplicates are harmless; no interior chunks -> skip them)
   float m = kNegInf;
 #pragma unroll
@@ -194,85 +242,165 @@ __device__ __forceinline__ void row_stats_general(const T* __restrict__ base, in
   sg = group_reduce<G, SumOp>(static_cast<double>(sloc * scale), 0.0);
 }
 
-// FAST: rows take row_stats_fast (the launcher checks that NB*G covers every
-// row's interior chunks); otherwise row_stats_general.
-constexpr int kMaxRowsPerBlock = 1024;
+// FAST: blocks whose rows lie in whole chunks take the pipelined path (the
+// launcher checks that NB*G covers every row's interior chunks and that a block's
+// rows span less than 2 GB); others take row_stats_general.
+constexpr int kMaxRowsPerBlock = 256;
+constexpr int kXcds = 8;
+#ifndef RNNT_K1_XCD_RUN
+#define RNNT_K1_XCD_RUN 16
+#endif
+constexpr int kXcdRun = RNNT_K1_XCD_RUN;  // consecutive blocks per XCD turn
+
 
 template <typename T, int G, int NB, bool LATTICE, bool FAST>
 __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
-  constexpr int GROUPS = 256 / G;      // rows in flight per block
+  constexpr int GROUPS = 256 / G;  // rows in flight per block
+  // per row: the label, then the group results (max, sum of exp, z[blank], z[y])
   __shared__ int s_label[kMaxRowsPerBlock];
+  __shared__ float s_max[kMaxRowsPerBlock];
+  __shared__ double s_sum[kMaxRowsPerBlock];
+  __shared__ float s_zb[kMaxRowsPerBlock];
+  __shared__ float s_zy[kMaxRowsPerBlock];
 
   const int ND = p.T_max + p.U_max;  // anti-diagonals per utterance
-  const int diag = blockIdx.x / p.n_ublk;  // b * ND + d
-  const int ublk = blockIdx.x - diag * p.n_ublk;
+  // block order: runs of kXcdRun consecutive (b, d, ublk) are dealt to the XCDs in
+  // turn; XCD x holds physical blocks x, x+8, ..., and its k-th block is element
+  // k % kXcdRun of its (k / kXcdRun)-th run
+  const int64_t n_blocks = static_cast<int64_t>(p.B) * ND * p.n_ublk;
+  const int64_t kx = blockIdx.x / kXcds;
+  const int64_t lb = ((kx / kXcdRun) * kXcds + blockIdx.x % kXcds) * kXcdRun + kx % kXcdRun;
+  if (lb >= n_blocks) return;
+  const int diag = static_cast<int>(lb / p.n_ublk);  // b * ND + d
+  const int ublk = static_cast<int>(lb - static_cast<int64_t>(diag) * p.n_ublk);
   const int b = diag / ND;
   const int d = diag - b * ND;
   const int Tb = p.logit_lens[b];
   const int Ub = p.label_lens[b];
   if (Tb < 1 || Tb > p.T_max || Ub < 0 || Ub > p.U_max) return;
   const int u_first = ublk * p.rows_per_block;
-  const int u_lo = max(u_first, d - (Tb - 1));           // t = d - u <= T_b - 1
+  const int u_lo = max(u_first, d - (Tb - 1));  // t = d - u <= T_b - 1
   const int u_hi = min(u_first + p.rows_per_block, min(d, Ub) + 1);
   if (u_lo >= u_hi) return;
+  const int n_rows = u_hi - u_lo;
 
   const int lg = threadIdx.x % G;  // lane inside the row group
   const int grp = threadIdx.x / G;
   // the block's labels go through LDS, so no label load waits inside the row loop
-  for (int i = threadIdx.x; i < u_hi - u_first; i += blockDim.x) {
-    const int u = u_first + i;
+  for (int i = threadIdx.x; i < n_rows; i += blockDim.x) {
+    const int u = u_lo + i;
     s_label[i] = (u < Ub) ? p.labels[static_cast<int64_t>(b) * p.U_max + u] : kNoLabel;
   }
   __syncthreads();
 
   const T* __restrict__ base = static_cast<const T*>(p.logits);
   const int64_t full_chunks = p.n_elem / EPC;
+  const int U1 = p.U_max + 1;
+  // row j of the block is unit u_lo + j; rows of a diagonal lie U_max rows apart,
+  // the first (u_lo) at the highest address
+  const int64_t row_lo = (static_cast<int64_t>(b) * p.T_max + (d - u_lo)) * U1 + u_lo;
+  const int64_t e_first = row_lo * p.V;
+  const int64_t row_step = static_cast<int64_t>(p.U_max) * p.V;  // elements between consecutive rows
+  const int64_t c_end = (e_first + p.V + EPC - 1) / EPC;
+  const int64_t e_base = e_first - (n_rows - 1) * row_step;  // the lowest row (u_hi - 1)
+  const int64_t c_base = e_base / EPC;
+  const int n_iter = (n_rows + GROUPS - 1) / GROUPS;
 
-  // all lanes of a wave stay in the loop (the group reductions use every lane);
-  // a group past the block's last row computes a row it does not write
-  const int n_iter = (u_hi - u_lo + GROUPS - 1) / GROUPS;
-  for (int it = 0; it < n_iter; ++it) {
-    const int u_raw = u_lo + it * GROUPS + grp;
-    const bool live = u_raw >= u_lo && u_raw < u_hi;
-    const int u = live ? u_raw : u_lo;  // dead groups recompute the block's first row
-    const int t = d - u;
-    const int64_t row = (static_cast<int64_t>(b) * p.T_max + t) * (p.U_max + 1) + u;
-    const int64_t e0 = row * p.V;
-    const int64_t c0 = e0 / EPC;
-    const int mis = static_cast<int>(e0 - c0 * EPC);
-    const int nch = (mis + p.V + EPC - 1) / EPC;
-    const int y = s_label[u - u_first];
-    const bool y_ok = (y >= 0 && y < p.V);
-    // z[blank], z[y]: the same address in every lane of the group (one request,
-    // a line the row's chunk loads bring in anyway), issued ahead of them
-    const float zb = ElemTraits<T>::load1(base + e0 + p.blank);
-    const float zy = ElemTraits<T>::load1(base + e0 + (y_ok ? y : 0));
-
-    float mg;
-    double sg;
-    if (FAST && c0 + nch <= full_chunks)
-      row_stats_fast<T, G, NB>(base, c0, mis, nch, p.V, lg, mg, sg);
-    else
-      row_stats_general<T, G, NB>(base, e0, c0, mis, nch, p.V, full_chunks, lg, mg, sg);
-
-    if (live && lg == 0) {
-      const double lse = static_cast<double>(mg) + log(sg);
-      const double lpb = static_cast<double>(zb) - lse;
-      const double lpl = (u < Ub) ? (y_ok ? static_cast<double>(zy) - lse : __builtin_nan("")) : -__builtin_inf();
-      if (LATTICE) {
-        const int64_t sc = static_cast<int64_t>(diag) * (p.U_max + 1) + u;
-        const bool blank_arc = (t < Tb - 1) || (u == Ub);  // absent: last frame below the top row
-        double2 w;
-        w.x = blank_arc ? clamp_no_arc(lpb * kLog2eD) : kNoArc;
-        w.y = (u < Ub) ? clamp_no_arc(lpl * kLog2eD) : kNoArc;
-        p.lp2[sc] = w;
-        p.lse2[sc] = static_cast<float>(lse * kLog2eD);
-      } else {
-        if (p.lse_out) p.lse_out[row] = lse;
-        p.lp_blank_out[row] = lpb;
-        p.lp_label_out[row] = lpl;
+  if (FAST && c_end <= full_chunks) {
+    const __amdgpu_buffer_rsrc_t rsrc =
+        make_buffer(reinterpret_cast<const uint4*>(base) + c_base, (c_end - c_base) * 16);
+    // element offset of row j from the block's first chunk (fits 32 bits: the span is checked)
+    const int e_rel0 = static_cast<int>(e_first - c_base * EPC);
+    const int step = static_cast<int>(row_step);
+    auto geom = [&](int it) {
+      RowGeom g;
+      const int j = it * GROUPS + grp;
+      g.live = j < n_rows;
+      g.j = g.live ? j : 0;
+      const int e_rel = e_rel0 - g.j * step;
+      g.mis = e_rel & (EPC - 1);
+      g.nch = (g.mis + p.V + EPC - 1) / EPC;
+      g.off0 = (e_rel - g.mis) * static_cast<int>(sizeof(T));
+      g.y = s_label[g.j];
+      return g;
+    };
+    auto finish = [&](const RowRegs<T, NB>& R, const RowGeom& g) {
+      float mg;
+      double sg;
+      reduce_row<T, G, NB>(R, g, p.V, lg, mg, sg);
+      if (g.live && lg == 0) {
+        s_max[g.j] = mg;
+        s_sum[g.j] = sg;
+        s_zb[g.j] = R.zb;
+        s_zy[g.j] = R.zy;
       }
+    };
+    // two register sets in turn (a copy between them would wait for the loads in flight)
+    RowGeom g0 = geom(0), g1;
+    RowRegs<T, NB> R0, R1;
+    issue_row<T, G, NB>(rsrc, g0, p.V, p.blank, lg, R0);
+    for (int it = 0; it < n_iter; it += 2) {
+      g1 = geom(it + 1);  // past the block's rows: not live, no memory access
+      issue_row<T, G, NB>(rsrc, g1, p.V, p.blank, lg, R1);
+      __builtin_amdgcn_sched_barrier(0);  // the next row's loads go out before this row is reduced
+      finish(R0, g0);
+      g0 = geom(it + 2);
+      issue_row<T, G, NB>(rsrc, g0, p.V, p.blank, lg, R0);
+      __builtin_amdgcn_sched_barrier(0);
+      finish(R1, g1);
+    }
+  } else {
+    // all lanes of a wave stay in the loop (the group reductions use every lane);
+    // a group past the block's last row computes a row it does not keep
+    for (int it = 0; it < n_iter; ++it) {
+      const int j_raw = it * GROUPS + grp;
+      const bool live = j_raw < n_rows;
+      const int j = live ? j_raw : 0;
+      const int64_t e0 = e_first - j * row_step;
+      const int64_t c0 = e0 / EPC;
+      const int mis = static_cast<int>(e0 - c0 * EPC);
+      const int nch = (mis + p.V + EPC - 1) / EPC;
+      const int y = s_label[j];
+      const bool y_ok = (y >= 0 && y < p.V);
+      const float zb = ElemTraits<T>::load1(base + e0 + p.blank);
+      const float zy = ElemTraits<T>::load1(base + e0 + (y_ok ? y : 0));
+      float mg;
+      double sg;
+      row_stats_general<T, G, NB>(base, e0, c0, mis, nch, p.V, full_chunks, lg, mg, sg);
+      if (live && lg == 0) {
+        s_max[j] = mg;
+        s_sum[j] = sg;
+        s_zb[j] = zb;
+        s_zy[j] = zy;
+      }
+    }
+  }
+  __syncthreads();
+
+  // one thread per row: lse = max + ln(sum), the arc weights in float64, and the
+  // block's results leave in one pass (a contiguous run in the lattice form)
+  for (int j = threadIdx.x; j < n_rows; j += blockDim.x) {
+    const int u = u_lo + j;
+    const int t = d - u;
+    const int y = s_label[j];
+    const bool y_ok = y >= 0 && y < p.V;
+    const double lse = static_cast<double>(s_max[j]) + log(s_sum[j]);
+    const double lpb = static_cast<double>(s_zb[j]) - lse;
+    const double lpl = (u < Ub) ? (y_ok ? static_cast<double>(s_zy[j]) - lse : __builtin_nan("")) : -__builtin_inf();
+    if (LATTICE) {
+      const int64_t sc = static_cast<int64_t>(diag) * U1 + u;
+      const bool blank_arc = (t < Tb - 1) || (u == Ub);  // absent: last frame below the top row
+      double2 w;
+      w.x = blank_arc ? clamp_no_arc(lpb * kLog2eD) : kNoArc;
+      w.y = (u < Ub) ? clamp_no_arc(lpl * kLog2eD) : kNoArc;
+      p.lp2[sc] = w;
+      p.lse2[sc] = static_cast<float>(lse * kLog2eD);
+    } else {
+      const int64_t row = row_lo - static_cast<int64_t>(j) * p.U_max;
+      if (p.lse_out) p.lse_out[row] = lse;
+      p.lp_blank_out[row] = lpb;
+      p.lp_label_out[row] = lpl;
     }
   }
 }

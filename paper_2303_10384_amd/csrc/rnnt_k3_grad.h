@@ -108,10 +108,6 @@ __device__ __forceinline__ void grad_chunks_general(const GradParams& p, int64_t
   }
 }
 
-constexpr int kBufferWord3 = 0x00020000;  // raw buffer, 32-bit format (gfx9 family)
-constexpr int kOutOfRange = static_cast<int>(0x80000000u);
-constexpr int kBufferNT = RNNT_K3_NT_LOAD ? 2 : 0;  // cache policy bits of a buffer load: nt
-
 // Tin: logits element type; Tout: gradient element type (Tin or float).
 // A block covers kGradTileChunks consecutive chunks.  Every block but the one
 // holding the tensor's final partial chunk takes the fast path, in three phases
@@ -150,9 +146,7 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
   }
   __builtin_amdgcn_sched_barrier(0);  // all record loads issue before any of them is used
   const int64_t tile_bytes = min<int64_t>(kGradTileChunks, n_full - tile0) * 16;
-  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint4*>(static_cast<const uint4*>(p.logits) + tile0), static_cast<short>(0),
-      static_cast<int>(tile_bytes), kBufferWord3);
+  const __amdgpu_buffer_rsrc_t rsrc = make_buffer(static_cast<const uint4*>(p.logits) + tile0, tile_bytes);
   u32x4 raw[Q];
   bool store[Q];
 #pragma unroll
@@ -163,7 +157,7 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
     const bool zero = ri0[q].label == kZeroRow && (!split || ri1[q].label == kZeroRow);
     store[q] = live;
     const int off = (live && !zero) ? cl * 16 : kOutOfRange;
-    raw[q] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, kBufferNT);
+    raw[q] = buffer_load16<kK3StreamLoads>(rsrc, off);
   }
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll

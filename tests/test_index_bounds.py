@@ -32,11 +32,26 @@ def test_populate_kernel_addresses(B, T, U, V, dt):
     epc = EPC[dt]
     n_elem = B * T * (U + 1) * V
     G, NB, fast = k1_shape(V, epc)
-    rows_per_block = min(U + 1, 1024)
+    rows_per_block = min(U + 1, 256)
     n_ublk = -(-(U + 1) // rows_per_block)
     ND = T + U
-    blocks = B * ND * n_ublk
-    assert blocks < 2**31
+    DPB = 1  # anti-diagonals per block
+    n_dblk = -(-ND // DPB)
+    blocks = B * n_dblk * n_ublk
+    run = 16  # consecutive blocks per XCD turn
+    grid = -(-(-(-blocks // run)) // 8) * 8 * run
+    assert grid < 2**31
+    # XCD-major numbering: physical block i (XCD i % 8, its k-th block, k = i // 8) ->
+    # logical ((k // run) * 8 + i % 8) * run + k % run, a bijection onto [0, blocks) once
+    # the logical numbers >= blocks (the grid's round-up) are dropped
+    i = np.arange(grid, dtype=np.int64)
+    k = i // 8
+    lb = ((k // run) * 8 + i % 8) * run + k % run
+    kept = np.sort(lb[lb < blocks])
+    assert np.array_equal(kept, np.arange(blocks))
+    span_rows = (DPB - 1) * (U + 1) + (rows_per_block - 1) * U + 1
+    span_fits = span_rows * V * {"f32": 4, "bf16": 2, "f16": 2}[dt] + 64 < 0x7fffffff
+    fast = fast and span_fits
     # every (b, d, u) a block can reach with full lengths: t = d - u in [0, T), u in [0, U]
     b, d, u = np.meshgrid(np.arange(B), np.arange(ND), np.arange(U + 1), indexing="ij")
     t = d - u
@@ -61,6 +76,42 @@ def test_populate_kernel_addresses(B, T, U, V, dt):
         assert np.all(np.maximum(kl, 0) < nch) and np.all(kf <= nch)
     # only rows reaching into the tensor's final partial chunk read element-wise
     assert np.all((e0 + V > (n_elem // epc) * epc)[~whole])
+    if fast:
+        # per-block buffer: from the block's lowest row to the end of its highest; the kernel
+        # finds them as the largest-u / smallest-u row of each of its diagonals
+        key = (b.astype(np.int64) * n_dblk + d // DPB) * n_ublk + u // rows_per_block
+        order = np.lexsort((u, d, key))
+        ks, ds, us, rs = key[order], d[order], u[order], row[order]
+        starts = np.r_[0, np.nonzero(np.diff(ks))[0] + 1]
+        r_lo_true = np.minimum.reduceat(rs, starts)
+        r_hi_true = np.maximum.reduceat(rs, starts)
+        dstarts = np.r_[0, np.nonzero(np.diff(ks * (ND + 1) + ds))[0] + 1]
+        dblk = np.searchsorted(starts, dstarts, side="right") - 1
+        d_of = ds[dstarts]
+        u_max = np.maximum.reduceat(us, dstarts)
+        u_min = np.minimum.reduceat(us, dstarts)
+        bb = b[order][dstarts].astype(np.int64)
+        cand_lo = (bb * T + d_of - u_max) * (U + 1) + u_max
+        cand_hi = (bb * T + d_of - u_min) * (U + 1) + u_min
+        r_lo = np.full(len(starts), np.iinfo(np.int64).max)
+        r_hi = np.full(len(starts), -1)
+        np.minimum.at(r_lo, dblk, cand_lo)
+        np.maximum.at(r_hi, dblk, cand_hi)
+        assert np.array_equal(r_lo, r_lo_true) and np.array_equal(r_hi, r_hi_true)
+        c_base = (r_lo * V) // epc
+        c_end = (r_hi * V + V + epc - 1) // epc
+        assert np.all((c_end - c_base) * 16 < 2**31)
+        blk = np.repeat(np.arange(len(starts)), np.diff(np.r_[starts, len(ks)]))
+        cs = c0[order]
+        off0 = (cs - c_base[blk]) * 16
+        assert np.all(off0 >= 0) and np.all(off0 + nch[order] * 16 <= (c_end - c_base)[blk] * 16)
+        # rows per block fit the LDS arrays
+        assert np.diff(np.r_[starts, len(ks)]).max() <= DPB * 256
+        # the kernel's 32-bit element offsets: row j at e_rel0 - j * U*V from the block's first chunk
+        e_rel = e0[order] - c_base[blk] * epc
+        assert np.all(e_rel >= 0) and np.all(e_rel * {"f32": 4, "bf16": 2, "f16": 2}[dt] < 2**31)
+        if U > 0:
+            assert U * V < 2**31
     # lattice-form writes at (b*ND + d)*(U+1) + u inside the C-cell arrays
     sc = (b.astype(np.int64) * ND + d) * (U + 1) + u
     assert sc.max() < B * ND * (U + 1) and sc.min() >= 0
