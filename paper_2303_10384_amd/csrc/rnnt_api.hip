@@ -37,7 +37,8 @@ rnnt_status_t check_shape(const rnnt_shape_t& s) {
 }
 
 // Workspace, all pieces 256-byte aligned (C = B * (T_max+U_max) * (U_max+1)
-// anti-diagonal cells, S = B * (T_max+U_max+1) * (U_max+1) score cells):
+// anti-diagonal cells, S = B * (T_max+U_max+1) * u_pad score cells, u_pad =
+// 64 * units per lane of the lattice sweep):
 //   rowinfo  B*T_max*(U_max+1) RowInfo        (rnnt_loss)
 //   lp2      C double2 {lp_blank, lp_label}    (rnnt_loss)
 //   lse2     C float                           (rnnt_loss)
@@ -53,7 +54,8 @@ Layout make_layout(const rnnt_shape_t& s, bool with_populate) {
   const size_t U1 = static_cast<size_t>(s.U_max) + 1;
   const size_t rows = static_cast<size_t>(s.B) * s.T_max * U1;
   const size_t cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max) * U1;
-  const size_t score_cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max + 1) * U1;
+  const size_t u_pad = 64 * static_cast<size_t>(units_per_lane(s.U_max + 1));
+  const size_t score_cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max + 1) * u_pad;
   Layout L{};
   size_t o = 0;
   if (with_populate) {
@@ -175,12 +177,13 @@ hipError_t launch_k2_k(const LatticeParams& p, hipStream_t stream) {
 
 template <int VAR, int MODE, bool DENSE_IN>
 hipError_t launch_k2_v(const LatticeParams& p, hipStream_t stream) {
-  const int units1 = p.U_max + 1;
-  if (units1 <= 64) return launch_k2_k<1, VAR, MODE, DENSE_IN>(p, stream);
-  if (units1 <= 128) return launch_k2_k<2, VAR, MODE, DENSE_IN>(p, stream);
-  if (units1 <= 256) return launch_k2_k<4, VAR, MODE, DENSE_IN>(p, stream);
-  if (units1 <= 512) return launch_k2_k<8, VAR, MODE, DENSE_IN>(p, stream);
-  return launch_k2_k<16, VAR, MODE, DENSE_IN>(p, stream);
+  switch (units_per_lane(p.U_max + 1)) {
+    case 1: return launch_k2_k<1, VAR, MODE, DENSE_IN>(p, stream);
+    case 2: return launch_k2_k<2, VAR, MODE, DENSE_IN>(p, stream);
+    case 4: return launch_k2_k<4, VAR, MODE, DENSE_IN>(p, stream);
+    case 8: return launch_k2_k<8, VAR, MODE, DENSE_IN>(p, stream);
+    default: return launch_k2_k<16, VAR, MODE, DENSE_IN>(p, stream);
+  }
 }
 
 template <int MODE, bool DENSE_IN>
@@ -343,6 +346,7 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
   p2.lp2 = p1.lp2;
   p2.alpha = reinterpret_cast<double*>(ws + L.alpha);
   p2.beta = reinterpret_cast<double*>(ws + L.beta);
+  p2.u_pad = 64 * units_per_lane(shape.U_max + 1);
   p2.lnp2_fwd = reinterpret_cast<double*>(ws + L.lnp);
   p2.lnp2_bwd = p2.lnp2_fwd + shape.B;
   p2.status = reinterpret_cast<int32_t*>(ws + L.status);
@@ -366,6 +370,7 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
     pb.lse2 = p1.lse2;
     pb.alpha = p2.alpha;
     pb.beta = p2.beta;
+    pb.u_pad = p2.u_pad;
     pb.lnp2_fwd = p2.lnp2_fwd;
     pb.lnp2_bwd = p2.lnp2_bwd;
     pb.n_rows = n_rows;
@@ -459,6 +464,7 @@ rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label
   p2.lp_label = lp_label;
   p2.alpha = reinterpret_cast<double*>(ws + L.alpha);
   p2.beta = reinterpret_cast<double*>(ws + L.beta);
+  p2.u_pad = 64 * units_per_lane(shape.U_max + 1);
   p2.lnp2_fwd = reinterpret_cast<double*>(ws + L.lnp);
   p2.lnp2_bwd = p2.lnp2_fwd + s.B;
   p2.status = reinterpret_cast<int32_t*>(ws + L.status);
@@ -477,6 +483,7 @@ rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label
   pb.lp_label = lp_label;
   pb.alpha = p2.alpha;
   pb.beta = p2.beta;
+  pb.u_pad = p2.u_pad;
   pb.lnp2_fwd = p2.lnp2_fwd;
   pb.lnp2_bwd = p2.lnp2_bwd;
   pb.n_rows = static_cast<int64_t>(s.B) * s.T_max * (s.U_max + 1);

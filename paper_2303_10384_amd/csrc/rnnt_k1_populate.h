@@ -282,6 +282,7 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   const int u_first = ublk * p.rows_per_block;
   const int u_lo = max(u_first, d - (Tb - 1));  // t = d - u <= T_b - 1
   const int u_hi = min(u_first + p.rows_per_block, min(d, Ub) + 1);
+  const int U1 = p.U_max + 1;
   if (u_lo >= u_hi) return;
   const int n_rows = u_hi - u_lo;
 
@@ -296,7 +297,6 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
 
   const T* __restrict__ base = static_cast<const T*>(p.logits);
   const int64_t full_chunks = p.n_elem / EPC;
-  const int U1 = p.U_max + 1;
   // row j of the block is unit u_lo + j; rows of a diagonal lie U_max rows apart,
   // the first (u_lo) at the highest address
   const int64_t row_lo = (static_cast<int64_t>(b) * p.T_max + (d - u_lo)) * U1 + u_lo;

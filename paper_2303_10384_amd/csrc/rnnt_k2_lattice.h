@@ -18,13 +18,17 @@
 // value with the neighbouring lane (a DPP whole-wave shift).  The forward and
 // backward waves of an utterance run concurrently in one block.  The weights of
 // the next PF diagonals stay in flight in registers (one contiguous run per
-// diagonal in the anti-diagonal layout of kernel 1).  No node is masked: absent
-// arcs carry kNoArc, so a node outside the utterance accumulates only kNoArc
-// or never feeds a node inside it; weights of cells outside the utterance are
-// read from a clamped cell inside it.  The wild-card arcs cost two running
-// log-sums held by the lanes owning u = 0 and u = U.  Every lane stores every
-// step (nodes past U_max or past the last diagonal go to a scratch row), so no
-// load or store sits under a branch.
+// diagonal in the anti-diagonal layout of kernel 1).  No node is masked:
+// absent arcs carry kNoArc, so a node outside the utterance accumulates only
+// kNoArc or never feeds a node inside it; weights of cells outside the
+// utterance are read from a cell clamped into it (a wave-uniform diagonal and
+// two per-lane min/max on the unit), so every value stays finite.  alpha and
+// beta rows are 64*K wide, one column per lane slot, and the
+// steps past the utterance's last diagonal (or before the first) store into
+// spare rows, so every load and store goes through a wave-uniform row pointer
+// plus a constant lane offset and none sits under a branch.  The wild-card
+// arcs cost two running log-sums held by the lanes owning u = 0 and u = U,
+// updated under wave-uniform conditions on the diagonal.
 //
 // Kernel 2b, one thread per padded row (t, u):
 //   occ_blank(t,u) = 2^(alpha(t,u) + lp_blank(t,u) + beta(t+1,u) - log2 P)   (t < T-1)
@@ -51,8 +55,9 @@ struct LatticeParams {
   const double2* lp2;       // kernel 1's lattice form (log2 units, by diagonal, kNoArc marks), or
   const double* lp_blank;   // dense natural-log weights (B, T_max, U_max+1)
   const double* lp_label;
-  double* alpha;  // (B, T_max+U_max+1, U_max+1), by diagonal, log2 units; last row per utterance: scratch
+  double* alpha;  // (B, T_max+U_max+1, u_pad), by diagonal, log2 units; rows past D_b + 1: spare
   double* beta;
+  int32_t u_pad;     // row width of alpha / beta: 64 * units per lane
   double* lnp2_fwd;  // (B) log2 P from the forward wave
   double* lnp2_bwd;  // (B) beta(0,0)
   int32_t* status;   // (B) 0: good, 1: bad data
@@ -103,6 +108,23 @@ __device__ __forceinline__ double wave_shift_down(double x, double fill) {
   return __hiloint2double(hi, lo);
 }
 
+// Number of units a lane owns so that 64 lanes cover U_max + 1 units.
+__host__ __device__ constexpr int units_per_lane(int units1) {
+  return units1 <= 64 ? 1 : units1 <= 128 ? 2 : units1 <= 256 ? 4 : units1 <= 512 ? 8 : 16;
+}
+
+// The value of unit u in this lane's slots (x[k] holds unit lane*K + k), or
+// `other` in lanes not owning u.  Selecting by the per-lane unit, never by a
+// slot number, keeps every index into x static (a run-time slot index would
+// move the array out of registers).
+template <int K>
+__device__ __forceinline__ double at_unit(const double (&x)[K], int lane, int u, double other) {
+  double r = other;
+#pragma unroll
+  for (int k = 0; k < K; ++k) r = (lane * K + k == u) ? x[k] : r;
+  return r;
+}
+
 // VAR: 0 RNN-T, 1 W-Transducer force-final, 2 allow-ignore.
 // DENSE_IN: weights from the dense natural-log arrays instead of kernel 1.
 template <int K, int PF, int VAR, int MODE, bool DENSE_IN>
@@ -112,6 +134,7 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 128) void k2_lattice(Latti
   const int T = p.logit_lens[b];
   const int U = p.label_lens[b];
   const int U1 = p.U_max + 1;
+  const int ND = p.T_max + p.U_max;  // diagonals of the lattice form
   const double kNaN = __builtin_nan("");
 
   bool ok = (T >= 1 && T <= p.T_max && U >= 0 && U <= p.U_max);
@@ -136,33 +159,52 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 128) void k2_lattice(Latti
   const int wave = tid >> 6;
   const int lane = tid & 63;
   const int D = T - 1 + U;  // last diagonal
-  const int64_t ab0 = static_cast<int64_t>(b) * (p.T_max + p.U_max + 1) * U1;
-  const int64_t dump = static_cast<int64_t>(p.T_max + p.U_max) * U1;  // scratch row
   const int owner_top = U / K;  // lane owning u = U
+  // weights of cell (e, u) clamped into the utterance: diagonal into [0, D], then the
+  // unit into [e - (T-1), min(e, U)] (t = e - u in [0, T-1]); the row pointer is wave-uniform
+  const double2* __restrict__ w_utt = p.lp2 + static_cast<int64_t>(b) * ND * U1;
+  auto load_w = [&](int e, int k, double& wb, double& wl) {
+    if (!DENSE_IN) {
+      const int ec = min(max(e, 0), D);
+      const int uc = min(max(lane * K + k, ec - (T - 1)), min(ec, U));
+      const double2 w = w_utt[ec * U1 + uc];
+      wb = w.x;
+      wl = w.y;
+    } else {
+      load_cell<true>(p, b, e, lane * K + k, T, U, D, wb, wl);
+    }
+  };
+  // score rows: diagonals 0..D, then spare rows up to ND
+  double* __restrict__ a_utt = p.alpha + static_cast<int64_t>(b) * (ND + 1) * p.u_pad;
+  double* __restrict__ b_utt = p.beta + static_cast<int64_t>(b) * (ND + 1) * p.u_pad;
 
   // weight of the closing blank, lp_blank(T-1, U)
   double w_close, w_unused;
-  load_cell<DENSE_IN>(p, b, D, U, T, U, D, w_close, w_unused);
-  if (DENSE_IN) w_close = to_lattice(w_close, true);
+  if (!DENSE_IN) {
+    w_close = w_utt[D * U1 + U].x;
+  } else {
+    load_cell<true>(p, b, D, U, T, U, D, w_close, w_unused);
+    w_close = to_lattice(w_close, true);
+  }
 
   if (wave == 0) {
     // ---------------- forward sweep ----------------
     double a[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) a[k] = (lane * K + k == 0) ? 0.0 : kNoArc;
-    double acc_top = kNoArc;                   // log-sum of alpha(t, U), t <= T-2 (owner lane)
+    double acc_top = kNoArc;                   // log-sum of alpha(t, U), t <= T-2
     double a_top = (U == 0) ? 0.0 : kNoArc;    // alpha(T-1, U) once the sweep reaches D
     if (VAR != 0 && U == 0 && T >= 2) acc_top = 0.0;  // alpha(0, U) itself when U = 0
-    if (MODE != kLossOnly && lane == 0) p.alpha[ab0] = 0.0;
+    if (MODE != kLossOnly && lane == 0) a_utt[0] = 0.0;
 
     double rb[PF][K], rl[PF][K];
 #pragma unroll
     for (int s = 0; s < PF; ++s)
 #pragma unroll
-      for (int k = 0; k < K; ++k) load_cell<DENSE_IN>(p, b, s, lane * K + k, T, U, D, rb[s][k], rl[s][k]);
+      for (int k = 0; k < K; ++k) load_w(s, k, rb[s][k], rl[s][k]);
 
     // whole blocks of PF steps, no branch around loads or stores; the up to PF-1
-    // steps past D touch only nodes outside the utterance
+    // steps past D touch only nodes outside the utterance and store into spare rows
     for (int d0 = 1; d0 <= D; d0 += PF) {
 #pragma unroll
       for (int s = 0; s < PF; ++s) {
@@ -181,20 +223,26 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 128) void k2_lattice(Latti
         }
         const double left = wave_shift_up(el[K - 1], kNoArc);
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-          const int u = lane * K + k;
-          double n = log_add2(eb[k], k == 0 ? left : el[k > 0 ? k - 1 : 0]);
-          if (VAR != 0 && u == 0 && d <= T - 1) n = log_add2(n, 0.0);    // (0,0)->(d,0)
-          if (VAR == 1 && u == U && d == D) n = log_add2(n, acc_top);    // (t,U)->(T-1,U)
-          a[k] = n;
-          if (MODE != kLossOnly)
-            p.alpha[ab0 + (u <= p.U_max && d <= D ? static_cast<int64_t>(d) * U1 + u : dump)] = n;
-          if (u == U && d == D) a_top = n;
-          if (VAR != 0 && u == U && d >= U && d - U <= T - 2) acc_top = log_add2(acc_top, n);
+        for (int k = 0; k < K; ++k) a[k] = log_add2(eb[k], k == 0 ? left : el[k > 0 ? k - 1 : 0]);
+        // wave-uniform conditions on the diagonal; no memory access inside
+        if (VAR != 0 && d <= T - 1 && lane == 0) a[0] = log_add2(a[0], 0.0);  // (0,0)->(d,0)
+        if (d == D) {
+          if (VAR == 1) {
+#pragma unroll
+            for (int k = 0; k < K; ++k)
+              if (lane * K + k == U) a[k] = log_add2(a[k], acc_top);  // (t,U)->(T-1,U)
+          }
+          a_top = at_unit(a, lane, U, a_top);
+        }
+        if (VAR != 0 && d >= U && d - U <= T - 2) acc_top = log_add2(acc_top, at_unit(a, lane, U, kNoArc));  // alpha(d-U, U)
+        if (MODE != kLossOnly) {
+          double* __restrict__ row = a_utt + static_cast<int64_t>(min(d, D + 1)) * p.u_pad + lane * K;
+#pragma unroll
+          for (int k = 0; k < K; ++k) row[k] = a[k];
         }
 #pragma unroll
-        for (int k = 0; k < K; ++k)
-          load_cell<DENSE_IN>(p, b, d - 1 + PF, lane * K + k, T, U, D, rb[s][k], rl[s][k]);
+        for (int k = 0; k < K; ++k) load_w(d - 1 + PF, k, rb[s][k], rl[s][k]);
+        __builtin_amdgcn_sched_barrier(0);  // the prefetch stays PF steps ahead of its use
       }
     }
     if (lane == owner_top) {
@@ -209,16 +257,16 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 128) void k2_lattice(Latti
 #pragma unroll
     for (int k = 0; k < K; ++k) bv[k] = (lane * K + k == U) ? w_close : kNoArc;
     const double b_top = w_close;  // beta(T-1, U)
-    double acc0 = kNoArc;          // log-sum of beta(t, 0), t >= 1 (lane 0)
+    double acc0 = kNoArc;          // log-sum of beta(t, 0), t >= 1
     if (VAR != 0 && U == 0 && T >= 2) acc0 = w_close;
-    if (lane == owner_top) p.beta[ab0 + static_cast<int64_t>(D) * U1 + U] = w_close;
+    if (lane == owner_top) b_utt[static_cast<int64_t>(D) * p.u_pad + U] = w_close;
     double b00 = (D == 0) ? w_close : kNoArc;  // beta(0,0)
 
     double rb[PF][K], rl[PF][K];
 #pragma unroll
     for (int s = 0; s < PF; ++s)
 #pragma unroll
-      for (int k = 0; k < K; ++k) load_cell<DENSE_IN>(p, b, D - 1 - s, lane * K + k, T, U, D, rb[s][k], rl[s][k]);
+      for (int k = 0; k < K; ++k) load_w(D - 1 - s, k, rb[s][k], rl[s][k]);
 
     for (int d0 = D - 1; d0 >= 0; d0 -= PF) {
 #pragma unroll
@@ -228,28 +276,35 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 128) void k2_lattice(Latti
         double nb[K];
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-          const int u = lane * K + k;
           double wb = rb[s][k], wl = rl[s][k];
           if (DENSE_IN) {
-            const int t = d - u;
+            const int u = lane * K + k, t = d - u;
             wb = to_lattice(wb, t < T - 1 || u == U);
             wl = to_lattice(wl, u < U);
           }
           const double xb = wb + bv[k];
           const double xl = wl + (k == K - 1 ? right : bv[k + 1 < K ? k + 1 : k]);
-          double n = log_add2(xb, xl);
-          if (VAR != 0 && u == U && d >= U && d - U <= T - 2) n = log_add2(n, VAR == 1 ? b_top : 0.0);
-          if (VAR != 0 && u == 0 && d == 0) n = log_add2(n, acc0);  // (0,0)->(t,0)
-          nb[k] = n;
-          p.beta[ab0 + (u <= p.U_max && d >= 0 ? static_cast<int64_t>(d) * U1 + u : dump)] = n;
-          if (VAR != 0 && u == 0 && d >= 1 && d <= T - 1) acc0 = log_add2(acc0, n);
-          if (u == 0 && d == 0) b00 = n;
+          nb[k] = log_add2(xb, xl);
+        }
+        if (VAR != 0 && d >= U && d - U <= T - 2) {  // wave-uniform: (d-U, U)->(T-1, U) or ->final
+          const double x = log_add2(at_unit(nb, lane, U, kNoArc), VAR == 1 ? b_top : 0.0);
+#pragma unroll
+          for (int k = 0; k < K; ++k) nb[k] = (lane * K + k == U) ? x : nb[k];
+        }
+        if (d == 0) {  // wave-uniform
+          if (VAR != 0 && lane == 0) nb[0] = log_add2(nb[0], acc0);  // (0,0)->(t,0)
+          b00 = nb[0];
+        }
+        if (VAR != 0 && d >= 1 && d <= T - 1) acc0 = log_add2(acc0, nb[0]);  // beta(d, 0), lane 0
+        double* __restrict__ row = b_utt + static_cast<int64_t>(d >= 0 ? d : ND) * p.u_pad + lane * K;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          bv[k] = nb[k];
+          row[k] = nb[k];
         }
 #pragma unroll
-        for (int k = 0; k < K; ++k) bv[k] = nb[k];
-#pragma unroll
-        for (int k = 0; k < K; ++k)
-          load_cell<DENSE_IN>(p, b, d - PF, lane * K + k, T, U, D, rb[s][k], rl[s][k]);
+        for (int k = 0; k < K; ++k) load_w(d - PF, k, rb[s][k], rl[s][k]);
+        __builtin_amdgcn_sched_barrier(0);  // the prefetch stays PF steps ahead of its use
       }
     }
     if (lane == 0) p.lnp2_bwd[b] = b00;
@@ -274,6 +329,7 @@ struct PostParams {
   const double* lnp2_fwd;
   const double* lnp2_bwd;
   int64_t n_rows;
+  int32_t u_pad;          // row width of alpha / beta
   RowInfo* rowinfo;       // row records for the gradient kernel, or
   double* alpha_out;      // dense float64 natural-log outputs (each may be null)
   double* beta_out;
@@ -309,8 +365,8 @@ __global__ __launch_bounds__(kPostThreads) void k2b_posteriors(PostParams p) {
   }
   const double lnP2 = p.lnp2_fwd[b];
   const int d = t + u;
-  const int64_t ab0 = static_cast<int64_t>(b) * (p.T_max + p.U_max + 1) * U1;
-  const double al = p.alpha[ab0 + static_cast<int64_t>(d) * U1 + u];
+  const int64_t ab0 = static_cast<int64_t>(b) * (p.T_max + p.U_max + 1) * p.u_pad;
+  const double al = p.alpha[ab0 + static_cast<int64_t>(d) * p.u_pad + u];
   double wb, wl;
   float lse2 = 0.f;
   if (!DENSE) {
@@ -324,9 +380,9 @@ __global__ __launch_bounds__(kPostThreads) void k2b_posteriors(PostParams p) {
     wl = to_lattice(u < U ? p.lp_label[r] : 0.0, u < U);
   }
   double xb = kNoArc, xl = kNoArc;
-  if (t < T - 1) xb = al + wb + p.beta[ab0 + static_cast<int64_t>(d + 1) * U1 + u] - lnP2;
+  if (t < T - 1) xb = al + wb + p.beta[ab0 + static_cast<int64_t>(d + 1) * p.u_pad + u] - lnP2;
   else if (u == U) xb = al + wb - lnP2;
-  if (u < U) xl = al + wl + p.beta[ab0 + static_cast<int64_t>(d + 1) * U1 + u + 1] - lnP2;
+  if (u < U) xl = al + wl + p.beta[ab0 + static_cast<int64_t>(d + 1) * p.u_pad + u + 1] - lnP2;
   if (!DENSE) {
     RowInfo o;
     o.lse2 = lse2;
@@ -337,7 +393,7 @@ __global__ __launch_bounds__(kPostThreads) void k2b_posteriors(PostParams p) {
   } else {
     const double ln2 = 1.0 / kLog2eD;
     if (p.alpha_out) p.alpha_out[r] = al * ln2;
-    if (p.beta_out) p.beta_out[r] = p.beta[ab0 + static_cast<int64_t>(d) * U1 + u] * ln2;
+    if (p.beta_out) p.beta_out[r] = p.beta[ab0 + static_cast<int64_t>(d) * p.u_pad + u] * ln2;
     if (p.occ_blank_out) p.occ_blank_out[r] = exp2(xb);
     if (p.occ_label_out) p.occ_label_out[r] = exp2(xl);
   }

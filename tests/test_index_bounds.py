@@ -153,25 +153,39 @@ def test_gradient_kernel_chunk_mapping(B, T, U, V, dt):
 
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
 def test_lattice_kernel_addresses(B, T, U, V, dt):
+    """Sweep kernel: weights of any step e read at the cell clamped into the utterance,
+    diagonal ec = clamp(e, 0, D), unit clamp(u, ec - (T_b-1), min(ec, U_b)), a valid cell;
+    alpha stored in row min(d, D+1), beta in row d (or the spare row ND when d < 0), each row
+    u_pad = 64*K wide; the posterior kernel reads alpha, beta only at diagonals <= D."""
     U1 = U + 1
     ND = T + U
     K = next(k for k in (1, 2, 4, 8, 16) if U1 <= 64 * k)
-    assert 64 * K >= U1
-    sab = (ND + 1) * U1
-    # stores: node (d, u) with d <= D <= T-1+U, u <= U; everything else to the scratch row
-    hi = (B - 1) * sab + (T - 1 + U) * U1 + U
-    assert hi < B * sab
-    assert (B - 1) * sab + ND * U1 < B * sab
-    # weight loads are clamped into the utterance: d in [0, D], u in [max(0, d-T+1), min(d, U)]
+    u_pad = 64 * K
+    n_cells = B * ND * U1
+    n_scores = B * (ND + 1) * u_pad
+    lanes = np.arange(64)
     for Tb, Ub in [(T, U), (1, 0), (max(1, T // 2), U // 2), (1, U), (T, 0)]:
         D = Tb - 1 + Ub
-        for d in range(-20, D + 40):
-            dc = min(max(d, 0), D)
-            for u in range(0, 64 * K):
-                uc = min(max(u, dc - (Tb - 1)), min(dc, Ub))
-                assert 0 <= dc - uc < Tb and 0 <= uc <= Ub
-    # the posterior kernel reads beta at diagonal t+u+1 <= T-1+U only for t < T-1 or u < U
-    assert (T - 2) + U + 1 <= T - 1 + U
+        PF = 2 if K >= 16 else min(24, 48 // K)
+        for bb in {0, B - 1}:
+            for e in range(-PF - 2, D + PF + 2):  # every diagonal a load or store step can name
+                ec = min(max(e, 0), D)
+                for k in range(K):
+                    uc = np.minimum(np.maximum(lanes * K + k, ec - (Tb - 1)), min(ec, Ub))
+                    tc = ec - uc
+                    assert np.all((tc >= 0) & (tc < Tb) & (uc >= 0) & (uc <= Ub))  # a cell kernel 1 wrote
+                    w = (bb * ND + ec) * U1 + uc
+                    assert np.all(w >= 0) and np.all(w < n_cells)
+                    rows = []
+                    if 1 <= e <= D + PF - 1:  # forward steps d = 1 .. (last block's end)
+                        rows.append(min(e, D + 1))
+                    if -PF + 1 <= e <= D - 1:  # backward steps d = D-1 .. (last block's end)
+                        rows.append(e if e >= 0 else ND)
+                    for row in rows:
+                        a = (bb * (ND + 1) + row) * u_pad + lanes * K + k
+                        assert np.all(a >= 0) and np.all(a < n_scores)
+        # spare rows never overlap the rows the posterior kernel reads (d <= D)
+        assert D + 1 <= ND
 
 
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
