@@ -256,6 +256,30 @@ def test_random_shapes(torch, pkg, dtype, gdt, variant, B, T, U, V, blank, seed)
     tol_check(loss, grad, loss_ref, grad_ref, dtype, tl, ul, grad_dtype=gdt)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("B,T,U,V,seed", [
+    (2, 4, 300, 6, 21),    # 8 units per lane of the sweep; a diagonal split over two populate blocks
+    (1, 3, 700, 5, 22),    # 16 units per lane
+    (1, 2, 1023, 3, 23),   # the widest label axis the sweep takes (U_max + 1 = 1024)
+])
+def test_wide_label_axis(torch, pkg, dtype, variant, B, T, U, V, seed):
+    logits, tl, ul, labels = W.small_case(B, T, U, V, seed=seed, sigma=2.0)
+    loss, grad, seen = run_case(torch, pkg, logits, tl, ul, labels, variant=variant, dtype=dtype,
+                                grad_dtype="f32")
+    loss_ref, grad_ref = R.rnnt_loss_grad(seen, labels, tl, ul, 0, variant)
+    tol_check(loss, grad, loss_ref, grad_ref, dtype, tl, ul, grad_dtype="f32")
+
+
+@pytest.mark.parametrize("dtype,V,blank", [("f32", 4100, 17), ("bf16", 8200, 8199), ("f16", 2600, 0)])
+def test_large_vocabulary(torch, pkg, dtype, V, blank):
+    # rows longer than the populate kernel's register path (64 lanes x 5 chunks) take its batched path
+    logits, tl, ul, labels = W.small_case(3, 7, 5, V, seed=V, sigma=3.0, blank=blank)
+    loss, grad, seen = run_case(torch, pkg, logits, tl, ul, labels, blank=blank, dtype=dtype)
+    loss_ref, grad_ref = R.rnnt_loss_grad(seen, labels, tl, ul, blank, "rnnt")
+    tol_check(loss, grad, loss_ref, grad_ref, dtype, tl, ul)
+
+
 def test_loss_only_matches_fused(torch, pkg):
     logits, tl, ul, labels = W.small_case(4, 12, 9, 40, seed=11)
     a, _, _ = run_case(torch, pkg, logits, tl, ul, labels, need_grad=False)

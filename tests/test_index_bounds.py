@@ -14,7 +14,8 @@ from paper_2303_10384_amd.workloads import WORKLOADS
 EPC = {"f32": 4, "bf16": 8, "f16": 8}
 SHAPES = [(w.B, w.T_max, w.U_max, w.V, w.dtype) for w in WORKLOADS.values()] + [
     (3, 7, 0, 2, "f32"), (2, 5, 4, 3, "bf16"), (1, 1, 1023, 5, "f32"), (4, 9, 63, 4097, "f16"),
-    (5, 3, 64, 7, "bf16"), (2, 2, 127, 8, "f32")]
+    (5, 3, 64, 7, "bf16"), (2, 2, 127, 8, "f32"), (2, 4, 300, 6, "f32"), (1, 3, 700, 5, "bf16"),
+    (1, 2, 1023, 3, "bf16"), (3, 7, 5, 4100, "f32"), (3, 7, 5, 8200, "bf16"), (3, 7, 5, 2600, "f16")]
 
 
 def k1_shape(V, epc):
