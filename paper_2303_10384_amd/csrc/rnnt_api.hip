@@ -197,7 +197,7 @@ hipError_t launch_k2(int variant, const LatticeParams& p, hipStream_t stream) {
 
 template <bool DENSE>
 hipError_t launch_k2b(const PostParams& p, hipStream_t stream) {
-  const int64_t blocks = (p.n_rows + kPostThreads - 1) / kPostThreads;
+  const int64_t blocks = static_cast<int64_t>(p.B) * ((p.T_max + kPostTileT - 1) / kPostTileT);
   if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL((k2b_posteriors<DENSE>), dim3(static_cast<uint32_t>(blocks)), dim3(kPostThreads), 0, stream, p);
   return hipGetLastError();

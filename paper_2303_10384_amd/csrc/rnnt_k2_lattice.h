@@ -30,7 +30,7 @@
 // arcs cost two running log-sums held by the lanes owning u = 0 and u = U,
 // updated under wave-uniform conditions on the diagonal.
 //
-// Kernel 2b, one thread per padded row (t, u):
+// Kernel 2b, for every padded row (t, u):
 //   occ_blank(t,u) = 2^(alpha(t,u) + lp_blank(t,u) + beta(t+1,u) - log2 P)   (t < T-1)
 //   occ_blank(T-1,U) = 2^(alpha(T-1,U) + lp_blank(T-1,U) - log2 P)
 //   occ_label(t,u) = 2^(alpha(t,u) + lp_label(t,u) + beta(t,u+1) - log2 P)   (u < U)
@@ -340,62 +340,82 @@ struct PostParams {
 };
 
 constexpr int kPostThreads = 256;
+constexpr int kPostTileT = 8;  // frames per block
 
+// One block per (utterance, kPostTileT frames t0 .. t0+7, every unit).  Its
+// threads walk the tile's cells diagonal by diagonal (consecutive threads:
+// consecutive t, so consecutive cells of one diagonal), which makes the loads
+// of alpha, beta and the lattice form contiguous; the tile's row records are
+// one contiguous range of memory, completed by the block.
 template <bool DENSE>
 __global__ __launch_bounds__(kPostThreads) void k2b_posteriors(PostParams p) {
-  const int64_t r = static_cast<int64_t>(blockIdx.x) * kPostThreads + threadIdx.x;
-  if (r >= p.n_rows) return;
   const int U1 = p.U_max + 1;
-  const int rows_utt = p.T_max * U1;
-  const int b = static_cast<int>(r / rows_utt);
-  const int rem = static_cast<int>(r - static_cast<int64_t>(b) * rows_utt);
-  const int t = rem / U1;
-  const int u = rem - t * U1;
+  const int n_tiles = (p.T_max + kPostTileT - 1) / kPostTileT;
+  const int b = static_cast<int>(blockIdx.x / n_tiles);
+  const int t0 = static_cast<int>(blockIdx.x - static_cast<int64_t>(b) * n_tiles) * kPostTileT;
+  const int t_end = min(t0 + kPostTileT, p.T_max);
   const int T = p.logit_lens[b];
   const int U = p.label_lens[b];
   const bool good = p.status[b] == 0;
-  if (DENSE && rem == 0) {
+  const int64_t r_utt = static_cast<int64_t>(b) * p.T_max * U1;
+  if (DENSE && t0 == 0 && threadIdx.x == 0) {
     const double ln2 = 1.0 / kLog2eD;
     if (p.loss_out) p.loss_out[b] = good ? -p.lnp2_fwd[b] * ln2 : __builtin_nan("");
     if (p.loss_bwd_out) p.loss_bwd_out[b] = good ? -p.lnp2_bwd[b] * ln2 : __builtin_nan("");
   }
-  if (!good || t >= T || u > U) {
-    if (!DENSE) p.rowinfo[r] = RowInfo{0.f, 0.f, 0.f, kZeroRow};
+  if (!good || t0 >= T) {  // the whole tile is zero rows
+    if (!DENSE) {
+      const int64_t r0 = r_utt + static_cast<int64_t>(t0) * U1;
+      const int n = (t_end - t0) * U1;
+      for (int i = threadIdx.x; i < n; i += kPostThreads) p.rowinfo[r0 + i] = RowInfo{0.f, 0.f, 0.f, kZeroRow};
+    }
     return;
   }
   const double lnP2 = p.lnp2_fwd[b];
-  const int d = t + u;
   const int64_t ab0 = static_cast<int64_t>(b) * (p.T_max + p.U_max + 1) * p.u_pad;
-  const double al = p.alpha[ab0 + static_cast<int64_t>(d) * p.u_pad + u];
-  double wb, wl;
-  float lse2 = 0.f;
-  if (!DENSE) {
-    const int64_t sc = (static_cast<int64_t>(b) * (p.T_max + p.U_max) + d) * U1 + u;
-    const double2 w = p.lp2[sc];
-    wb = w.x;
-    wl = w.y;
-    lse2 = p.lse2[sc];
-  } else {
-    wb = to_lattice(p.lp_blank[r], true);
-    wl = to_lattice(u < U ? p.lp_label[r] : 0.0, u < U);
-  }
-  double xb = kNoArc, xl = kNoArc;
-  if (t < T - 1) xb = al + wb + p.beta[ab0 + static_cast<int64_t>(d + 1) * p.u_pad + u] - lnP2;
-  else if (u == U) xb = al + wb - lnP2;
-  if (u < U) xl = al + wl + p.beta[ab0 + static_cast<int64_t>(d + 1) * p.u_pad + u + 1] - lnP2;
-  if (!DENSE) {
-    RowInfo o;
-    o.lse2 = lse2;
-    o.occ_blank = fast_exp2(static_cast<float>(xb));
-    o.occ_label = fast_exp2(static_cast<float>(xl));
-    o.label = (u < U) ? p.labels[static_cast<int64_t>(b) * p.U_max + u] : kNoLabel;
-    p.rowinfo[r] = o;
-  } else {
-    const double ln2 = 1.0 / kLog2eD;
-    if (p.alpha_out) p.alpha_out[r] = al * ln2;
-    if (p.beta_out) p.beta_out[r] = p.beta[ab0 + static_cast<int64_t>(d) * p.u_pad + u] * ln2;
-    if (p.occ_blank_out) p.occ_blank_out[r] = exp2(xb);
-    if (p.occ_label_out) p.occ_label_out[r] = exp2(xl);
+  const int64_t sc0 = static_cast<int64_t>(b) * (p.T_max + p.U_max) * U1;
+  const int n_items = kPostTileT * (kPostTileT - 1 + U1);
+  for (int i = threadIdx.x; i < n_items; i += kPostThreads) {
+    const int t = t0 + i % kPostTileT;
+    const int d = t0 + i / kPostTileT;  // diagonal
+    const int u = d - t;
+    if (t >= t_end || u < 0 || u > p.U_max) continue;
+    const int64_t r = r_utt + static_cast<int64_t>(t) * U1 + u;
+    if (t >= T || u > U) {
+      if (!DENSE) p.rowinfo[r] = RowInfo{0.f, 0.f, 0.f, kZeroRow};
+      continue;
+    }
+    const double al = p.alpha[ab0 + static_cast<int64_t>(d) * p.u_pad + u];
+    double wb, wl;
+    float lse2 = 0.f;
+    if (!DENSE) {
+      const int64_t sc = sc0 + static_cast<int64_t>(d) * U1 + u;
+      const double2 w = p.lp2[sc];
+      wb = w.x;
+      wl = w.y;
+      lse2 = p.lse2[sc];
+    } else {
+      wb = to_lattice(p.lp_blank[r], true);
+      wl = to_lattice(u < U ? p.lp_label[r] : 0.0, u < U);
+    }
+    double xb = kNoArc, xl = kNoArc;
+    if (t < T - 1) xb = al + wb + p.beta[ab0 + static_cast<int64_t>(d + 1) * p.u_pad + u] - lnP2;
+    else if (u == U) xb = al + wb - lnP2;
+    if (u < U) xl = al + wl + p.beta[ab0 + static_cast<int64_t>(d + 1) * p.u_pad + u + 1] - lnP2;
+    if (!DENSE) {
+      RowInfo o;
+      o.lse2 = lse2;
+      o.occ_blank = fast_exp2(static_cast<float>(xb));
+      o.occ_label = fast_exp2(static_cast<float>(xl));
+      o.label = (u < U) ? p.labels[static_cast<int64_t>(b) * p.U_max + u] : kNoLabel;
+      p.rowinfo[r] = o;
+    } else {
+      const double ln2 = 1.0 / kLog2eD;
+      if (p.alpha_out) p.alpha_out[r] = al * ln2;
+      if (p.beta_out) p.beta_out[r] = p.beta[ab0 + static_cast<int64_t>(d) * p.u_pad + u] * ln2;
+      if (p.occ_blank_out) p.occ_blank_out[r] = exp2(xb);
+      if (p.occ_label_out) p.occ_label_out[r] = exp2(xl);
+    }
   }
 }
 

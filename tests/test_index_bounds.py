@@ -218,3 +218,25 @@ def test_gradient_kernel_fast_path_buffer(B, T, U, V, dt):
         r = np.minimum(r_tile + (v_tile + cl * epc) // V, n_rows - 1)
         assert np.all(r >= 0) and np.all(np.minimum(r + 1, n_rows - 1) < n_rows)
     assert 0x80000000 > tile * 16  # the out-of-range offset lies past every block's buffer
+
+
+@pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
+def test_posterior_kernel_tiles_cover_every_row_once(B, T, U, V, dt):
+    """Posterior kernel: block (b, tile) walks item i -> t = t0 + i % 8, d = t0 + i // 8, u = d - t
+    over 8 * (7 + U + 1) items; kept items (t < min(t0+8, T), 0 <= u <= U) are every row once."""
+    TT = 8
+    U1 = U + 1
+    n_tiles = -(-T // TT)
+    assert B * n_tiles < 2**31
+    seen = np.zeros((T, U1), np.int64)
+    for tile in range(n_tiles):
+        t0 = tile * TT
+        i = np.arange(TT * (TT - 1 + U1))
+        t = t0 + i % TT
+        d = t0 + i // TT
+        u = d - t
+        keep = (t < min(t0 + TT, T)) & (u >= 0) & (u <= U)
+        np.add.at(seen, (t[keep], u[keep]), 1)
+        # consecutive items of one diagonal are consecutive cells (coalesced loads)
+        assert np.all(np.diff(u[:TT]) == -1)
+    assert np.all(seen == 1)
