@@ -55,6 +55,37 @@ def _walk_from(s, T, U, lp_blank, lp_label, variant, out):
                 out.append(score)
 
 
+def path_alignments(lp_blank, lp_label, variant="rnnt"):
+    """Every alignment as (log-score, label frames, start frame, end frame).
+
+    Label frame i is the frame at which unit y_{i+1} is emitted; the start frame
+    is the frame the walk starts from (after an initial jump, or 0); the end frame
+    is the frame of the last emitted unit's node (e, U) left by a final jump, or
+    T-1 when the walk reaches (T-1, U) by itself.  The walk is the one of
+    ``path_log_scores``, recording where each unit is emitted.
+    """
+    T = len(lp_blank)
+    U = len(lp_blank[0]) - 1
+    out = []
+    starts = [0] if variant == "rnnt" else list(range(T))
+    for s in starts:
+        stack = [(s, 0, 0.0, ())]
+        while stack:
+            t, u, score, frames = stack.pop()
+            if t == T - 1 and u == U:
+                out.append((score + lp_blank[t][u], frames, s, T - 1))
+            if t < T - 1:
+                stack.append((t + 1, u, score + lp_blank[t][u], frames))
+            if u < U:
+                stack.append((t, u + 1, score + lp_label[t][u], frames + (t,)))
+            if u == U and t < T - 1:
+                if variant == "wrnnt":
+                    out.append((score + lp_blank[T - 1][U], frames, s, t))
+                elif variant == "wrnnt_allow_ignore":
+                    out.append((score, frames, s, t))
+    return out
+
+
 def brute_force_log_prob(lp_blank, lp_label, variant="rnnt"):
     """ln of the summed probability of every alignment."""
     scores = path_log_scores(lp_blank, lp_label, variant)
