@@ -181,6 +181,38 @@ rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label
                                   double* occ_label_out, void* workspace, size_t workspace_bytes,
                                   hipStream_t stream);
 
+/* Forced alignment: the single most probable path through the utterance's lattice
+ * (the grid of Fig. 1, or the W-Transducer lattices of Section 3.2 / Fig. 4 and
+ * Section 4.3 for variant = RNNT_VARIANT_WRNNT / RNNT_VARIANT_WRNNT_ALLOW_IGNORE),
+ * the lattice serving forced alignment as it serves training (Section 2.2).
+ *
+ * Arguments as rnnt_loss for logits (any of the three dtypes; shape.grad_dtype is
+ * ignored), labels, lengths, blank and variant.  Outputs, device memory owned by
+ * the caller:
+ *   score_out        (B) float: the best path's log-probability (natural log,
+ *                    the closing blank included where the path takes it);
+ *   label_frames_out (B, U_max) int32: entry [b, i] is the frame at which unit
+ *                    y_{i+1} is emitted (the path takes the label arc
+ *                    (t, i) -> (t, i+1)); -1 for i >= U_b;
+ *   span_out         (B, 2) int32 or NULL: the first frame of the path (s > 0
+ *                    when it enters (s, 0) by an initial wild-card arc) and the
+ *                    last (e < T_b - 1 when it leaves (e, U_b) by a final
+ *                    wild-card arc); (0, T_b - 1) for RNN-T.
+ * Ties between equally probable paths are broken by a fixed order: at a node the
+ * blank arc, then the label arc, then the initial wild-card arc, then the final
+ * wild-card arcs (the earliest source frame) -- a later candidate wins only when
+ * strictly more probable; at the end of the allow-ignore lattice the closing
+ * blank wins a tie with the jump to the final state.  A bad utterance (as in
+ * rnnt_loss) gets score NaN and frames / span -1.  Needs a workspace of
+ * rnnt_viterbi_workspace_bytes(shape) bytes (256-byte aligned) or NULL (then
+ * allocated stream-ordered).  U_max + 1 <= 1024 (else RNNT_ERR_UNSUPPORTED).
+ */
+size_t rnnt_viterbi_workspace_bytes(rnnt_shape_t shape);
+rnnt_status_t rnnt_viterbi(const void* logits, rnnt_shape_t shape, const int32_t* labels,
+                           const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
+                           rnnt_variant_t variant, float* score_out, int32_t* label_frames_out,
+                           int32_t* span_out, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Static description of a status code (never NULL). */
 const char* rnnt_status_string(rnnt_status_t status);
 

@@ -1,12 +1,14 @@
 """RNN-Transducer and W-Transducer loss + gradient on the T x (U+1) grid lattice,
 for AMD Instinct MI355X (gfx950).
 
-The work is done by three HIP kernels in librnnt_mi355x.so behind the C-ABI in
-include/rnnt_mi355x.h; this package is the thin Python binding.
+The work is done by HIP kernels in librnnt_mi355x.so behind the C-ABI in
+include/rnnt_mi355x.h (the loss and its gradient, and forced alignment on the
+same lattices); this package is the thin Python binding.
 """
 from .binding import (RNNTError, lattice_scores, load_library, log_softmax_gather, loss_workspace_bytes,  # noqa: F401
-                      rnnt_loss, status_string, version)
+                      rnnt_loss, status_string, version, viterbi_align, viterbi_workspace_bytes)
 from .autograd import RNNTLoss, rnnt_loss_autograd  # noqa: F401
 
 __all__ = ["rnnt_loss", "log_softmax_gather", "lattice_scores", "loss_workspace_bytes", "RNNTLoss",
-           "rnnt_loss_autograd", "RNNTError", "load_library", "status_string", "version"]
+           "rnnt_loss_autograd", "RNNTError", "load_library", "status_string", "version", "viterbi_align",
+           "viterbi_workspace_bytes"]

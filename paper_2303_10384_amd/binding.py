@@ -22,7 +22,7 @@ DTYPE_F32, DTYPE_BF16, DTYPE_F16 = 0, 1, 2
 
 # every symbol declared in include/rnnt_mi355x.h
 EXPORTED = ("rnnt_loss_workspace_bytes", "rnnt_loss", "rnnt_loss_timed", "rnnt_log_softmax_gather", "rnnt_lattice_workspace_bytes",
-            "rnnt_lattice_scores", "rnnt_status_string", "rnnt_version")
+            "rnnt_lattice_scores", "rnnt_status_string", "rnnt_version", "rnnt_viterbi_workspace_bytes", "rnnt_viterbi")
 
 
 class Shape(ctypes.Structure):
@@ -61,6 +61,10 @@ def load_library():
     lib.rnnt_log_softmax_gather.restype = ctypes.c_int
     lib.rnnt_lattice_scores.argtypes = [vp, vp, Shape, vp, vp, ctypes.c_int, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.rnnt_lattice_scores.restype = ctypes.c_int
+    lib.rnnt_viterbi_workspace_bytes.argtypes = [Shape]
+    lib.rnnt_viterbi_workspace_bytes.restype = sz
+    lib.rnnt_viterbi.argtypes = [vp, Shape, vp, vp, vp, i32, ctypes.c_int, vp, vp, vp, vp, sz, vp]
+    lib.rnnt_viterbi.restype = ctypes.c_int
     lib.rnnt_status_string.argtypes = [ctypes.c_int]
     lib.rnnt_status_string.restype = ctypes.c_char_p
     lib.rnnt_version.argtypes = []
@@ -210,3 +214,43 @@ def lattice_scores(lp_blank, lp_label, logit_lens, label_lens, variant="rnnt"):
     if st != RNNT_OK:
         raise RNNTError(st, "rnnt_lattice_scores")
     return out
+
+
+def viterbi_workspace_bytes(B, T_max, U_max, V, dtype_code_=DTYPE_F32):
+    return load_library().rnnt_viterbi_workspace_bytes(Shape(B, T_max, U_max, V, dtype_code_, dtype_code_))
+
+
+def viterbi_align(logits, labels, logit_lens, label_lens, blank=0, variant="rnnt", workspace=None):
+    """Forced alignment (best path) of every utterance.
+
+    Returns (score (B,) float32 natural-log best path log-probability,
+    label_frames (B, U_max) int32 frame of each unit or -1, span (B, 2) int32
+    first / last frame of the path).
+    """
+    torch = _torch()
+    lib = load_library()
+    _check_gpu("logits", logits)
+    _check_gpu("labels", labels, torch.int32)
+    _check_gpu("logit_lens", logit_lens, torch.int32)
+    _check_gpu("label_lens", label_lens, torch.int32)
+    if logits.dim() != 4:
+        raise ValueError("logits must be (B, T_max, U_max+1, V)")
+    shape = shape_of(logits)
+    if labels.shape != (shape.B, shape.U_max) or logit_lens.shape != (shape.B,) or label_lens.shape != (shape.B,):
+        raise ValueError("labels must be (B, U_max) and the length vectors (B,)")
+    if variant not in VARIANTS:
+        raise ValueError("variant must be one of %s" % sorted(VARIANTS))
+    dev = logits.device
+    score = torch.empty(shape.B, dtype=torch.float32, device=dev)
+    frames = torch.empty((shape.B, shape.U_max), dtype=torch.int32, device=dev)
+    span = torch.empty((shape.B, 2), dtype=torch.int32, device=dev)
+    ws_ptr, ws_bytes = ctypes.c_void_p(0), 0
+    if workspace is not None:
+        _check_gpu("workspace", workspace)
+        ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
+    st = lib.rnnt_viterbi(_ptr(logits), shape, _ptr(labels), _ptr(logit_lens), _ptr(label_lens), int(blank),
+                          VARIANTS[variant], _ptr(score), _ptr(frames), _ptr(span), ws_ptr, ws_bytes,
+                          _stream_handle(dev))
+    if st != RNNT_OK:
+        raise RNNTError(st, "rnnt_viterbi")
+    return score, frames, span

@@ -11,7 +11,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB_NAME = "librnnt_mi355x.so"
 SOURCES = ["csrc/rnnt_api.hip"]
-HEADERS = ["csrc/rnnt_device.h", "csrc/rnnt_k1_populate.h", "csrc/rnnt_k2_lattice.h", "csrc/rnnt_k3_grad.h"]
+HEADERS = ["csrc/rnnt_device.h", "csrc/rnnt_k1_populate.h", "csrc/rnnt_k2_lattice.h", "csrc/rnnt_k2_viterbi.h",
+           "csrc/rnnt_k3_grad.h"]
 
 
 def hipcc():

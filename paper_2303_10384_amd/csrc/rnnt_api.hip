@@ -10,6 +10,7 @@
 #include "rnnt_k1_populate.h"
 #include "rnnt_k2_lattice.h"
 #include "rnnt_k3_grad.h"
+#include "rnnt_k2_viterbi.h"
 
 namespace rnnt {
 namespace {
@@ -165,6 +166,28 @@ hipError_t launch_k1_dtype(rnnt_dtype_t dt, const PopulateParams& p, hipStream_t
   }
 }
 
+// Workspace of the forced alignment: the lattice form (lp2, lse2) as in the loss,
+// the decision words B * (T_max+U_max+1) * K uint64, 256-byte aligned pieces.
+struct ViterbiLayout {
+  size_t lp2, lse2, decisions, total;
+};
+
+ViterbiLayout make_viterbi_layout(const rnnt_shape_t& s) {
+  const size_t U1 = static_cast<size_t>(s.U_max) + 1;
+  const size_t cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max) * U1;
+  const size_t words = static_cast<size_t>(s.B) * (s.T_max + s.U_max + 1) * units_per_lane(s.U_max + 1);
+  ViterbiLayout L{};
+  size_t o = 0;
+  L.lp2 = o;
+  o = align256(o + cells * 2 * sizeof(double));
+  L.lse2 = o;
+  o = align256(o + cells * sizeof(float));
+  L.decisions = o;
+  o = align256(o + words * sizeof(uint64_t));
+  L.total = o;
+  return L;
+}
+
 // ---- kernel 2 ---------------------------------------------------------------
 
 template <int K, int VAR, int MODE, bool DENSE_IN>
@@ -192,6 +215,32 @@ hipError_t launch_k2(int variant, const LatticeParams& p, hipStream_t stream) {
     case RNNT_VARIANT_RNNT: return launch_k2_v<0, MODE, DENSE_IN>(p, stream);
     case RNNT_VARIANT_WRNNT: return launch_k2_v<1, MODE, DENSE_IN>(p, stream);
     default: return launch_k2_v<2, MODE, DENSE_IN>(p, stream);
+  }
+}
+
+template <int K, int VAR>
+hipError_t launch_k2v_k(const ViterbiParams& p, hipStream_t stream) {
+  constexpr int PF = (K >= 16) ? 2 : (48 / K > 24 ? 24 : 48 / K);
+  hipLaunchKernelGGL((k2_viterbi<K, PF, VAR>), dim3(p.B), dim3(64), 0, stream, p);
+  return hipGetLastError();
+}
+
+template <int VAR>
+hipError_t launch_k2v_v(const ViterbiParams& p, hipStream_t stream) {
+  switch (units_per_lane(p.U_max + 1)) {
+    case 1: return launch_k2v_k<1, VAR>(p, stream);
+    case 2: return launch_k2v_k<2, VAR>(p, stream);
+    case 4: return launch_k2v_k<4, VAR>(p, stream);
+    case 8: return launch_k2v_k<8, VAR>(p, stream);
+    default: return launch_k2v_k<16, VAR>(p, stream);
+  }
+}
+
+hipError_t launch_k2v(int variant, const ViterbiParams& p, hipStream_t stream) {
+  switch (variant) {
+    case RNNT_VARIANT_RNNT: return launch_k2v_v<0>(p, stream);
+    case RNNT_VARIANT_WRNNT: return launch_k2v_v<1>(p, stream);
+    default: return launch_k2v_v<2>(p, stream);
   }
 }
 
@@ -401,6 +450,65 @@ rnnt_status_t rnnt_loss(const void* logits, rnnt_shape_t shape, const int32_t* l
                         size_t workspace_bytes, hipStream_t stream) {
   return rnnt_loss_timed(logits, shape, labels, logit_lens, label_lens, blank, variant, loss_out, grad_out,
                          workspace, workspace_bytes, stream, nullptr);
+}
+
+size_t rnnt_viterbi_workspace_bytes(rnnt_shape_t shape) {
+  rnnt_shape_t s = shape;
+  s.grad_dtype = s.dtype;
+  if (check_shape(s) != RNNT_OK) return 0;
+  return make_viterbi_layout(s).total;
+}
+
+rnnt_status_t rnnt_viterbi(const void* logits, rnnt_shape_t shape, const int32_t* labels,
+                           const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
+                           rnnt_variant_t variant, float* score_out, int32_t* label_frames_out, int32_t* span_out,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  shape.grad_dtype = shape.dtype;  // no gradient here
+  rnnt_status_t st = check_shape(shape);
+  if (st != RNNT_OK) return st;
+  if (!logits || !logit_lens || !label_lens || !score_out || (!labels && shape.U_max > 0) ||
+      (!label_frames_out && shape.U_max > 0))
+    return RNNT_ERR_NULL_PTR;
+  if (blank < 0 || blank >= shape.V) return RNNT_ERR_BAD_BLANK;
+  if (!variant_known(variant)) return RNNT_ERR_BAD_VARIANT;
+  if (!aligned16(logits)) return RNNT_ERR_ALIGNMENT;
+  if (shape.U_max + 1 > kMaxUnits1) return RNNT_ERR_UNSUPPORTED;
+  const ViterbiLayout L = make_viterbi_layout(shape);
+  Scratch scratch;
+  char* ws = nullptr;
+  st = take_workspace(workspace, workspace_bytes, L.total, stream, scratch, &ws);
+  if (st != RNNT_OK) return st;
+
+  PopulateParams p1{};
+  p1.logits = logits;
+  p1.B = shape.B;
+  p1.T_max = shape.T_max;
+  p1.U_max = shape.U_max;
+  p1.V = shape.V;
+  p1.blank = blank;
+  p1.labels = labels;
+  p1.logit_lens = logit_lens;
+  p1.label_lens = label_lens;
+  p1.n_elem = static_cast<int64_t>(shape.B) * shape.T_max * (shape.U_max + 1) * shape.V;
+  p1.lp2 = reinterpret_cast<double2*>(ws + L.lp2);
+  p1.lse2 = reinterpret_cast<float*>(ws + L.lse2);
+  if (launch_k1_dtype<true>(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
+
+  ViterbiParams pv{};
+  pv.B = shape.B;
+  pv.T_max = shape.T_max;
+  pv.U_max = shape.U_max;
+  pv.V = shape.V;
+  pv.blank = blank;
+  pv.labels = labels;
+  pv.logit_lens = logit_lens;
+  pv.label_lens = label_lens;
+  pv.lp2 = p1.lp2;
+  pv.decisions = reinterpret_cast<uint64_t*>(ws + L.decisions);
+  pv.score_out = score_out;
+  pv.label_frames = label_frames_out;
+  pv.span = span_out;
+  return launch_k2v(variant, pv, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
 }
 
 rnnt_status_t rnnt_log_softmax_gather(const void* logits, rnnt_shape_t shape, const int32_t* labels,

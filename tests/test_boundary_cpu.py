@@ -30,7 +30,7 @@ def test_header_declares_the_documented_entry_points():
     names = declared_functions()
     assert names == sorted(["rnnt_loss_workspace_bytes", "rnnt_loss", "rnnt_loss_timed", "rnnt_log_softmax_gather",
                             "rnnt_lattice_workspace_bytes", "rnnt_lattice_scores", "rnnt_status_string",
-                            "rnnt_version"])
+                            "rnnt_version", "rnnt_viterbi_workspace_bytes", "rnnt_viterbi"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -131,6 +131,47 @@ def test_other_entry_points_host_errors(lib):
     st = lib.rnnt_lattice_scores(vp(FAKE), vp(FAKE), shape(), vp(FAKE), vp(FAKE), 0, vp(0), vp(0), vp(0), vp(0),
                                  vp(0), vp(0), vp(FAKE), need - 1, vp(0))
     assert st == 6
+
+
+def expected_viterbi_workspace(B, T, U, V):
+    a = lambda x: (x + 255) // 256 * 256  # noqa: E731
+    cells = B * (T + U) * (U + 1)
+    K = next(k for k in (1, 2, 4, 8, 16) if U + 1 <= 64 * k or k == 16)
+    o = a(cells * 16)                    # {lp_blank, lp_label}
+    o = a(o + cells * 4)                 # lse * log2 e
+    return a(o + B * (T + U + 1) * K * 8)  # decision words
+
+
+@pytest.mark.parametrize("B,T,U,V", [(1, 1, 0, 2), (32, 250, 80, 1025), (3, 7, 200, 9), (2, 5, 1023, 3)])
+def test_viterbi_workspace_size(lib, B, T, U, V):
+    assert lib.rnnt_viterbi_workspace_bytes(shape(B, T, U, V)) == expected_viterbi_workspace(B, T, U, V)
+    assert lib.rnnt_viterbi_workspace_bytes(shape(B=0)) == 0
+
+
+def call_viterbi(lib, sh, logits=FAKE, labels=FAKE, tl=FAKE, ul=FAKE, blank=0, variant=0, score=FAKE,
+                 frames=FAKE, span=0, ws=None, ws_bytes=None):
+    vp = ctypes.c_void_p
+    if ws is None:  # a workspace one byte short: every call stops before any device work
+        ws, ws_bytes = FAKE, max(0, lib.rnnt_viterbi_workspace_bytes(sh) - 1)
+    return lib.rnnt_viterbi(vp(logits), sh, vp(labels), vp(tl), vp(ul), blank, variant, vp(score), vp(frames),
+                            vp(span), vp(ws), ws_bytes, vp(0))
+
+
+def test_viterbi_host_errors(lib):
+    assert call_viterbi(lib, shape(B=0)) == 2
+    assert call_viterbi(lib, shape(V=1)) == 2
+    assert call_viterbi(lib, shape(dt=3)) == 4
+    assert call_viterbi(lib, shape(), logits=0) == 1
+    assert call_viterbi(lib, shape(), labels=0) == 1
+    assert call_viterbi(lib, shape(), score=0) == 1
+    assert call_viterbi(lib, shape(), frames=0) == 1
+    assert call_viterbi(lib, shape(), blank=7) == 3
+    assert call_viterbi(lib, shape(), variant=3) == 5
+    assert call_viterbi(lib, shape(), logits=FAKE + 4) == 7
+    assert call_viterbi(lib, shape(U=1024)) == 9
+    assert call_viterbi(lib, shape()) == 6  # workspace one byte short
+    need = lib.rnnt_viterbi_workspace_bytes(shape())
+    assert call_viterbi(lib, shape(), ws=FAKE + 16, ws_bytes=need) == 7
 
 
 def test_binding_refuses_cpu_tensors(lib):

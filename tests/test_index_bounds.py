@@ -240,3 +240,38 @@ def test_posterior_kernel_tiles_cover_every_row_once(B, T, U, V, dt):
         # consecutive items of one diagonal are consecutive cells (coalesced loads)
         assert np.all(np.diff(u[:TT]) == -1)
     assert np.all(seen == 1)
+
+
+@pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
+def test_viterbi_kernel_addresses(B, T, U, V, dt):
+    """Forced-alignment kernel: decision words stored at row min(d, D+1), K words a row, and the
+    backtrace's windows [w_lo, w_hi] (w_hi = d*K + K-1, w_lo = max(0, w_hi - 63)) inside the
+    utterance's (T_max+U_max+1)*K words; every word the walk reads lies in its window."""
+    U1 = U + 1
+    ND = T + U
+    K = next(k for k in (1, 2, 4, 8, 16) if U1 <= 64 * k)
+    words = (ND + 1) * K
+    for Tb, Ub in [(T, U), (1, 0), (max(1, T // 2), U // 2), (1, U), (T, 0)]:
+        D = Tb - 1 + Ub
+        PF = 2 if K >= 16 else min(24, 48 // K)
+        for d in range(1, D + PF):
+            row = min(d, D + 1)
+            for lane in range(64):
+                assert 0 <= row * K + min(lane, K - 1) < words
+        # a walk that takes every label move first, then every blank move (and the reverse)
+        for labels_first in (True, False):
+            t, u = Tb - 1, Ub
+            w_lo = None
+            while t + u > 0:
+                dd = t + u
+                widx = dd * K + u % K
+                if w_lo is None or widx < w_lo:
+                    w_hi = dd * K + K - 1
+                    w_lo = max(0, w_hi - 63)
+                    assert 0 <= w_lo and w_hi < words
+                assert w_lo <= widx <= w_lo + 63
+                assert 0 <= u // K < 64
+                if (labels_first and u > 0) or t == 0:
+                    u -= 1
+                else:
+                    t -= 1
