@@ -6,9 +6,11 @@ and gather, kernel 2 lattice sweep and arc posteriors, kernel 3 gradient) over
 one batch of the workload, inputs already resident in HBM.  Prints ONE JSON
 line: throughput in joint-logit elements/s (padded tensor B*T_max*(U_max+1)*V
 per step), the achieved HBM bandwidth of the dominant kernel against the
-MI355X peak, and the CPU oracle timed on a bounded sample.
+MI355X peak, and the CPU oracle timed on a bounded sample.  With --mode viterbi
+a step is one forced alignment of the batch (populate kernel, alignment kernel)
+and the line reports that path the same way.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload bpe]
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload bpe] [--mode loss|viterbi]
 """
 import argparse
 import ctypes
@@ -56,9 +58,10 @@ class HipEvents:
             self.hip.hipEventDestroy(ctypes.c_void_p(h))
 
 
-def profiled_traffic(workload):
-    """HBM bytes per gradient-kernel launch from the committed rocprofv3 counter
-    record, if it was taken on the kernel sources as they are now; else None."""
+def profiled_traffic(workload, kernel="k3_grad"):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter record
+    of the fused loss, if it was taken on the kernel sources as they are now; else
+    None."""
     from paper_2303_10384_amd.profiling import KERNEL_SOURCES, source_digest
     path = os.path.join(PROFILE_DIR, "k3_grad_%s_traffic.json" % workload)
     if not os.path.exists(path):
@@ -67,7 +70,9 @@ def profiled_traffic(workload):
         rec = json.load(f)
     if rec.get("source_digest") != source_digest(KERNEL_SOURCES):
         return None
-    return rec.get("hbm_bytes_per_launch")
+    if kernel == "k3_grad":
+        return rec.get("hbm_bytes_per_launch")
+    return rec.get("kernels", {}).get(kernel, {}).get("hbm_bytes")
 
 
 def algorithmic_bytes(w, tl, ul, s_in, s_out):
@@ -95,15 +100,18 @@ def algorithmic_bytes(w, tl, ul, s_in, s_out):
 def cpu_oracle_worker(args):
     import numpy as np
 
-    from oracle import rnnt_ref
-    T_b, U_b, V, sigma, seed, labels, variant = args
+    from oracle import rnnt_ref, viterbi
+    T_b, U_b, V, sigma, seed, labels, variant, mode = args
     z = np.random.default_rng(seed).standard_normal((T_b, U_b + 1, V), dtype=np.float32) * np.float32(sigma)
     t0 = time.perf_counter()
-    rnnt_ref.utterance_loss_grad(z.astype(np.float64), labels, 0, variant, need_grad=True)
+    if mode == "viterbi":
+        viterbi.utterance_alignment(z.astype(np.float64), labels, 0, variant)
+    else:
+        rnnt_ref.utterance_loss_grad(z.astype(np.float64), labels, 0, variant, need_grad=True)
     return time.perf_counter() - t0
 
 
-def cpu_baseline(w, tl, ul, labels, budget_s):
+def cpu_baseline(w, tl, ul, labels, budget_s, mode="loss"):
     """Time the float64 oracle (loss + gradient) on utterances of this workload
     (same lengths and labels, same logit distribution), spread over a process
     pool.  Runs before the GPU is touched, so the workers are plain forks."""
@@ -111,8 +119,8 @@ def cpu_baseline(w, tl, ul, labels, budget_s):
 
     cores = max(1, min(16, len(os.sched_getaffinity(0))))
     per_utt_elems = w.T_max * (w.U_max + 1) * w.V
-    jobs = [(int(tl[b]), int(ul[b]), w.V, w.sigma, w.seed * 1000 + b, labels[b, :int(ul[b])].copy(), w.variant)
-            for b in range(w.B)]
+    jobs = [(int(tl[b]), int(ul[b]), w.V, w.sigma, w.seed * 1000 + b, labels[b, :int(ul[b])].copy(), w.variant,
+             mode) for b in range(w.B)]
     ctx = mp.get_context("fork")
     with ctx.Pool(cores) as pool:
         t0 = time.perf_counter()
@@ -133,8 +141,10 @@ def cpu_baseline(w, tl, ul, labels, budget_s):
         "cores": min(cores, n),
         "kind": "oracle",
         "sample": "%d utterance evaluations cycling through the %d utterances of the batch (their lengths and "
-                  "labels, N(0,%g) logits), float64 loss + gradient, %d worker processes, %.1f s; elements "
-                  "counted as padded rows x V like the GPU value" % (n, w.B, w.sigma, min(cores, n), dt),
+                  "labels, N(0,%g) logits), float64 %s, %d worker processes, %.1f s; elements counted as padded "
+                  "rows x V like the GPU value" % (n, w.B, w.sigma,
+                                                   "forced alignment" if mode == "viterbi" else "loss + gradient",
+                                                   min(cores, n), dt),
     }
 
 
@@ -151,6 +161,83 @@ def copy_probe(torch, w, steps):
     print(json.dumps({"copy_probe_bytes": nbytes, "copies": steps}), flush=True)
 
 
+def viterbi_bench(args, w, tl, ul, logits, labels_d, tl_d, ul_d, cpu):
+    """Forced alignment of the workload's batch: populate kernel + alignment kernel
+    (sweep and backtrace) per step, timed with HIP events on the launch stream."""
+    import numpy as np
+    import torch
+
+    from paper_2303_10384_amd import binding
+    dev = logits.device
+    outs = (torch.empty(w.B, dtype=torch.float32, device=dev),
+            torch.empty((w.B, w.U_max), dtype=torch.int32, device=dev),
+            torch.empty((w.B, 2), dtype=torch.int32, device=dev))
+    ws = torch.empty(binding.viterbi_workspace_bytes(w.B, w.T_max, w.U_max, w.V, binding.dtype_code(logits.dtype)),
+                     dtype=torch.uint8, device=dev)
+    call = lambda ev=None: binding.viterbi_align(logits, labels_d, tl_d, ul_d, 0, w.variant, ws, outs, ev)  # noqa: E731
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    log("[bench] warmup done")
+    ev = HipEvents()
+    events = [ev.create(3) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        call(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    k_ms = [[ev.elapsed_ms(e[i], e[i + 1]) for i in range(2)] for e in events]
+    total_ms = ev.elapsed_ms(events[0][0], events[-1][2])
+    for e in events:
+        ev.destroy(e)
+    ms_per_step = total_ms / args.steps
+    k1_ms, kv_ms = (float(np.mean([r[i] for r in k_ms])) for i in range(2))
+    log("[bench] per step %.4f ms (wall %.4f ms): k1 %.4f  k2_viterbi %.4f ms"
+        % (ms_per_step, wall * 1e3 / args.steps, k1_ms, kv_ms))
+    ab = algorithmic_bytes(w, tl, ul, logits.element_size(), logits.element_size())
+    elems = ab["padded_rows"] * w.V
+    k1_gbs = ab["k1_populate"] / (k1_ms * 1e-3) / 1e9
+    result = {
+        "metric": "forced-alignment joint-logit elements/sec (best path and its frames) and achieved HBM GB/s vs peak",
+        "value": elems / (ms_per_step * 1e-3),
+        "unit": "joint-logit elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": w.describe() + " forced alignment",
+            "B": w.B, "T_max": w.T_max, "U_max": w.U_max, "V": w.V, "variant": w.variant,
+            "valid_rows": ab["valid_rows"], "padded_rows": ab["padded_rows"],
+            "lattice_scores": "f64", "softmax": "f32",
+        },
+        "hbm_gbs_step": round(ab["k1_populate"] / (ms_per_step * 1e-3) / 1e9, 1),
+        "hbm_frac_step": round(ab["k1_populate"] / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "kernel_ms": {"k1_populate": round(k1_ms, 5), "k2_viterbi": round(kv_ms, 5)},
+        "kernel_gbs": {"k1_populate": round(k1_gbs, 1)},
+        "algorithmic_bytes": {"k1_populate": ab["k1_populate"], "step": ab["k1_populate"]},
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k1_populate (row log-normaliser and gather)",
+            "achieved": round(k1_gbs, 1),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(k1_gbs / PEAK_HBM_GBS, 4),
+            "traffic": profiled_traffic(args.workload, "k1_populate"),
+            "bytes_per_launch": ab["k1_populate"],
+            "launch_ms": round(k1_ms, 5),
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -159,6 +246,8 @@ def main():
     ap.add_argument("--workload", default="bpe", choices=["tiny", "char", "bpe", "wrnnt", "large"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=30.0, help="seconds of oracle work to time")
+    ap.add_argument("--mode", default="loss", choices=["loss", "viterbi"],
+                    help="loss: the fused loss + gradient (the headline metric); viterbi: forced alignment")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run --steps device-to-device copies of the workload's gradient size (the "
                          "known-size copy that calibrates the HBM byte counters), then exit")
@@ -184,7 +273,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle (budget %.0f s)" % args.cpu_budget)
-        cpu = cpu_baseline(w, tl, ul, labels, args.cpu_budget)
+        cpu = cpu_baseline(w, tl, ul, labels, args.cpu_budget, args.mode)
         log("[bench] cpu oracle: %.3g elements/s on %d cores" % (cpu["value"], cpu["cores"]))
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
@@ -194,6 +283,9 @@ def main():
     labels_d = torch.from_numpy(labels).to(dev)
     tl_d = torch.from_numpy(tl).to(dev)
     ul_d = torch.from_numpy(ul).to(dev)
+    if args.mode == "viterbi":
+        viterbi_bench(args, w, tl, ul, logits, labels_d, tl_d, ul_d, cpu)
+        return
     grad = torch.empty_like(logits)
     loss = torch.empty(w.B, dtype=torch.float32, device=dev)
     ws = torch.empty(binding.loss_workspace_bytes(w.B, w.T_max, w.U_max, w.V, binding.dtype_code(logits.dtype)),

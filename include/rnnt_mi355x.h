@@ -213,6 +213,14 @@ rnnt_status_t rnnt_viterbi(const void* logits, rnnt_shape_t shape, const int32_t
                            rnnt_variant_t variant, float* score_out, int32_t* label_frames_out,
                            int32_t* span_out, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* rnnt_viterbi, recording events[0..2] (caller-created hipEvent_t) on `stream`:
+ * before the populate kernel, after it, and after the alignment kernel. */
+rnnt_status_t rnnt_viterbi_timed(const void* logits, rnnt_shape_t shape, const int32_t* labels,
+                                 const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
+                                 rnnt_variant_t variant, float* score_out, int32_t* label_frames_out,
+                                 int32_t* span_out, void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                 hipEvent_t* events);
+
 /* Static description of a status code (never NULL). */
 const char* rnnt_status_string(rnnt_status_t status);
 

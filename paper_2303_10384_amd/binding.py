@@ -22,7 +22,8 @@ DTYPE_F32, DTYPE_BF16, DTYPE_F16 = 0, 1, 2
 
 # every symbol declared in include/rnnt_mi355x.h
 EXPORTED = ("rnnt_loss_workspace_bytes", "rnnt_loss", "rnnt_loss_timed", "rnnt_log_softmax_gather", "rnnt_lattice_workspace_bytes",
-            "rnnt_lattice_scores", "rnnt_status_string", "rnnt_version", "rnnt_viterbi_workspace_bytes", "rnnt_viterbi")
+            "rnnt_lattice_scores", "rnnt_status_string", "rnnt_version", "rnnt_viterbi_workspace_bytes", "rnnt_viterbi",
+            "rnnt_viterbi_timed")
 
 
 class Shape(ctypes.Structure):
@@ -65,6 +66,8 @@ def load_library():
     lib.rnnt_viterbi_workspace_bytes.restype = sz
     lib.rnnt_viterbi.argtypes = [vp, Shape, vp, vp, vp, i32, ctypes.c_int, vp, vp, vp, vp, sz, vp]
     lib.rnnt_viterbi.restype = ctypes.c_int
+    lib.rnnt_viterbi_timed.argtypes = [vp, Shape, vp, vp, vp, i32, ctypes.c_int, vp, vp, vp, vp, sz, vp, vp]
+    lib.rnnt_viterbi_timed.restype = ctypes.c_int
     lib.rnnt_status_string.argtypes = [ctypes.c_int]
     lib.rnnt_status_string.restype = ctypes.c_char_p
     lib.rnnt_version.argtypes = []
@@ -220,12 +223,15 @@ def viterbi_workspace_bytes(B, T_max, U_max, V, dtype_code_=DTYPE_F32):
     return load_library().rnnt_viterbi_workspace_bytes(Shape(B, T_max, U_max, V, dtype_code_, dtype_code_))
 
 
-def viterbi_align(logits, labels, logit_lens, label_lens, blank=0, variant="rnnt", workspace=None):
+def viterbi_align(logits, labels, logit_lens, label_lens, blank=0, variant="rnnt", workspace=None, outputs=None,
+                  events=None):
     """Forced alignment (best path) of every utterance.
 
     Returns (score (B,) float32 natural-log best path log-probability,
     label_frames (B, U_max) int32 frame of each unit or -1, span (B, 2) int32
-    first / last frame of the path).
+    first / last frame of the path).  outputs: optional preallocated (score,
+    label_frames, span); events: optional ctypes array of 3 hipEvent_t recorded
+    around the two kernels.
     """
     torch = _torch()
     lib = load_library()
@@ -241,16 +247,24 @@ def viterbi_align(logits, labels, logit_lens, label_lens, blank=0, variant="rnnt
     if variant not in VARIANTS:
         raise ValueError("variant must be one of %s" % sorted(VARIANTS))
     dev = logits.device
-    score = torch.empty(shape.B, dtype=torch.float32, device=dev)
-    frames = torch.empty((shape.B, shape.U_max), dtype=torch.int32, device=dev)
-    span = torch.empty((shape.B, 2), dtype=torch.int32, device=dev)
+    if outputs is None:
+        score = torch.empty(shape.B, dtype=torch.float32, device=dev)
+        frames = torch.empty((shape.B, shape.U_max), dtype=torch.int32, device=dev)
+        span = torch.empty((shape.B, 2), dtype=torch.int32, device=dev)
+    else:
+        score, frames, span = outputs
+        _check_gpu("score", score, torch.float32)
+        _check_gpu("label_frames", frames, torch.int32)
+        _check_gpu("span", span, torch.int32)
+        if score.shape != (shape.B,) or frames.shape != (shape.B, shape.U_max) or span.shape != (shape.B, 2):
+            raise ValueError("outputs must be (B,), (B, U_max) and (B, 2)")
     ws_ptr, ws_bytes = ctypes.c_void_p(0), 0
     if workspace is not None:
         _check_gpu("workspace", workspace)
         ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
-    st = lib.rnnt_viterbi(_ptr(logits), shape, _ptr(labels), _ptr(logit_lens), _ptr(label_lens), int(blank),
-                          VARIANTS[variant], _ptr(score), _ptr(frames), _ptr(span), ws_ptr, ws_bytes,
-                          _stream_handle(dev))
+    args = (_ptr(logits), shape, _ptr(labels), _ptr(logit_lens), _ptr(label_lens), int(blank), VARIANTS[variant],
+            _ptr(score), _ptr(frames), _ptr(span), ws_ptr, ws_bytes, _stream_handle(dev))
+    st = lib.rnnt_viterbi(*args) if events is None else lib.rnnt_viterbi_timed(*args, events)
     if st != RNNT_OK:
         raise RNNTError(st, "rnnt_viterbi")
     return score, frames, span

@@ -459,10 +459,11 @@ size_t rnnt_viterbi_workspace_bytes(rnnt_shape_t shape) {
   return make_viterbi_layout(s).total;
 }
 
-rnnt_status_t rnnt_viterbi(const void* logits, rnnt_shape_t shape, const int32_t* labels,
-                           const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
-                           rnnt_variant_t variant, float* score_out, int32_t* label_frames_out, int32_t* span_out,
-                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+rnnt_status_t rnnt_viterbi_timed(const void* logits, rnnt_shape_t shape, const int32_t* labels,
+                                 const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
+                                 rnnt_variant_t variant, float* score_out, int32_t* label_frames_out,
+                                 int32_t* span_out, void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                 hipEvent_t* events) {
   shape.grad_dtype = shape.dtype;  // no gradient here
   rnnt_status_t st = check_shape(shape);
   if (st != RNNT_OK) return st;
@@ -478,6 +479,8 @@ rnnt_status_t rnnt_viterbi(const void* logits, rnnt_shape_t shape, const int32_t
   char* ws = nullptr;
   st = take_workspace(workspace, workspace_bytes, L.total, stream, scratch, &ws);
   if (st != RNNT_OK) return st;
+  auto mark = [&](int i) { return events ? hipEventRecord(events[i], stream) : hipSuccess; };
+  if (mark(0) != hipSuccess) return RNNT_ERR_HIP;
 
   PopulateParams p1{};
   p1.logits = logits;
@@ -493,6 +496,7 @@ rnnt_status_t rnnt_viterbi(const void* logits, rnnt_shape_t shape, const int32_t
   p1.lp2 = reinterpret_cast<double2*>(ws + L.lp2);
   p1.lse2 = reinterpret_cast<float*>(ws + L.lse2);
   if (launch_k1_dtype<true>(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (mark(1) != hipSuccess) return RNNT_ERR_HIP;
 
   ViterbiParams pv{};
   pv.B = shape.B;
@@ -508,7 +512,16 @@ rnnt_status_t rnnt_viterbi(const void* logits, rnnt_shape_t shape, const int32_t
   pv.score_out = score_out;
   pv.label_frames = label_frames_out;
   pv.span = span_out;
-  return launch_k2v(variant, pv, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
+  if (launch_k2v(variant, pv, stream) != hipSuccess) return RNNT_ERR_HIP;
+  return mark(2) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
+}
+
+rnnt_status_t rnnt_viterbi(const void* logits, rnnt_shape_t shape, const int32_t* labels,
+                           const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
+                           rnnt_variant_t variant, float* score_out, int32_t* label_frames_out, int32_t* span_out,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return rnnt_viterbi_timed(logits, shape, labels, logit_lens, label_lens, blank, variant, score_out,
+                            label_frames_out, span_out, workspace, workspace_bytes, stream, nullptr);
 }
 
 rnnt_status_t rnnt_log_softmax_gather(const void* logits, rnnt_shape_t shape, const int32_t* labels,

@@ -18,8 +18,8 @@
 // arc.  Each step stores, per lane slot k, the wave's ballot of those bits: one
 // 64-bit word per (diagonal, k), bit j for unit K*j + k.  The same wave then
 // walks back from the path's end, one diagonal per step, reading the words
-// through a window of 64 words held one per lane (refilled every 64 words, so
-// no step waits on memory), and records each unit's frame in LDS.
+// through a window of 64 words held one per lane, with the next 64 words loaded
+// ahead (so no step waits on memory), and records each unit's frame in LDS.
 #pragma once
 
 #include "rnnt_device.h"
@@ -61,7 +61,7 @@ __device__ __forceinline__ V from_lane(V x, int lane) {
 // VAR: 0 RNN-T, 1 W-Transducer force-final, 2 allow-ignore.
 template <int K, int PF, int VAR>
 __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
-  __shared__ int s_frames[kViterbiMaxUnits1];
+  __shared__ int s_frames[kViterbiMaxUnits1 + 1];  // the last slot takes the stores of blank moves
   const int b = blockIdx.x;
   const int lane = threadIdx.x;
   const int T = p.logit_lens[b];
@@ -188,30 +188,39 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
   // ---------------- backtrace ----------------
   __syncthreads();  // the decision words stored above are read back below
   int u = U, start_frame = 0;
-  int w_lo = 0x7fffffff;  // words [w_lo, w_lo + 64) are in `win`, one per lane
-  uint64_t win = 0;
-  while (t + u > 0) {
-    const int dd = t + u;
-    const int widx = dd * K + u % K;
-    if (widx < w_lo) {
-      const int w_hi = dd * K + K - 1;
-      w_lo = max(0, w_hi - 63);
-      win = (w_lo + lane <= w_hi) ? dec_utt[w_lo + lane] : 0;
+  // Two windows of 64 words, one per lane, in turn: the walk reads one while the next
+  // 64 words below load into the other (a copy between them would wait for that load).
+  // A step moves the word index down by at most 2K-1 < 64, so the walk leaves a window
+  // only into the next one.
+  auto load_window = [&](int lo) { return lo + lane >= 0 ? dec_utt[lo + lane] : uint64_t{0}; };
+  // walks while its word lies in [lo, lo + 64); true once (0,0) is reached or the path jumped
+  auto walk = [&](const uint64_t& win, int lo) {
+    while (t + u > 0) {
+      const int widx = (t + u) * K + u % K;
+      if (widx < lo) return false;
+      const uint64_t wd = readlane_u64(win, widx - lo);
+      const bool bit = (wd >> (u / K)) & 1u;
+      // the move, without branches: the label arc (t,u-1)->(t,u) (the only way into (0,u))
+      // emits unit u at frame t; at u = 0 a set bit is the initial wild-card arc from (0,0)
+      const bool label = u > 0 && (bit || t == 0);
+      const bool jumped = VAR != 0 && u == 0 && bit;
+      s_frames[label ? u - 1 : kViterbiMaxUnits1] = t;  // every lane the same value; a spare slot otherwise
+      start_frame = jumped ? t : start_frame;
+      u -= label ? 1 : 0;
+      t = jumped ? 0 : t - (label ? 0 : 1);  // a jump ends the walk: (t,u) becomes (0,0)
     }
-    const uint64_t wd = readlane_u64(win, widx - w_lo);
-    const bool bit = (wd >> (u / K)) & 1u;
-    if (u == 0) {
-      if (VAR != 0 && bit) {  // entered from (0,0) by the initial wild-card arc
-        start_frame = t;
-        break;
-      }
-      --t;
-    } else if (bit || t == 0) {  // label arc (t,u-1)->(t,u) (the only way into (0,u)): unit u at frame t
-      if (lane == 0) s_frames[u - 1] = t;
-      --u;
-    } else {
-      --t;
-    }
+    return true;
+  };
+  int lo = (t + u) * K + K - 64;
+  uint64_t win_a = load_window(lo);
+  uint64_t win_b = load_window(lo - 64);
+  while (true) {
+    if (walk(win_a, lo)) break;
+    lo -= 64;
+    win_a = load_window(lo - 64);
+    if (walk(win_b, lo)) break;
+    lo -= 64;
+    win_b = load_window(lo - 64);
   }
   __syncthreads();
   for (int i = lane; i < p.U_max; i += 64)

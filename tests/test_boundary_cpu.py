@@ -30,7 +30,8 @@ def test_header_declares_the_documented_entry_points():
     names = declared_functions()
     assert names == sorted(["rnnt_loss_workspace_bytes", "rnnt_loss", "rnnt_loss_timed", "rnnt_log_softmax_gather",
                             "rnnt_lattice_workspace_bytes", "rnnt_lattice_scores", "rnnt_status_string",
-                            "rnnt_version", "rnnt_viterbi_workspace_bytes", "rnnt_viterbi"])
+                            "rnnt_version", "rnnt_viterbi_workspace_bytes", "rnnt_viterbi",
+                            "rnnt_viterbi_timed"])
 
 
 def test_every_declared_symbol_is_exported(lib):

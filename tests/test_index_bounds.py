@@ -244,9 +244,10 @@ def test_posterior_kernel_tiles_cover_every_row_once(B, T, U, V, dt):
 
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
 def test_viterbi_kernel_addresses(B, T, U, V, dt):
-    """Forced-alignment kernel: decision words stored at row min(d, D+1), K words a row, and the
-    backtrace's windows [w_lo, w_hi] (w_hi = d*K + K-1, w_lo = max(0, w_hi - 63)) inside the
-    utterance's (T_max+U_max+1)*K words; every word the walk reads lies in its window."""
+    """Forced-alignment kernel: decision words stored at row min(d, D+1), K words a row; the
+    backtrace's windows of 64 words start at w_lo = D_end*K + K - 64 and step down by 64, each load
+    (index w_lo + lane, skipped below 0) inside the utterance's (T_max+U_max+1)*K words, and every
+    word the walk reads lies in the current window."""
     U1 = U + 1
     ND = T + U
     K = next(k for k in (1, 2, 4, 8, 16) if U1 <= 64 * k)
@@ -261,14 +262,19 @@ def test_viterbi_kernel_addresses(B, T, U, V, dt):
         # a walk that takes every label move first, then every blank move (and the reverse)
         for labels_first in (True, False):
             t, u = Tb - 1, Ub
-            w_lo = None
+            w_lo = (t + u) * K + K - 64
+
+            def window_ok(lo):
+                idx = lo + np.arange(64)
+                idx = idx[idx >= 0]
+                return np.all(idx < words)
+            assert window_ok(w_lo) and window_ok(w_lo - 64)
             while t + u > 0:
                 dd = t + u
                 widx = dd * K + u % K
-                if w_lo is None or widx < w_lo:
-                    w_hi = dd * K + K - 1
-                    w_lo = max(0, w_hi - 63)
-                    assert 0 <= w_lo and w_hi < words
+                if widx < w_lo:
+                    w_lo -= 64
+                    assert window_ok(w_lo - 64)
                 assert w_lo <= widx <= w_lo + 63
                 assert 0 <= u // K < 64
                 if (labels_first and u > 0) or t == 0:
