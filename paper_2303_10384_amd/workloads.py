@@ -136,3 +136,34 @@ def small_case(B, T_max, U_max, V, seed, sigma=1.5, dtype="f32", full=False, bla
     labels = non_blank[rng.integers(0, len(non_blank), size=(B, U_max))].astype(np.int32)
     logits = (rng.standard_normal(size=(B, T_max, U_max + 1, V)) * sigma).astype(np.float32)
     return logits, tl, ul, labels
+
+
+ARC_DTYPE = np.dtype([("src", "<i4"), ("dst", "<i4"), ("t", "<i4"), ("u", "<i4"), ("label", "<i4"),
+                      ("score", "<f4")])
+
+
+def random_arc_lattice(rng, T_b, U_b, V, n_states, n_arcs, eps_frac=0.2, score_sigma=0.5, long_frac=0.1):
+    """A seeded random acyclic lattice over one utterance's rows (structure only).
+
+    States 0 .. n_states-1 (0 the start, n_states-1 the final state).  A chain
+    0 -> 1 -> ... -> n_states-1 guarantees a complete path; the other arcs join
+    random pairs src < dst, mostly between nearby states, a share `long_frac`
+    anywhere.  Each arc reads a random row (t < T_b, u <= U_b) and label, or,
+    with probability eps_frac, no logits (label -1); scores are N(0, score_sigma).
+    Returns (n_states, arcs) with arcs a numpy array of ARC_DTYPE.
+    """
+    n_states = max(1, int(n_states))
+    pairs = [(s, s + 1) for s in range(n_states - 1)]
+    while len(pairs) < n_arcs and n_states >= 2:
+        s = int(rng.integers(0, n_states - 1))
+        if rng.random() < long_frac:
+            d = int(rng.integers(s + 1, n_states))
+        else:
+            d = min(n_states - 1, s + 1 + int(rng.integers(0, 3)))
+        pairs.append((s, d))
+    arcs = np.zeros(len(pairs), ARC_DTYPE)
+    for i, (s, d) in enumerate(pairs):
+        eps = rng.random() < eps_frac
+        arcs[i] = (s, d, 0 if eps else rng.integers(0, T_b), 0 if eps else rng.integers(0, U_b + 1),
+                   -1 if eps else rng.integers(0, V), rng.standard_normal() * score_sigma)
+    return n_states, arcs[rng.permutation(len(arcs))]
