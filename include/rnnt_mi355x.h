@@ -58,7 +58,10 @@ typedef enum {
   RNNT_ERR_WORKSPACE = 6,    /* workspace given but smaller than required        */
   RNNT_ERR_ALIGNMENT = 7,    /* logits or grad not 16-byte aligned               */
   RNNT_ERR_HIP = 8,          /* a HIP runtime call failed (launch, allocation)   */
-  RNNT_ERR_UNSUPPORTED = 9   /* shape outside what this build handles (U_max+1 > 1024) */
+  RNNT_ERR_UNSUPPORTED = 9,  /* shape outside what this build handles (U_max+1 > 1024,
+                                or an arc-list lattice beyond the sweep's limits)   */
+  RNNT_ERR_BAD_LATTICE = 10  /* an arc list that breaks the numbering rules of
+                                rnnt_arc_plan, or a plan that does not match      */
 } rnnt_status_t;
 
 typedef enum {
@@ -220,6 +223,111 @@ rnnt_status_t rnnt_viterbi_timed(const void* logits, rnnt_shape_t shape, const i
                                  rnnt_variant_t variant, float* score_out, int32_t* label_frames_out,
                                  int32_t* span_out, void* workspace, size_t workspace_bytes, hipStream_t stream,
                                  hipEvent_t* events);
+
+/* ---------------------------------------------------------------------------
+ * Lattices given as arc lists (Section 2.2: the lattice is built as a graph and
+ * its arcs are filled in by indexed selection from X = log_softmax(logits) with
+ * each arc's time index, unit index and label; the grid of Fig. 1 and the
+ * W-Transducer lattices of Fig. 4 are particular arc lists, and a new loss is a
+ * new graph, with no new kernel).
+ *
+ * An arc leaves state src for state dst and weighs (natural log)
+ *     score + ln softmax(logits[b, t, u, :])[label]    when label >= 0,
+ *     score                                            when label == -1 (an arc
+ *                                                      that reads no logits).
+ * Per utterance the states are numbered 0 .. n_b-1: 0 is the start, n_b-1 the
+ * final state, and every arc goes from a lower to a higher number (n_b = 1 is
+ * the lattice whose only path is empty).  Parallel arcs are separate entries
+ * and their probabilities add.
+ *     loss_b = -ln (sum over start -> final paths of exp(sum of arc weights)),
+ * +inf when no path reaches the final state (then the gradient is 0);
+ *     d loss_b / d logits[b, t, u, :] = sum over arcs a on row (t, u) of
+ *                                       g_a (softmax(logits[b, t, u]) - onehot(label_a)),
+ * g_a the arc's posterior.
+ *
+ * Work splits in two:
+ *   rnnt_arc_plan (host only) rearranges a batch's arc lists for the device
+ *     sweep -- topological levels, arcs grouped by destination level for the
+ *     forward sweep and by source level for the backward one, arcs grouped by
+ *     logits row for the gradient -- into one image of host memory, which the
+ *     caller copies to device memory as it is (it holds no pointers).
+ *   rnnt_arc_loss (device) computes the losses and the gradient of a batch of
+ *     logits with that device image.  The plan depends on the lattices only, not
+ *     on the logits or the lengths.
+ */
+typedef struct {
+  int32_t src, dst; /* states of the utterance, 0 <= src < dst < n_b                 */
+  int32_t t, u;     /* logits row read by the arc: 0 <= t < T_max, 0 <= u <= U_max  */
+                    /* (ignored when label == -1)                                  */
+  int32_t label;    /* vocabulary index in [0, V), or -1                            */
+  float score;      /* natural-log weight added to the arc                          */
+} rnnt_arc_t;
+
+/* Descriptor of a plan (host memory, filled by rnnt_arc_plan).  The sizes are
+ * informative; off[] and the chunk counts are read by rnnt_arc_loss. */
+typedef struct {
+  int32_t B, T_max, U_max, V, blank;
+  int32_t num_states, num_levels, num_arcs, num_row_arcs, num_extra_rows;
+  int32_t max_level_states, max_level_arcs, max_in_degree, max_pins;
+  int32_t state_chunks, arc_chunks; /* per-level register chunks of the sweep */
+  int64_t image_bytes;              /* bytes of the image to copy to the device */
+  int64_t off[16];                  /* byte offsets of the image's arrays       */
+} rnnt_arc_plan_t;
+
+/* Upper bound of the image bytes rnnt_arc_plan writes for a batch with these
+ * totals (0 if the arguments are out of range).  Host only. */
+size_t rnnt_arc_plan_bytes_bound(int32_t B, int32_t T_max, int32_t U_max, int64_t num_states, int64_t num_arcs);
+
+/* Plans a batch of B arc lists (host only; every pointer here is HOST memory).
+ *   num_states  (B): n_b >= 1;
+ *   arc_begin   (B+1): utterance b's arcs are arcs[arc_begin[b] .. arc_begin[b+1]),
+ *               arc_begin[0] = 0, non-decreasing;
+ *   arcs        the arc records, states local to their utterance;
+ *   image       receives the device image (image_bytes >= the bound above is
+ *               always enough); plan receives the descriptor.
+ * The logits shape (T_max, U_max, V) and blank are those of the later loss calls
+ * (blank decides how the gradient kernel groups a row's arcs).  Returns
+ * RNNT_ERR_BAD_LATTICE for an arc list breaking the rules above,
+ * RNNT_ERR_BAD_SHAPE / RNNT_ERR_BAD_BLANK for the shape, RNNT_ERR_WORKSPACE when
+ * image_bytes is too small, and RNNT_ERR_UNSUPPORTED past the sweep's limits:
+ * more than 4096 states on one topological level or 4096 arcs entering one, more
+ * than 2048 states per utterance and direction whose scores must outlive the
+ * sweep's 4096-state window (sources of arcs that span that many states), more
+ * than 1024 label arcs on a row that carries two or more non-blank labels,
+ * more than 2^27 states or arcs in one utterance, or batch totals of 2^31
+ * states, arcs or logits rows. */
+rnnt_status_t rnnt_arc_plan(int32_t B, int32_t T_max, int32_t U_max, int32_t V, int32_t blank,
+                            const int32_t* num_states, const int64_t* arc_begin, const rnnt_arc_t* arcs,
+                            void* image, size_t image_bytes, rnnt_arc_plan_t* plan);
+
+/* Bytes of device workspace rnnt_arc_loss needs with this plan (0 if plan is NULL). */
+size_t rnnt_arc_loss_workspace_bytes(const rnnt_arc_plan_t* plan);
+
+/* Loss and gradient of a batch of arc-list lattices.
+ *   logits, shape     as in rnnt_loss; (B, T_max, U_max, V) must equal the plan's;
+ *   logit_lens, label_lens  (B) int32: the valid rows of utterance b are t < T_b,
+ *                     u <= U_b; only those are read;
+ *   plan              the descriptor (HOST memory) from rnnt_arc_plan;
+ *   plan_image        the plan's image, copied to DEVICE memory (16-byte aligned);
+ *   loss_out          (B) float32: loss_b, +inf when no path reaches the final state;
+ *   grad_out          gradient as in rnnt_loss, or NULL for the loss alone.
+ * Data errors seen on the device -- T_b outside [1, T_max], U_b outside
+ * [0, U_max], an arc with a label that reads a row outside the utterance's valid
+ * rows, or NaN logits on a row an arc reads -- give loss NaN and a zero gradient
+ * for that utterance.  Workspace: rnnt_arc_loss_workspace_bytes(plan) bytes,
+ * 256-byte aligned, or NULL (then allocated stream-ordered). */
+rnnt_status_t rnnt_arc_loss(const void* logits, rnnt_shape_t shape, const int32_t* logit_lens,
+                            const int32_t* label_lens, const rnnt_arc_plan_t* plan, const void* plan_image,
+                            float* loss_out, void* grad_out, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream);
+
+/* rnnt_arc_loss, recording events[0..5] (caller-created) on `stream`: before the
+ * row normaliser, after it, after the arc populate kernel, after the sweep, after
+ * the row records, and after the gradient kernels. */
+rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const int32_t* logit_lens,
+                                  const int32_t* label_lens, const rnnt_arc_plan_t* plan, const void* plan_image,
+                                  float* loss_out, void* grad_out, void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream, hipEvent_t* events);
 
 /* Static description of a status code (never NULL). */
 const char* rnnt_status_string(rnnt_status_t status);

@@ -15,7 +15,7 @@ RNNT_OK = 0
 STATUS_NAMES = {
     0: "RNNT_OK", 1: "RNNT_ERR_NULL_PTR", 2: "RNNT_ERR_BAD_SHAPE", 3: "RNNT_ERR_BAD_BLANK",
     4: "RNNT_ERR_BAD_DTYPE", 5: "RNNT_ERR_BAD_VARIANT", 6: "RNNT_ERR_WORKSPACE", 7: "RNNT_ERR_ALIGNMENT",
-    8: "RNNT_ERR_HIP", 9: "RNNT_ERR_UNSUPPORTED",
+    8: "RNNT_ERR_HIP", 9: "RNNT_ERR_UNSUPPORTED", 10: "RNNT_ERR_BAD_LATTICE",
 }
 VARIANTS = {"rnnt": 0, "wrnnt": 1, "wrnnt_allow_ignore": 2}
 DTYPE_F32, DTYPE_BF16, DTYPE_F16 = 0, 1, 2
@@ -23,12 +23,21 @@ DTYPE_F32, DTYPE_BF16, DTYPE_F16 = 0, 1, 2
 # every symbol declared in include/rnnt_mi355x.h
 EXPORTED = ("rnnt_loss_workspace_bytes", "rnnt_loss", "rnnt_loss_timed", "rnnt_log_softmax_gather", "rnnt_lattice_workspace_bytes",
             "rnnt_lattice_scores", "rnnt_status_string", "rnnt_version", "rnnt_viterbi_workspace_bytes", "rnnt_viterbi",
-            "rnnt_viterbi_timed")
+            "rnnt_viterbi_timed", "rnnt_arc_plan_bytes_bound", "rnnt_arc_plan", "rnnt_arc_loss_workspace_bytes",
+            "rnnt_arc_loss", "rnnt_arc_loss_timed")
 
 
 class Shape(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("T_max", ctypes.c_int32), ("U_max", ctypes.c_int32),
                 ("V", ctypes.c_int32), ("dtype", ctypes.c_int), ("grad_dtype", ctypes.c_int)]
+
+
+class ArcPlanDesc(ctypes.Structure):
+    """rnnt_arc_plan_t."""
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "B", "T_max", "U_max", "V", "blank", "num_states", "num_levels", "num_arcs", "num_row_arcs",
+        "num_extra_rows", "max_level_states", "max_level_arcs", "max_in_degree", "max_pins", "state_chunks",
+        "arc_chunks")] + [("image_bytes", ctypes.c_int64), ("off", ctypes.c_int64 * 16)]
 
 
 class RNNTError(RuntimeError):
@@ -68,6 +77,17 @@ def load_library():
     lib.rnnt_viterbi.restype = ctypes.c_int
     lib.rnnt_viterbi_timed.argtypes = [vp, Shape, vp, vp, vp, i32, ctypes.c_int, vp, vp, vp, vp, sz, vp, vp]
     lib.rnnt_viterbi_timed.restype = ctypes.c_int
+    i64 = ctypes.c_int64
+    lib.rnnt_arc_plan_bytes_bound.argtypes = [i32, i32, i32, i64, i64]
+    lib.rnnt_arc_plan_bytes_bound.restype = sz
+    lib.rnnt_arc_plan.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, sz, ctypes.POINTER(ArcPlanDesc)]
+    lib.rnnt_arc_plan.restype = ctypes.c_int
+    lib.rnnt_arc_loss_workspace_bytes.argtypes = [ctypes.POINTER(ArcPlanDesc)]
+    lib.rnnt_arc_loss_workspace_bytes.restype = sz
+    lib.rnnt_arc_loss.argtypes = [vp, Shape, vp, vp, ctypes.POINTER(ArcPlanDesc), vp, vp, vp, vp, sz, vp]
+    lib.rnnt_arc_loss.restype = ctypes.c_int
+    lib.rnnt_arc_loss_timed.argtypes = [vp, Shape, vp, vp, ctypes.POINTER(ArcPlanDesc), vp, vp, vp, vp, sz, vp, vp]
+    lib.rnnt_arc_loss_timed.restype = ctypes.c_int
     lib.rnnt_status_string.argtypes = [ctypes.c_int]
     lib.rnnt_status_string.restype = ctypes.c_char_p
     lib.rnnt_version.argtypes = []
@@ -268,3 +288,101 @@ def viterbi_align(logits, labels, logit_lens, label_lens, blank=0, variant="rnnt
     if st != RNNT_OK:
         raise RNNTError(st, "rnnt_viterbi")
     return score, frames, span
+
+
+class ArcPlan:
+    """A batch of arc-list lattices planned by rnnt_arc_plan: the descriptor
+    (`desc`, host) and the image (`image`, a uint8 tensor, on the device once
+    `to()` has copied it there)."""
+
+    def __init__(self, desc, image):
+        self.desc = desc
+        self.image = image
+
+    def to(self, device):
+        return ArcPlan(self.desc, self.image.to(device))
+
+    def __getattr__(self, name):  # the descriptor's sizes
+        if name in ("desc", "image"):
+            raise AttributeError(name)
+        return getattr(self.desc, name)
+
+
+def arc_plan(lattices, T_max, U_max, V, blank=0, device=None):
+    """Plan a batch of lattices given as arc lists (host work, in the library).
+
+    lattices: one (n_states, arcs) per utterance, arcs a numpy array of
+    topologies.ARC_DTYPE (states local to the utterance).  Returns an ArcPlan,
+    its image moved to `device` when given.
+    """
+    import numpy as np
+    from .topologies import ARC_DTYPE
+    torch = _torch()
+    lib = load_library()
+    B = len(lattices)
+    num_states = np.array([int(n) for n, _ in lattices], np.int32)
+    arc_lists = [np.ascontiguousarray(np.asarray(a, dtype=ARC_DTYPE)) for _, a in lattices]
+    counts = np.array([len(a) for a in arc_lists], np.int64)
+    arc_begin = np.zeros(B + 1, np.int64)
+    np.cumsum(counts, out=arc_begin[1:])
+    arcs = np.concatenate(arc_lists) if B else np.zeros(0, ARC_DTYPE)
+    arcs = np.ascontiguousarray(arcs, dtype=ARC_DTYPE)
+    bound = lib.rnnt_arc_plan_bytes_bound(B, int(T_max), int(U_max), int(num_states.sum()), int(arc_begin[-1]))
+    if bound == 0:
+        raise RNNTError(2, "rnnt_arc_plan_bytes_bound")
+    image = torch.empty(bound, dtype=torch.uint8)
+    desc = ArcPlanDesc()
+    st = lib.rnnt_arc_plan(B, int(T_max), int(U_max), int(V), int(blank), num_states.ctypes.data,
+                           arc_begin.ctypes.data, arcs.ctypes.data if len(arcs) else None,
+                           ctypes.c_void_p(image.data_ptr()), bound, ctypes.byref(desc))
+    if st != RNNT_OK:
+        raise RNNTError(st, "rnnt_arc_plan")
+    plan = ArcPlan(desc, image[:desc.image_bytes].clone())
+    return plan.to(device) if device is not None else plan
+
+
+def arc_loss_workspace_bytes(plan):
+    return load_library().rnnt_arc_loss_workspace_bytes(ctypes.byref(plan.desc))
+
+
+def arc_loss(logits, logit_lens, label_lens, plan, need_grad=True, workspace=None, grad_out=None, loss_out=None,
+             events=None, grad_dtype=None):
+    """Per-utterance loss (float32 (B,)) and gradient of a batch of arc-list lattices.
+
+    logits (B, T_max, U_max+1, V) on the GPU; logit_lens, label_lens (B,) int32;
+    plan: an ArcPlan whose image is on the logits' device.  events: optional
+    ctypes array of 6 hipEvent_t recorded around the kernels.
+    """
+    torch = _torch()
+    lib = load_library()
+    _check_gpu("logits", logits)
+    _check_gpu("logit_lens", logit_lens, torch.int32)
+    _check_gpu("label_lens", label_lens, torch.int32)
+    _check_gpu("plan image", plan.image, torch.uint8)
+    if logits.dim() != 4:
+        raise ValueError("logits must be (B, T_max, U_max+1, V)")
+    if grad_out is not None and grad_dtype is None:
+        grad_dtype = grad_out.dtype
+    shape = shape_of(logits, grad_dtype)
+    if logit_lens.shape != (shape.B,) or label_lens.shape != (shape.B,):
+        raise ValueError("the length vectors must be (B,)")
+    dev = logits.device
+    loss = loss_out if loss_out is not None else torch.empty(shape.B, dtype=torch.float32, device=dev)
+    _check_gpu("loss_out", loss, torch.float32)
+    grad = None
+    if need_grad:
+        gdt = logits.dtype if grad_dtype is None else grad_dtype
+        grad = grad_out if grad_out is not None else torch.empty(logits.shape, dtype=gdt, device=dev)
+        _check_gpu("grad_out", grad, gdt)
+        if grad.shape != logits.shape:
+            raise ValueError("grad_out must have the logits' shape")
+    ws_ptr, ws_bytes = ctypes.c_void_p(0), 0
+    if workspace is not None:
+        _check_gpu("workspace", workspace)
+        ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
+    args = (_ptr(logits), shape, _ptr(logit_lens), _ptr(label_lens), ctypes.byref(plan.desc), _ptr(plan.image),
+            _ptr(loss), _ptr(grad), ws_ptr, ws_bytes, _stream_handle(dev))
+    st = lib.rnnt_arc_loss(*args) if events is None else lib.rnnt_arc_loss_timed(*args, events)
+    if st != RNNT_OK:
+        raise RNNTError(st, "rnnt_arc_loss")
+    return loss, grad

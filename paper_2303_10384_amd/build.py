@@ -10,9 +10,9 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB_NAME = "librnnt_mi355x.so"
-SOURCES = ["csrc/rnnt_api.hip"]
+SOURCES = ["csrc/rnnt_api.hip", "csrc/rnnt_arc_plan.cpp"]
 HEADERS = ["csrc/rnnt_device.h", "csrc/rnnt_k1_populate.h", "csrc/rnnt_k2_lattice.h", "csrc/rnnt_k2_viterbi.h",
-           "csrc/rnnt_k3_grad.h"]
+           "csrc/rnnt_k3_grad.h", "csrc/rnnt_arc_layout.h", "csrc/rnnt_arc_kernels.h"]
 
 
 def hipcc():

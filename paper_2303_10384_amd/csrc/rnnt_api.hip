@@ -11,6 +11,7 @@
 #include "rnnt_k2_lattice.h"
 #include "rnnt_k3_grad.h"
 #include "rnnt_k2_viterbi.h"
+#include "rnnt_arc_kernels.h"
 
 namespace rnnt {
 namespace {
@@ -114,26 +115,26 @@ void k1_blocking(PopulateParams& p) {
   p.n_ublk = (p.U_max + 1 + p.rows_per_block - 1) / p.rows_per_block;
 }
 
-template <typename T, int G, int NB, bool LATTICE, bool FAST>
+template <typename T, int G, int NB, int OUT, bool FAST>
 hipError_t launch_k1_g(PopulateParams p, hipStream_t stream) {
   k1_blocking(p);
   const int64_t blocks = static_cast<int64_t>(p.B) * (p.T_max + p.U_max) * p.n_ublk;
   const int64_t runs = (blocks + kXcdRun - 1) / kXcdRun;  // whole rounds of the XCD-major numbering
   const int64_t grid = (runs + kXcds - 1) / kXcds * kXcds * kXcdRun;
   if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((k1_populate<T, G, NB, LATTICE, FAST>), dim3(static_cast<uint32_t>(grid)), dim3(256), 0,
+  hipLaunchKernelGGL((k1_populate<T, G, NB, OUT, FAST>), dim3(static_cast<uint32_t>(grid)), dim3(256), 0,
                      stream, p);
   return hipGetLastError();
 }
 
-template <typename T, int G, bool LATTICE>
+template <typename T, int G, int OUT>
 hipError_t launch_k1_nb(int nb, const PopulateParams& p, hipStream_t stream) {
   switch (nb) {
-    case 1: return launch_k1_g<T, G, 1, LATTICE, true>(p, stream);
-    case 2: return launch_k1_g<T, G, 2, LATTICE, true>(p, stream);
-    case 3: return launch_k1_g<T, G, 3, LATTICE, true>(p, stream);
-    case 4: return launch_k1_g<T, G, 4, LATTICE, true>(p, stream);
-    default: return launch_k1_g<T, G, 5, LATTICE, true>(p, stream);
+    case 1: return launch_k1_g<T, G, 1, OUT, true>(p, stream);
+    case 2: return launch_k1_g<T, G, 2, OUT, true>(p, stream);
+    case 3: return launch_k1_g<T, G, 3, OUT, true>(p, stream);
+    case 4: return launch_k1_g<T, G, 4, OUT, true>(p, stream);
+    default: return launch_k1_g<T, G, 5, OUT, true>(p, stream);
   }
 }
 
@@ -145,24 +146,24 @@ bool k1_span_fits(PopulateParams p, int elem_bytes) {
   return rows * p.V * elem_bytes + 64 < 0x7fffffffLL;
 }
 
-template <typename T, bool LATTICE>
+template <typename T, int OUT>
 hipError_t launch_k1(const PopulateParams& p, hipStream_t stream) {
   const K1Shape ks = k1_shape<T>(p.V);
-  if (!ks.fast || !k1_span_fits(p, static_cast<int>(sizeof(T)))) return launch_k1_g<T, 64, 5, LATTICE, false>(p, stream);
+  if (!ks.fast || !k1_span_fits(p, static_cast<int>(sizeof(T)))) return launch_k1_g<T, 64, 5, OUT, false>(p, stream);
   switch (ks.G) {
-    case 8: return launch_k1_nb<T, 8, LATTICE>(ks.NB, p, stream);
-    case 16: return launch_k1_nb<T, 16, LATTICE>(ks.NB, p, stream);
-    case 32: return launch_k1_nb<T, 32, LATTICE>(ks.NB, p, stream);
-    default: return launch_k1_nb<T, 64, LATTICE>(ks.NB, p, stream);
+    case 8: return launch_k1_nb<T, 8, OUT>(ks.NB, p, stream);
+    case 16: return launch_k1_nb<T, 16, OUT>(ks.NB, p, stream);
+    case 32: return launch_k1_nb<T, 32, OUT>(ks.NB, p, stream);
+    default: return launch_k1_nb<T, 64, OUT>(ks.NB, p, stream);
   }
 }
 
-template <bool LATTICE>
+template <int OUT>
 hipError_t launch_k1_dtype(rnnt_dtype_t dt, const PopulateParams& p, hipStream_t stream) {
   switch (dt) {
-    case RNNT_DTYPE_F32: return launch_k1<float, LATTICE>(p, stream);
-    case RNNT_DTYPE_BF16: return launch_k1<bf16_t, LATTICE>(p, stream);
-    default: return launch_k1<f16_t, LATTICE>(p, stream);
+    case RNNT_DTYPE_F32: return launch_k1<float, OUT>(p, stream);
+    case RNNT_DTYPE_BF16: return launch_k1<bf16_t, OUT>(p, stream);
+    default: return launch_k1<f16_t, OUT>(p, stream);
   }
 }
 
@@ -302,6 +303,114 @@ rnnt_status_t take_workspace(void* workspace, size_t workspace_bytes, size_t nee
   return RNNT_OK;
 }
 
+// ---- arc-list lattices -------------------------------------------------------
+
+// Workspace of rnnt_arc_loss, 256-byte aligned pieces (R logits rows, A arcs,
+// S states of the plan):
+//   lse2     R double   lse * log2(e) per row
+//   w0, w1   A double   arc weights in the two sweep orders
+//   val0/1   S double   forward / backward scores
+//   lnp      2*B double
+//   status   B int32
+//   rowinfo  R RowInfo  (with a gradient)
+struct ArcLayout {
+  size_t lse2, w0, w1, val0, val1, lnp, status, rowinfo, total;
+};
+
+ArcLayout make_arc_layout(const rnnt_arc_plan_t& pl) {
+  const size_t R = static_cast<size_t>(pl.B) * pl.T_max * (static_cast<size_t>(pl.U_max) + 1);
+  const size_t A = static_cast<size_t>(pl.num_arcs), S = static_cast<size_t>(pl.num_states);
+  ArcLayout L{};
+  size_t o = 0;
+  L.lse2 = o;
+  o = align256(o + R * sizeof(double));
+  L.w0 = o;
+  o = align256(o + A * sizeof(double));
+  L.w1 = o;
+  o = align256(o + A * sizeof(double));
+  L.val0 = o;
+  o = align256(o + S * sizeof(double));
+  L.val1 = o;
+  o = align256(o + S * sizeof(double));
+  L.lnp = o;
+  o = align256(o + 2 * static_cast<size_t>(pl.B) * sizeof(double));
+  L.status = o;
+  o = align256(o + static_cast<size_t>(pl.B) * sizeof(int32_t));
+  L.rowinfo = o;
+  o = align256(o + R * sizeof(RowInfo));
+  L.total = o;
+  return L;
+}
+
+// The descriptor must describe an image of this shape with its arrays in order.
+bool plan_consistent(const rnnt_arc_plan_t& pl, const rnnt_shape_t& s) {
+  if (pl.B != s.B || pl.T_max != s.T_max || pl.U_max != s.U_max || pl.V != s.V) return false;
+  if (pl.num_states < pl.B || pl.num_arcs < 0 || pl.num_levels < pl.B || pl.num_row_arcs < 0 ||
+      pl.num_extra_rows < 0)
+    return false;
+  const int64_t R = static_cast<int64_t>(pl.B) * pl.T_max * (static_cast<int64_t>(pl.U_max) + 1);
+  if (R >= 0x7fffffffLL || pl.blank < 0 || pl.blank >= pl.V) return false;
+  for (int i = 0; i < kImgCount; ++i) {
+    if (pl.off[i] < 0 || (pl.off[i] & 255) || pl.off[i] > pl.image_bytes) return false;
+    if (i > 0 && pl.off[i] < pl.off[i - 1]) return false;
+  }
+  return true;
+}
+
+template <int NC, int NS>
+hipError_t launch_sweep_ns(const ArcSweepParams& p, hipStream_t stream) {
+  hipLaunchKernelGGL((k_arc_sweep<NC, NS>), dim3(2 * p.B), dim3(64), 0, stream, p);
+  return hipGetLastError();
+}
+
+template <int NC>
+hipError_t launch_sweep_nc(int ns, const ArcSweepParams& p, hipStream_t stream) {
+  switch (ns) {
+    case 1: return launch_sweep_ns<NC, 1>(p, stream);
+    case 2: return launch_sweep_ns<NC, 2>(p, stream);
+    case 4: return launch_sweep_ns<NC, 4>(p, stream);
+    default: return launch_sweep_ns<NC, 8>(p, stream);
+  }
+}
+
+hipError_t launch_sweep(int nc, int ns, const ArcSweepParams& p, hipStream_t stream) {
+  switch (nc) {
+    case 1: return launch_sweep_nc<1>(ns, p, stream);
+    case 2: return launch_sweep_nc<2>(ns, p, stream);
+    case 4: return launch_sweep_nc<4>(ns, p, stream);
+    default: return launch_sweep_nc<8>(ns, p, stream);
+  }
+}
+
+hipError_t launch_arc_populate(rnnt_dtype_t dt, const ArcPopulateParams& p, hipStream_t stream) {
+  if (p.n_arcs == 0) return hipSuccess;
+  const dim3 grid((p.n_arcs + 255) / 256);
+  switch (dt) {
+    case RNNT_DTYPE_F32: hipLaunchKernelGGL((k_arc_populate<float>), grid, dim3(256), 0, stream, p); break;
+    case RNNT_DTYPE_BF16: hipLaunchKernelGGL((k_arc_populate<bf16_t>), grid, dim3(256), 0, stream, p); break;
+    default: hipLaunchKernelGGL((k_arc_populate<f16_t>), grid, dim3(256), 0, stream, p); break;
+  }
+  return hipGetLastError();
+}
+
+template <typename Tin, typename Tout>
+hipError_t launch_extra_rows_t(const ArcExtraParams& p, int n, hipStream_t stream) {
+  hipLaunchKernelGGL((k_arc_extra_rows<Tin, Tout>), dim3(n), dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_extra_rows(rnnt_dtype_t dt, rnnt_dtype_t gdt, const ArcExtraParams& p, int n, hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  const bool f32_out = gdt == RNNT_DTYPE_F32;
+  switch (dt) {
+    case RNNT_DTYPE_F32: return launch_extra_rows_t<float, float>(p, n, stream);
+    case RNNT_DTYPE_BF16:
+      return f32_out ? launch_extra_rows_t<bf16_t, float>(p, n, stream) : launch_extra_rows_t<bf16_t, bf16_t>(p, n, stream);
+    default:
+      return f32_out ? launch_extra_rows_t<f16_t, float>(p, n, stream) : launch_extra_rows_t<f16_t, f16_t>(p, n, stream);
+  }
+}
+
 }  // namespace
 }  // namespace rnnt
 
@@ -320,12 +429,13 @@ const char* rnnt_status_string(rnnt_status_t status) {
     case RNNT_ERR_WORKSPACE: return "workspace smaller than required";
     case RNNT_ERR_ALIGNMENT: return "logits / grad must be 16-byte aligned, workspace 256-byte aligned";
     case RNNT_ERR_HIP: return "HIP runtime error";
-    case RNNT_ERR_UNSUPPORTED: return "unsupported shape (U_max + 1 > 1024)";
+    case RNNT_ERR_UNSUPPORTED: return "unsupported shape (U_max + 1 > 1024, or a lattice past the sweep's limits)";
+    case RNNT_ERR_BAD_LATTICE: return "arc list breaks the numbering rules, or the plan does not match the call";
   }
   return "unknown status";
 }
 
-const char* rnnt_version(void) { return "rnnt_mi355x 0.2.0 gfx950"; }
+const char* rnnt_version(void) { return "rnnt_mi355x 0.3.0 gfx950"; }
 
 size_t rnnt_loss_workspace_bytes(rnnt_shape_t shape) {
   if (check_shape(shape) != RNNT_OK) return 0;
@@ -379,7 +489,7 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
   p1.n_elem = n_elem;
   p1.lp2 = reinterpret_cast<double2*>(ws + L.lp2);
   p1.lse2 = reinterpret_cast<float*>(ws + L.lse2);
-  if (launch_k1_dtype<true>(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (launch_k1_dtype<kK1Lattice>(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(1) != hipSuccess) return RNNT_ERR_HIP;
 
   // kernel 2: forward / backward sweeps
@@ -495,7 +605,7 @@ rnnt_status_t rnnt_viterbi_timed(const void* logits, rnnt_shape_t shape, const i
   p1.n_elem = static_cast<int64_t>(shape.B) * shape.T_max * (shape.U_max + 1) * shape.V;
   p1.lp2 = reinterpret_cast<double2*>(ws + L.lp2);
   p1.lse2 = reinterpret_cast<float*>(ws + L.lse2);
-  if (launch_k1_dtype<true>(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (launch_k1_dtype<kK1Lattice>(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(1) != hipSuccess) return RNNT_ERR_HIP;
 
   ViterbiParams pv{};
@@ -524,6 +634,151 @@ rnnt_status_t rnnt_viterbi(const void* logits, rnnt_shape_t shape, const int32_t
                             label_frames_out, span_out, workspace, workspace_bytes, stream, nullptr);
 }
 
+size_t rnnt_arc_loss_workspace_bytes(const rnnt_arc_plan_t* plan) {
+  if (!plan) return 0;
+  return make_arc_layout(*plan).total;
+}
+
+rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const int32_t* logit_lens,
+                                  const int32_t* label_lens, const rnnt_arc_plan_t* plan, const void* plan_image,
+                                  float* loss_out, void* grad_out, void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream, hipEvent_t* events) {
+  rnnt_status_t st = check_shape(shape);
+  if (st != RNNT_OK) return st;
+  if (!logits || !logit_lens || !label_lens || !plan || !plan_image || !loss_out) return RNNT_ERR_NULL_PTR;
+  if (!plan_consistent(*plan, shape)) return RNNT_ERR_BAD_LATTICE;
+  if (!aligned16(logits) || (grad_out && !aligned16(grad_out)) || !aligned16(plan_image))
+    return RNNT_ERR_ALIGNMENT;
+  const ArcLayout L = make_arc_layout(*plan);
+  Scratch scratch;
+  char* ws = nullptr;
+  st = take_workspace(workspace, workspace_bytes, L.total, stream, scratch, &ws);
+  if (st != RNNT_OK) return st;
+  const char* img = static_cast<const char*>(plan_image);
+  auto arr = [&](int i) { return img + plan->off[i]; };
+
+  const int64_t U1 = shape.U_max + 1;
+  const int64_t n_rows = static_cast<int64_t>(shape.B) * shape.T_max * U1;
+  auto mark = [&](int i) { return events ? hipEventRecord(events[i], stream) : hipSuccess; };
+  if (mark(0) != hipSuccess) return RNNT_ERR_HIP;
+
+  // kernel 1 (rows form): lse * log2(e) of every valid row
+  PopulateParams p1{};
+  p1.logits = logits;
+  p1.B = shape.B;
+  p1.T_max = shape.T_max;
+  p1.U_max = shape.U_max;
+  p1.V = shape.V;
+  p1.blank = plan->blank;
+  p1.labels = nullptr;
+  p1.logit_lens = logit_lens;
+  p1.label_lens = label_lens;
+  p1.n_elem = n_rows * shape.V;
+  p1.lse2_rows = reinterpret_cast<double*>(ws + L.lse2);
+  if (launch_k1_dtype<kK1Rows>(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (mark(1) != hipSuccess) return RNNT_ERR_HIP;
+
+  // arc weights in both sweep orders
+  ArcPopulateParams pp{};
+  pp.logits = logits;
+  pp.B = shape.B;
+  pp.T_max = shape.T_max;
+  pp.U_max = shape.U_max;
+  pp.V = shape.V;
+  pp.n_arcs = plan->num_arcs;
+  pp.n_rows = static_cast<int32_t>(n_rows);
+  pp.logit_lens = logit_lens;
+  pp.label_lens = label_lens;
+  pp.arcs = reinterpret_cast<const int4*>(arr(kImgArcs));
+  pp.score = reinterpret_cast<const float*>(arr(kImgScore));
+  pp.perm = reinterpret_cast<const int32_t*>(arr(kImgPerm));
+  pp.lse2_rows = p1.lse2_rows;
+  pp.w0 = reinterpret_cast<double*>(ws + L.w0);
+  pp.w1 = reinterpret_cast<double*>(ws + L.w1);
+  if (launch_arc_populate(shape.dtype, pp, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (mark(2) != hipSuccess) return RNNT_ERR_HIP;
+
+  // forward and backward sweeps
+  ArcSweepParams ps{};
+  ps.B = shape.B;
+  ps.T_max = shape.T_max;
+  ps.U_max = shape.U_max;
+  ps.logit_lens = logit_lens;
+  ps.label_lens = label_lens;
+  ps.utt = reinterpret_cast<const int4*>(arr(kImgUtt));
+  ps.ends = reinterpret_cast<const int4*>(arr(kImgEnds));
+  for (int g = 0; g < 2; ++g) {
+    ps.level[g] = reinterpret_cast<const int4*>(arr(g ? kImgLevel1 : kImgLevel0));
+    ps.seg[g] = reinterpret_cast<const int32_t*>(arr(g ? kImgSeg1 : kImgSeg0));
+    ps.pin[g] = reinterpret_cast<const int32_t*>(arr(g ? kImgPin1 : kImgPin0));
+    ps.loc[g] = reinterpret_cast<const int32_t*>(arr(g ? kImgLoc1 : kImgLoc0));
+    ps.w[g] = g ? pp.w1 : pp.w0;
+    ps.val[g] = reinterpret_cast<double*>(ws + (g ? L.val1 : L.val0));
+  }
+  ps.lnp2 = reinterpret_cast<double*>(ws + L.lnp);
+  ps.status = reinterpret_cast<int32_t*>(ws + L.status);
+  ps.loss = loss_out;
+  if (launch_sweep(plan->arc_chunks, plan->state_chunks, ps, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (mark(3) != hipSuccess) return RNNT_ERR_HIP;
+
+  ArcRowParams pr{};
+  pr.T_max = shape.T_max;
+  pr.U_max = shape.U_max;
+  pr.blank = plan->blank;
+  pr.n_rows = static_cast<int32_t>(n_rows);
+  pr.n_arcs = plan->num_arcs;
+  pr.n_row_arcs = plan->num_row_arcs;
+  pr.n_states = plan->num_states;
+  pr.logit_lens = logit_lens;
+  pr.label_lens = label_lens;
+  pr.utt = ps.utt;
+  pr.arcs = pp.arcs;
+  pr.row_seg = reinterpret_cast<const int32_t*>(arr(kImgRowSeg));
+  pr.row_arc = reinterpret_cast<const int32_t*>(arr(kImgRowArc));
+  pr.w0 = pp.w0;
+  pr.val0 = ps.val[0];
+  pr.val1 = ps.val[1];
+  pr.lnp2 = ps.lnp2;
+  pr.status = ps.status;
+  pr.lse2_rows = p1.lse2_rows;
+  pr.rowinfo = reinterpret_cast<RowInfo*>(ws + L.rowinfo);
+  if (grad_out) {
+    hipLaunchKernelGGL(k_arc_rows, dim3(static_cast<uint32_t>((n_rows + 255) / 256)), dim3(256), 0, stream, pr);
+    if (hipGetLastError() != hipSuccess) return RNNT_ERR_HIP;
+  }
+  if (mark(4) != hipSuccess) return RNNT_ERR_HIP;
+
+  if (grad_out) {
+    GradParams p3{};
+    p3.logits = logits;
+    p3.grad = grad_out;
+    p3.rowinfo = pr.rowinfo;
+    p3.n_elem = n_rows * shape.V;
+    p3.n_rows = n_rows;
+    p3.V = shape.V;
+    p3.blank = plan->blank;
+    if (launch_k3_dtype(shape.dtype, shape.grad_dtype, p3, stream) != hipSuccess) return RNNT_ERR_HIP;
+    ArcExtraParams px{};
+    px.rows = pr;
+    px.logits = logits;
+    px.grad = grad_out;
+    px.xrows = reinterpret_cast<const int32_t*>(arr(kImgXrows));
+    px.V = shape.V;
+    if (launch_extra_rows(shape.dtype, shape.grad_dtype, px, plan->num_extra_rows, stream) != hipSuccess)
+      return RNNT_ERR_HIP;
+  }
+  if (mark(5) != hipSuccess) return RNNT_ERR_HIP;
+  return RNNT_OK;
+}
+
+rnnt_status_t rnnt_arc_loss(const void* logits, rnnt_shape_t shape, const int32_t* logit_lens,
+                            const int32_t* label_lens, const rnnt_arc_plan_t* plan, const void* plan_image,
+                            float* loss_out, void* grad_out, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream) {
+  return rnnt_arc_loss_timed(logits, shape, logit_lens, label_lens, plan, plan_image, loss_out, grad_out, workspace,
+                             workspace_bytes, stream, nullptr);
+}
+
 rnnt_status_t rnnt_log_softmax_gather(const void* logits, rnnt_shape_t shape, const int32_t* labels,
                                       const int32_t* logit_lens, const int32_t* label_lens,
                                       int32_t blank, double* lse_out, double* lp_blank_out,
@@ -549,7 +804,7 @@ rnnt_status_t rnnt_log_softmax_gather(const void* logits, rnnt_shape_t shape, co
   p1.lse_out = lse_out;
   p1.lp_blank_out = lp_blank_out;
   p1.lp_label_out = lp_label_out;
-  return launch_k1_dtype<false>(shape.dtype, p1, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
+  return launch_k1_dtype<kK1Dense>(shape.dtype, p1, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
 }
 
 rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label, rnnt_shape_t shape,

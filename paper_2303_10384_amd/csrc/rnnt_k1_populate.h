@@ -7,15 +7,18 @@
 //   lp_blank(t, u) = z[blank] - lse,  lp_label(t, u) = z[y_{u+1}] - lse.
 // Padding rows are never touched.
 //
-// Two output forms:
-//  * LATTICE (the fused loss): arc weights in log2 units, stored as
+// Three output forms (OUT):
+//  * kK1Lattice (the fused loss): arc weights in log2 units, stored as
 //    {lp_blank, lp_label} pairs by anti-diagonal (cell (t, u) of utterance b at
 //    (b*(T_max+U_max) + t+u)*(U_max+1) + u), where the lattice kernel reads a
 //    diagonal as one contiguous run; absent arcs (the label arc of the top row,
 //    the blank arcs of the last frame below the top row) carry kNoArc; plus
 //    lse * log2(e) as float32 at the same index.
-//  * dense natural-log lse / lp_blank / lp_label, (B, T_max, U_max+1) float64
-//    (the populate step on its own).
+//  * kK1Dense: natural-log lse / lp_blank / lp_label, (B, T_max, U_max+1)
+//    float64 (the populate step on its own);
+//  * kK1Rows: lse * log2(e) per row, (B, T_max, U_max+1) float64, and no
+//    labels read (the loss over arc-list lattices, whose arcs select their own
+//    labels).
 //
 // Mapping: a block owns up to `rows_per_block` consecutive units u of one
 // anti-diagonal d of one utterance; blocks are numbered so that consecutive
@@ -54,6 +57,10 @@ namespace rnnt {
 
 constexpr bool kK1StreamLoads = RNNT_K1_NT_LOAD != 0;
 
+constexpr int kK1Dense = 0;
+constexpr int kK1Lattice = 1;
+constexpr int kK1Rows = 2;
+
 struct PopulateParams {
   const void* logits;
   int32_t B, T_max, U_max, V, blank;
@@ -70,6 +77,8 @@ struct PopulateParams {
   double* lse_out;         // (B, T_max, U_max+1) or null
   double* lp_blank_out;
   double* lp_label_out;
+  // rows form
+  double* lse2_rows;       // (B, T_max, U_max+1): lse * log2(e)
 };
 
 // (max, sum of exp) of one batch of register-held values, merged into the
@@ -253,7 +262,7 @@ constexpr int kXcds = 8;
 constexpr int kXcdRun = RNNT_K1_XCD_RUN;  // consecutive blocks per XCD turn
 
 
-template <typename T, int G, int NB, bool LATTICE, bool FAST>
+template <typename T, int G, int NB, int OUT, bool FAST>
 __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
   constexpr int GROUPS = 256 / G;  // rows in flight per block
@@ -291,7 +300,7 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   // the block's labels go through LDS, so no label load waits inside the row loop
   for (int i = threadIdx.x; i < n_rows; i += blockDim.x) {
     const int u = u_lo + i;
-    s_label[i] = (u < Ub) ? p.labels[static_cast<int64_t>(b) * p.U_max + u] : kNoLabel;
+    s_label[i] = (OUT != kK1Rows && u < Ub) ? p.labels[static_cast<int64_t>(b) * p.U_max + u] : kNoLabel;
   }
   __syncthreads();
 
@@ -388,7 +397,7 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
     const double lse = static_cast<double>(s_max[j]) + log(s_sum[j]);
     const double lpb = static_cast<double>(s_zb[j]) - lse;
     const double lpl = (u < Ub) ? (y_ok ? static_cast<double>(s_zy[j]) - lse : __builtin_nan("")) : -__builtin_inf();
-    if (LATTICE) {
+    if (OUT == kK1Lattice) {
       const int64_t sc = static_cast<int64_t>(diag) * U1 + u;
       const bool blank_arc = (t < Tb - 1) || (u == Ub);  // absent: last frame below the top row
       double2 w;
@@ -396,6 +405,8 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
       w.y = (u < Ub) ? clamp_no_arc(lpl * kLog2eD) : kNoArc;
       p.lp2[sc] = w;
       p.lse2[sc] = static_cast<float>(lse * kLog2eD);
+    } else if (OUT == kK1Rows) {
+      p.lse2_rows[row_lo - static_cast<int64_t>(j) * p.U_max] = lse * kLog2eD;
     } else {
       const int64_t row = row_lo - static_cast<int64_t>(j) * p.U_max;
       if (p.lse_out) p.lse_out[row] = lse;

@@ -138,8 +138,7 @@ def small_case(B, T_max, U_max, V, seed, sigma=1.5, dtype="f32", full=False, bla
     return logits, tl, ul, labels
 
 
-ARC_DTYPE = np.dtype([("src", "<i4"), ("dst", "<i4"), ("t", "<i4"), ("u", "<i4"), ("label", "<i4"),
-                      ("score", "<f4")])
+from .topologies import ARC_DTYPE  # noqa: E402  (the record layout of an arc)
 
 
 def random_arc_lattice(rng, T_b, U_b, V, n_states, n_arcs, eps_frac=0.2, score_sigma=0.5, long_frac=0.1):

@@ -1,0 +1,262 @@
+"""The arc-list planner (rnnt_arc_plan, host code in the library), CPU only.
+
+The plan image is replayed here the way the device kernels read it: the
+level records in order; per level, each entering arc's source score read from
+the LDS slot the plan names (a ring of recent states that later states
+overwrite, plus pinned slots); each state's run of entering arcs; the
+reversed lattice through the mirror numbering and the arc permutation; the
+label arcs grouped by logits row.  Unwritten LDS slots hold NaN, so a slot read
+before it is written, or after the ring has overwritten it, shows up.  The
+losses and gradients of the replay must match the arc-list oracle.
+"""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+from scipy.special import log_softmax, logsumexp
+
+from oracle import arc_lattice as AL
+from paper_2303_10384_amd import topologies as TP
+from paper_2303_10384_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+LAYOUT = open(os.path.join(ROOT, "paper_2303_10384_amd", "csrc", "rnnt_arc_layout.h")).read()
+
+
+def const(name):
+    return int(re.search(r"constexpr int %s = (\w+)" % name, LAYOUT).group(1))
+
+
+RING, PINS, LEVEL_ARCS = const("kArcRing"), const("kArcPins"), const("kArcLevelArcs")
+DUMMY = RING + PINS
+
+
+@pytest.fixture(scope="module")
+def binding():
+    from paper_2303_10384_amd import binding as BD
+    if not os.path.exists(BD.LIB_PATH):
+        from paper_2303_10384_amd import build
+        build.build(verbose=False)
+    BD.load_library()
+    return BD
+
+
+def unpack(plan):
+    d, img = plan.desc, plan.image.numpy()
+    B, S, L, A, N, X = d.B, d.num_states, d.num_levels, d.num_arcs, d.num_row_arcs, d.num_extra_rows
+    R = B * d.T_max * (d.U_max + 1)
+
+    def arr(i, dtype, n, width=1):
+        return np.frombuffer(img, dtype=dtype, count=n * width, offset=d.off[i]).reshape((n, width) if width > 1
+                                                                                       else (n,))
+    return dict(
+        utt=arr(0, np.int32, B, 4), ends=arr(1, np.int32, B, 4), level=[arr(2, np.int32, L, 4), arr(3, np.int32, L, 4)],
+        seg=[arr(4, np.int32, S), arr(5, np.int32, S)], pin=[arr(6, np.int32, S), arr(7, np.int32, S)],
+        arcs=arr(8, np.int32, A, 4), score=arr(9, np.float32, A), loc=[arr(10, np.int32, A), arr(11, np.int32, A)],
+        perm=arr(12, np.int32, A), row_seg=arr(13, np.int32, R + 1), row_arc=arr(14, np.int32, N),
+        xrows=arr(15, np.int32, X))
+
+
+def replay_sweep(P, g, b, w):
+    """Scores of every state of utterance b in graph g, read as the sweep reads them."""
+    s_begin, s_end, l_begin, l_end = (int(x) for x in P["utt"][b])
+    fin0, start1, a_begin, a_end = (int(x) for x in P["ends"][b])
+    start = start1 if g else s_begin
+    lds = np.full(DUMMY + 1, np.nan)
+    val = np.full(s_end - s_begin, np.nan)
+    for k in range(l_begin, l_end):
+        s_lo, ns, a_lo, packed = (int(x) for x in P["level"][g][k])
+        na, maxdeg = packed & 0xFFFF, packed >> 16
+        assert na <= LEVEL_ARCS and ns <= RING
+        x = np.array([lds[P["loc"][g][a_lo + i]] + w[a_lo + i] for i in range(na)])
+        seen_deg = 0
+        for s in range(s_lo, s_lo + ns):
+            seg = int(P["seg"][g][s])
+            rel, cnt = seg & 0xFFFF, seg >> 16
+            seen_deg = max(seen_deg, cnt)
+            assert rel + cnt <= na
+            terms = x[rel:rel + cnt]
+            assert not np.isnan(terms).any(), "a source score read from an unwritten or overwritten slot"
+            v = logsumexp(terms) if cnt else -math.inf
+            v = 0.0 if s == start else v
+            lds[(s - s_begin) & (RING - 1)] = v
+            lds[P["pin"][g][s]] = v
+            val[s - s_begin] = v
+        assert seen_deg == maxdeg
+    assert not np.isnan(val).any()
+    return val
+
+
+def replay(plan, logits, logit_lens, label_lens, blank):
+    """Losses and gradient of the batch from the plan image (float64)."""
+    P = unpack(plan)
+    d = plan.desc
+    B, T_max, U1, V = logits.shape
+    logp = log_softmax(logits.astype(np.float64), axis=-1).reshape(-1, V)
+    A = d.num_arcs
+    w0 = np.empty(A)
+    bad = np.zeros(B, bool)
+    for q in range(A):
+        src, dst, row, label = (int(x) for x in P["arcs"][q])
+        w0[q] = float(P["score"][q])
+        if label >= 0:
+            b, rem = divmod(row, T_max * U1)
+            t, u = divmod(rem, U1)
+            if t >= logit_lens[b] or u > label_lens[b]:
+                bad[b] = True
+            w0[q] += logp[row, label]
+    w1 = np.empty(A)
+    w1[P["perm"]] = w0
+    assert sorted(P["perm"]) == list(range(A))
+    loss = np.full(B, np.nan)
+    grad = np.zeros(logits.shape).reshape(-1, V)
+    for b in range(B):
+        if bad[b]:
+            continue
+        alpha = replay_sweep(P, 0, b, w0)
+        beta = replay_sweep(P, 1, b, w1)
+        s_begin, s_end = int(P["utt"][b][0]), int(P["utt"][b][1])
+        fin = int(P["ends"][b][0]) - s_begin
+        lnP = alpha[fin]
+        assert lnP == beta[-1] == -math.inf or abs(beta[-1] - lnP) <= 1e-9 * max(1.0, abs(lnP))
+        loss[b] = -lnP
+        if lnP == -math.inf:
+            continue
+        rows = range(b * T_max * U1, (b + 1) * T_max * U1)
+        for r in rows:
+            j0, j1 = int(P["row_seg"][r]), int(P["row_seg"][r + 1])
+            if j0 == j1:
+                continue
+            occ, labels = [], []
+            for j in range(j0, j1):
+                q = int(P["row_arc"][j])
+                src, dst, row, label = (int(x) for x in P["arcs"][q])
+                assert row == r and label >= 0
+                e = alpha[src - s_begin] + w0[q] + beta[s_end - 1 - dst] - lnP
+                occ.append(math.exp(e) if e > -math.inf else 0.0)
+                labels.append(label)
+            non_blank = [l for l in labels if l != blank]
+            assert labels == sorted(labels, key=lambda l: (l != blank, l))  # blank first, then by label
+            assert (len(set(non_blank)) >= 2) == (r in set(P["xrows"].tolist()))
+            p = np.exp(logp[r])
+            grad[r] += p * sum(occ)
+            for o, l in zip(occ, labels):
+                grad[r, l] -= o
+    return loss, grad.reshape(logits.shape)
+
+
+def as_tuples(arcs):
+    return [(int(a["src"]), int(a["dst"]), int(a["t"]), int(a["u"]), int(a["label"]), float(a["score"])) for a in arcs]
+
+
+def check_against_oracle(binding, lattices, logits, tl, ul, blank):
+    B, T_max, U1, V = logits.shape
+    plan = binding.arc_plan(lattices, T_max, U1 - 1, V, blank)
+    loss, grad = replay(plan, logits, tl, ul, blank)
+    ref_loss, ref_grad = AL.batch_loss_grad(logits, tl, ul, [(n, as_tuples(a)) for n, a in lattices])
+    np.testing.assert_allclose(loss, ref_loss, rtol=1e-10, atol=0)
+    np.testing.assert_allclose(grad, ref_grad, rtol=0, atol=1e-11)
+    return plan
+
+
+@pytest.mark.parametrize("variant", TP.VARIANTS)
+def test_grid_lattices_replay(binding, variant):
+    logits, tl, ul, labels = W.small_case(3, 7, 4, 6, seed=3, blank=1)
+    lattices = TP.batch_grid_lattices(tl, ul, labels, 1, variant)
+    check_against_oracle(binding, lattices, logits, tl, ul, 1)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_lattices_replay(binding, seed):
+    rng = np.random.default_rng(seed)
+    B, T_max, U_max, V = 3, 5, 3, 7
+    logits = rng.standard_normal((B, T_max, U_max + 1, V)) * 2
+    tl = np.array([5, 3, 4])
+    ul = np.array([3, 2, 3])
+    lattices = [W.random_arc_lattice(rng, tl[b], ul[b], V, 6 + 5 * b, 20 + 12 * b, long_frac=0.3) for b in range(B)]
+    check_against_oracle(binding, lattices, logits, tl, ul, 0)
+
+
+def test_long_arcs_use_pinned_slots(binding):
+    # more states than the ring holds, with arcs from the start and into the final
+    # state spanning all of them (the W-Transducer's wild-card arcs, scaled up)
+    T, U, V = 100, 90, 5
+    rng = np.random.default_rng(9)
+    logits = rng.standard_normal((1, T, U + 1, V))
+    labels = rng.integers(1, V, size=(1, U))
+    for variant in ("wrnnt", "wrnnt_allow_ignore"):
+        lattices = TP.batch_grid_lattices([T], [U], labels, 0, variant)
+        assert lattices[0][0] > RING
+        plan = check_against_oracle(binding, lattices, logits, np.array([T]), np.array([U]), 0)
+        assert 0 < plan.max_pins <= PINS
+
+
+def test_rows_with_several_labels(binding):
+    # two label arcs with different labels on the same row: the extra-rows kernel's rows
+    rng = np.random.default_rng(2)
+    logits = rng.standard_normal((2, 3, 2, 5))
+    arcs = np.zeros(6, TP.ARC_DTYPE)
+    for i, a in enumerate([(0, 1, 0, 0, 2, 0.1), (0, 1, 0, 0, 3, -0.2), (0, 1, 0, 0, 0, 0.0), (1, 2, 1, 1, 4, 0.0),
+                           (1, 2, 1, 0, 1, 0.3), (2, 3, 2, 1, -1, 0.0)]):
+        arcs[i] = a
+    lattices = [(4, arcs), (4, arcs)]
+    plan = check_against_oracle(binding, lattices, logits, np.array([3, 3]), np.array([1, 1]), 0)
+    assert plan.num_extra_rows == 2
+
+
+def test_degenerate_lattices(binding):
+    logits = np.random.default_rng(1).standard_normal((3, 2, 2, 4))
+    one = (1, np.zeros(0, TP.ARC_DTYPE))                     # start is final: loss 0
+    cut = np.zeros(2, TP.ARC_DTYPE)                          # the final state unreachable: loss inf
+    cut[0] = (0, 1, 0, 0, 1, 0.0)
+    cut[1] = (2, 3, 1, 1, 2, 0.0)
+    outside = np.zeros(1, TP.ARC_DTYPE)                      # reads row t = 1 of a one-frame utterance
+    outside[0] = (0, 1, 1, 0, 1, 0.0)
+    check_against_oracle(binding, [one, (4, cut), (2, outside)], logits, np.array([2, 2, 1]), np.array([1, 1, 1]), 0)
+
+
+def test_planner_rejects_bad_lists(binding):
+    def plan_status(n, arcs, T=3, U=2, V=5, blank=0):
+        a = np.zeros(len(arcs), TP.ARC_DTYPE)
+        for i, x in enumerate(arcs):
+            a[i] = x
+        try:
+            binding.arc_plan([(n, a)], T, U, V, blank)
+            return 0
+        except binding.RNNTError as e:
+            return e.status
+    assert plan_status(3, [(0, 1, 0, 0, 1, 0.0), (1, 2, 0, 0, 1, 0.0)]) == 0
+    assert plan_status(3, [(1, 1, 0, 0, 1, 0.0)]) == 10     # not increasing
+    assert plan_status(3, [(2, 1, 0, 0, 1, 0.0)]) == 10
+    assert plan_status(3, [(0, 3, 0, 0, 1, 0.0)]) == 10     # state out of range
+    assert plan_status(3, [(0, 1, 0, 0, 5, 0.0)]) == 10     # label >= V
+    assert plan_status(3, [(0, 1, 0, 0, -2, 0.0)]) == 10
+    assert plan_status(3, [(0, 1, 3, 0, 1, 0.0)]) == 10     # t >= T_max
+    assert plan_status(3, [(0, 1, 0, 3, 1, 0.0)]) == 10     # u > U_max
+    assert plan_status(3, [(0, 1, 9, 9, -1, 0.0)]) == 0     # an arc without a label reads no row
+    assert plan_status(0, []) == 10
+    assert plan_status(3, [(0, 1, 0, 0, 1, 0.0)], blank=5) == 3
+    # a level with more entering arcs than the sweep holds
+    wide = [(0, 1, 0, 0, 1, 0.0)] * (LEVEL_ARCS + 1)
+    assert plan_status(2, wide) == 9
+
+
+def test_plan_descriptor_and_bound(binding):
+    lib = binding.load_library()
+    lattices = TP.batch_grid_lattices([4, 2], [2, 1], [[1, 2], [3, 0]], 0, "wrnnt")
+    plan = binding.arc_plan(lattices, 4, 2, 5, 0)
+    d = plan.desc
+    assert d.num_states == sum(n for n, _ in lattices) and d.num_arcs == sum(len(a) for _, a in lattices)
+    assert d.image_bytes <= lib.rnnt_arc_plan_bytes_bound(2, 4, 2, d.num_states, d.num_arcs)
+    assert all(o % 256 == 0 for o in d.off) and list(d.off) == sorted(d.off)
+    # too small an image buffer
+    buf = (ctypes.c_uint8 * 64)()
+    desc = binding.ArcPlanDesc()
+    arcs = np.concatenate([a for _, a in lattices])
+    st = lib.rnnt_arc_plan(2, 4, 2, 5, 0, np.array([n for n, _ in lattices], np.int32).ctypes.data,
+                           np.array([0, len(lattices[0][1]), len(arcs)], np.int64).ctypes.data, arcs.ctypes.data,
+                           ctypes.cast(buf, ctypes.c_void_p), 64, ctypes.byref(desc))
+    assert st == 6

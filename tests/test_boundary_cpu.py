@@ -31,7 +31,8 @@ def test_header_declares_the_documented_entry_points():
     assert names == sorted(["rnnt_loss_workspace_bytes", "rnnt_loss", "rnnt_loss_timed", "rnnt_log_softmax_gather",
                             "rnnt_lattice_workspace_bytes", "rnnt_lattice_scores", "rnnt_status_string",
                             "rnnt_version", "rnnt_viterbi_workspace_bytes", "rnnt_viterbi",
-                            "rnnt_viterbi_timed"])
+                            "rnnt_viterbi_timed", "rnnt_arc_plan_bytes_bound", "rnnt_arc_plan",
+                            "rnnt_arc_loss_workspace_bytes", "rnnt_arc_loss", "rnnt_arc_loss_timed"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -43,7 +44,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 def test_status_strings_and_version(lib):
     from paper_2303_10384_amd import binding
-    for code in range(10):
+    for code in range(11):
         assert binding.status_string(code)
     assert binding.status_string(0) == "ok"
     assert "gfx950" in binding.version()
@@ -182,3 +183,31 @@ def test_binding_refuses_cpu_tensors(lib):
     with pytest.raises(ValueError, match="GPU"):
         rnnt_loss(x, torch.zeros(1, 1, dtype=torch.int32), torch.ones(1, dtype=torch.int32),
                   torch.ones(1, dtype=torch.int32))
+
+
+def test_arc_loss_host_errors(lib):
+    from paper_2303_10384_amd import binding, topologies
+    plan = binding.arc_plan(topologies.batch_grid_lattices([5, 4], [3, 2], [[1, 2, 3], [4, 5, 0]]), 5, 3, 7, 0)
+    d = plan.desc
+    vp = ctypes.c_void_p
+    need = lib.rnnt_arc_loss_workspace_bytes(ctypes.byref(d))
+    assert need > 0 and lib.rnnt_arc_loss_workspace_bytes(None) == 0
+
+    def call(sh, logits=FAKE, tl=FAKE, ul=FAKE, desc=d, image=FAKE, loss=FAKE, grad=FAKE, ws=FAKE, ws_bytes=None):
+        return lib.rnnt_arc_loss(vp(logits), sh, vp(tl), vp(ul), ctypes.byref(desc) if desc is not None else None,
+                                 vp(image), vp(loss), vp(grad), vp(ws), need - 1 if ws_bytes is None else ws_bytes,
+                                 vp(0))
+    sh = shape(2, 5, 3, 7)
+    assert call(sh) == 6                        # everything right but a workspace one byte short
+    assert call(shape(B=0)) == 2
+    assert call(sh, logits=0) == 1
+    assert call(sh, desc=None) == 1
+    assert call(sh, image=0) == 1
+    assert call(sh, loss=0) == 1
+    assert call(shape(2, 5, 3, 8)) == 10        # the plan was made for V = 7
+    assert call(shape(3, 5, 3, 7)) == 10
+    assert call(sh, image=FAKE + 8) == 7
+    assert call(sh, ws=FAKE + 16, ws_bytes=need) == 7
+    bad = binding.ArcPlanDesc.from_buffer_copy(d)
+    bad.off[3] = bad.off[2] - 256               # offsets out of order
+    assert call(sh, desc=bad) == 10
