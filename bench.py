@@ -8,9 +8,11 @@ line: throughput in joint-logit elements/s (padded tensor B*T_max*(U_max+1)*V
 per step), the achieved HBM bandwidth of the dominant kernel against the
 MI355X peak, and the CPU oracle timed on a bounded sample.  With --mode viterbi
 a step is one forced alignment of the batch (populate kernel, alignment kernel)
-and the line reports that path the same way.
+and the line reports that path the same way.  With --mode arc a step is one
+rnnt_arc_loss call with a gradient, the workload's lattices given as arc lists
+(planned once on the host before timing, like the labels).
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload bpe] [--mode loss|viterbi]
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload bpe] [--mode loss|viterbi|arc]
 """
 import argparse
 import ctypes
@@ -58,17 +60,16 @@ class HipEvents:
             self.hip.hipEventDestroy(ctypes.c_void_p(h))
 
 
-def profiled_traffic(workload, kernel="k3_grad"):
+def profiled_traffic(workload, kernel="k3_grad", path_kind="loss"):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter record
-    of the fused loss, if it was taken on the kernel sources as they are now; else
-    None."""
-    from paper_2303_10384_amd.profiling import KERNEL_SOURCES, source_digest
+    of the path, if it was taken on the kernel sources as they are now; else None."""
+    from paper_2303_10384_amd.profiling import SOURCES, source_digest
     path = os.path.join(PROFILE_DIR, "k3_grad_%s_traffic.json" % workload)
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("source_digest") != source_digest(KERNEL_SOURCES):
+    if rec.get("source_digest") != source_digest(SOURCES[path_kind]):
         return None
     if kernel == "k3_grad":
         return rec.get("hbm_bytes_per_launch")
@@ -100,12 +101,19 @@ def algorithmic_bytes(w, tl, ul, s_in, s_out):
 def cpu_oracle_worker(args):
     import numpy as np
 
-    from oracle import rnnt_ref, viterbi
+    from oracle import arc_lattice, rnnt_ref, viterbi
+    from paper_2303_10384_amd import topologies
     T_b, U_b, V, sigma, seed, labels, variant, mode = args
     z = np.random.default_rng(seed).standard_normal((T_b, U_b + 1, V), dtype=np.float32) * np.float32(sigma)
+    if mode == "arc":
+        n, arcs = topologies.grid_lattice(T_b, U_b, labels, 0, variant)
+        arcs = [(int(a["src"]), int(a["dst"]), int(a["t"]), int(a["u"]), int(a["label"]), float(a["score"]))
+                for a in arcs]
     t0 = time.perf_counter()
     if mode == "viterbi":
         viterbi.utterance_alignment(z.astype(np.float64), labels, 0, variant)
+    elif mode == "arc":
+        arc_lattice.arc_lattice_loss_grad(z.astype(np.float64), arcs, n)
     else:
         rnnt_ref.utterance_loss_grad(z.astype(np.float64), labels, 0, variant, need_grad=True)
     return time.perf_counter() - t0
@@ -143,7 +151,9 @@ def cpu_baseline(w, tl, ul, labels, budget_s, mode="loss"):
         "sample": "%d utterance evaluations cycling through the %d utterances of the batch (their lengths and "
                   "labels, N(0,%g) logits), float64 %s, %d worker processes, %.1f s; elements counted as padded "
                   "rows x V like the GPU value" % (n, w.B, w.sigma,
-                                                   "forced alignment" if mode == "viterbi" else "loss + gradient",
+                                                   {"viterbi": "forced alignment",
+                                                    "arc": "arc-list loss + gradient (oracle/arc_lattice.py)"}.get(
+                                                       mode, "loss + gradient"),
                                                    min(cores, n), dt),
     }
 
@@ -238,6 +248,92 @@ def viterbi_bench(args, w, tl, ul, logits, labels_d, tl_d, ul_d, cpu):
     print(json.dumps(result), flush=True)
 
 
+def arc_bench(args, w, tl, ul, labels, logits, tl_d, ul_d, cpu):
+    """The loss over the workload's lattices given as arc lists: kernel 1 (rows form),
+    arc populate, the two level sweeps, row records, kernel 3 (+ rows with several
+    labels) per step, timed with HIP events on the launch stream."""
+    import numpy as np
+    import torch
+
+    from paper_2303_10384_amd import binding, topologies
+    dev = logits.device
+    t0 = time.perf_counter()
+    lattices = topologies.batch_grid_lattices(tl, ul, labels, 0, w.variant)
+    plan = binding.arc_plan(lattices, w.T_max, w.U_max, w.V, 0, device=dev)
+    plan_s = time.perf_counter() - t0
+    log("[bench] arc lists: %d states, %d arcs, %d levels; planned in %.2f s (host)"
+        % (plan.num_states, plan.num_arcs, plan.num_levels, plan_s))
+    grad = torch.empty_like(logits)
+    loss = torch.empty(w.B, dtype=torch.float32, device=dev)
+    ws = torch.empty(binding.arc_loss_workspace_bytes(plan), dtype=torch.uint8, device=dev)
+    call = lambda ev=None: binding.arc_loss(logits, tl_d, ul_d, plan, True, ws, grad, loss, ev)  # noqa: E731
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    log("[bench] warmup done")
+    ev = HipEvents()
+    events = [ev.create(6) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        call(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    k_ms = [[ev.elapsed_ms(e[i], e[i + 1]) for i in range(5)] for e in events]
+    total_ms = ev.elapsed_ms(events[0][0], events[-1][5])
+    for e in events:
+        ev.destroy(e)
+    ms_per_step = total_ms / args.steps
+    k1_ms, kp_ms, ks_ms, kr_ms, k3_ms = (float(np.mean([r[i] for r in k_ms])) for i in range(5))
+    log("[bench] per step %.4f ms (wall %.4f ms): k1 %.4f  populate %.4f  sweep %.4f  rows %.4f  k3 %.4f ms"
+        % (ms_per_step, wall * 1e3 / args.steps, k1_ms, kp_ms, ks_ms, kr_ms, k3_ms))
+    ab = algorithmic_bytes(w, tl, ul, logits.element_size(), grad.element_size())
+    elems = ab["padded_rows"] * w.V
+    k3_gbs = ab["k3_grad"] / (k3_ms * 1e-3) / 1e9
+    result = {
+        "metric": "arc-list lattice loss+grad joint-logit elements/sec and achieved HBM GB/s vs peak",
+        "value": elems / (ms_per_step * 1e-3),
+        "unit": "joint-logit elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": w.describe() + " as arc lists",
+            "B": w.B, "T_max": w.T_max, "U_max": w.U_max, "V": w.V, "variant": w.variant,
+            "valid_rows": ab["valid_rows"], "padded_rows": ab["padded_rows"],
+            "states": plan.num_states, "arcs": plan.num_arcs, "levels": plan.num_levels,
+            "plan": "built once on the host before timing (%.2f s), image %d bytes on the device"
+                    % (plan_s, plan.image_bytes),
+            "lattice_scores": "f64", "softmax": "f32",
+        },
+        "hbm_gbs_step": round(ab["step"] / (ms_per_step * 1e-3) / 1e9, 1),
+        "hbm_frac_step": round(ab["step"] / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "kernel_ms": {"k1_populate": round(k1_ms, 5), "arc_populate": round(kp_ms, 5), "arc_sweep": round(ks_ms, 5),
+                      "arc_rows": round(kr_ms, 5), "k3_grad": round(k3_ms, 5)},
+        "kernel_gbs": {"k1_populate": round(ab["k1_populate"] / (k1_ms * 1e-3) / 1e9, 1), "k3_grad": round(k3_gbs, 1)},
+        "algorithmic_bytes": {"k1_populate": ab["k1_populate"], "k3_grad": ab["k3_grad"], "step": ab["step"]},
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k3_grad (fused gradient)",
+            "achieved": round(k3_gbs, 1),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(k3_gbs / PEAK_HBM_GBS, 4),
+            "traffic": profiled_traffic(args.workload + "_arc", "k3_grad", "arc"),
+            "bytes_per_launch": ab["k3_grad"],
+            "launch_ms": round(k3_ms, 5),
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -246,8 +342,9 @@ def main():
     ap.add_argument("--workload", default="bpe", choices=["tiny", "char", "bpe", "wrnnt", "large"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=30.0, help="seconds of oracle work to time")
-    ap.add_argument("--mode", default="loss", choices=["loss", "viterbi"],
-                    help="loss: the fused loss + gradient (the headline metric); viterbi: forced alignment")
+    ap.add_argument("--mode", default="loss", choices=["loss", "viterbi", "arc"],
+                    help="loss: the fused loss + gradient (the headline metric); viterbi: forced alignment; "
+                         "arc: the loss + gradient over the workload's lattices given as arc lists")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run --steps device-to-device copies of the workload's gradient size (the "
                          "known-size copy that calibrates the HBM byte counters), then exit")
@@ -285,6 +382,9 @@ def main():
     ul_d = torch.from_numpy(ul).to(dev)
     if args.mode == "viterbi":
         viterbi_bench(args, w, tl, ul, logits, labels_d, tl_d, ul_d, cpu)
+        return
+    if args.mode == "arc":
+        arc_bench(args, w, tl, ul, labels, logits, tl_d, ul_d, cpu)
         return
     grad = torch.empty_like(logits)
     loss = torch.empty(w.B, dtype=torch.float32, device=dev)

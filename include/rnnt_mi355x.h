@@ -260,7 +260,7 @@ typedef struct {
   int32_t t, u;     /* logits row read by the arc: 0 <= t < T_max, 0 <= u <= U_max  */
                     /* (ignored when label == -1)                                  */
   int32_t label;    /* vocabulary index in [0, V), or -1                            */
-  float score;      /* natural-log weight added to the arc                          */
+  float score;      /* natural-log weight added to the arc (finite)                 */
 } rnnt_arc_t;
 
 /* Descriptor of a plan (host memory, filled by rnnt_arc_plan).  The sizes are
@@ -268,10 +268,13 @@ typedef struct {
 typedef struct {
   int32_t B, T_max, U_max, V, blank;
   int32_t num_states, num_levels, num_arcs, num_row_arcs, num_extra_rows;
+  int32_t num_slots[2];             /* arc slots of the forward / backward sweep
+                                       (the arcs plus padding)                   */
   int32_t max_level_states, max_level_arcs, max_in_degree, max_pins;
-  int32_t state_chunks, arc_chunks; /* per-level register chunks of the sweep */
+  int32_t state_chunks;             /* per-level register chunks of 64 states   */
+  int32_t slots_per_state;          /* arc slots per state held in registers    */
   int64_t image_bytes;              /* bytes of the image to copy to the device */
-  int64_t off[16];                  /* byte offsets of the image's arrays       */
+  int64_t off[17];                  /* byte offsets of the image's arrays       */
 } rnnt_arc_plan_t;
 
 /* Upper bound of the image bytes rnnt_arc_plan writes for a batch with these

@@ -34,10 +34,11 @@ class Shape(ctypes.Structure):
 
 class ArcPlanDesc(ctypes.Structure):
     """rnnt_arc_plan_t."""
-    _fields_ = [(n, ctypes.c_int32) for n in (
+    _fields_ = ([(n, ctypes.c_int32) for n in (
         "B", "T_max", "U_max", "V", "blank", "num_states", "num_levels", "num_arcs", "num_row_arcs",
-        "num_extra_rows", "max_level_states", "max_level_arcs", "max_in_degree", "max_pins", "state_chunks",
-        "arc_chunks")] + [("image_bytes", ctypes.c_int64), ("off", ctypes.c_int64 * 16)]
+        "num_extra_rows")] + [("num_slots", ctypes.c_int32 * 2)] + [(n, ctypes.c_int32) for n in (
+            "max_level_states", "max_level_arcs", "max_in_degree", "max_pins", "state_chunks",
+            "slots_per_state")] + [("image_bytes", ctypes.c_int64), ("off", ctypes.c_int64 * 17)])
 
 
 class RNNTError(RuntimeError):

@@ -308,26 +308,28 @@ rnnt_status_t take_workspace(void* workspace, size_t workspace_bytes, size_t nee
 // Workspace of rnnt_arc_loss, 256-byte aligned pieces (R logits rows, A arcs,
 // S states of the plan):
 //   lse2     R double   lse * log2(e) per row
-//   w0, w1   A double   arc weights in the two sweep orders
+//   rec0/1   A0, A1 x 12 bytes  slot records (weight, source LDS slot) of the two sweeps
 //   val0/1   S double   forward / backward scores
 //   lnp      2*B double
 //   status   B int32
+//   bad      B int32    bad-data flags of the populate kernel
 //   rowinfo  R RowInfo  (with a gradient)
 struct ArcLayout {
-  size_t lse2, w0, w1, val0, val1, lnp, status, rowinfo, total;
+  size_t lse2, w0, w1, val0, val1, lnp, status, bad, rowinfo, total;
 };
 
 ArcLayout make_arc_layout(const rnnt_arc_plan_t& pl) {
   const size_t R = static_cast<size_t>(pl.B) * pl.T_max * (static_cast<size_t>(pl.U_max) + 1);
-  const size_t A = static_cast<size_t>(pl.num_arcs), S = static_cast<size_t>(pl.num_states);
+  const size_t A0 = static_cast<size_t>(pl.num_slots[0]), A1 = static_cast<size_t>(pl.num_slots[1]);
+  const size_t S = static_cast<size_t>(pl.num_states);
   ArcLayout L{};
   size_t o = 0;
   L.lse2 = o;
   o = align256(o + R * sizeof(double));
   L.w0 = o;
-  o = align256(o + A * sizeof(double));
+  o = align256(o + A0 * kSlotWords * sizeof(int32_t));
   L.w1 = o;
-  o = align256(o + A * sizeof(double));
+  o = align256(o + A1 * kSlotWords * sizeof(int32_t));
   L.val0 = o;
   o = align256(o + S * sizeof(double));
   L.val1 = o;
@@ -335,6 +337,8 @@ ArcLayout make_arc_layout(const rnnt_arc_plan_t& pl) {
   L.lnp = o;
   o = align256(o + 2 * static_cast<size_t>(pl.B) * sizeof(double));
   L.status = o;
+  o = align256(o + static_cast<size_t>(pl.B) * sizeof(int32_t));
+  L.bad = o;
   o = align256(o + static_cast<size_t>(pl.B) * sizeof(int32_t));
   L.rowinfo = o;
   o = align256(o + R * sizeof(RowInfo));
@@ -346,7 +350,7 @@ ArcLayout make_arc_layout(const rnnt_arc_plan_t& pl) {
 bool plan_consistent(const rnnt_arc_plan_t& pl, const rnnt_shape_t& s) {
   if (pl.B != s.B || pl.T_max != s.T_max || pl.U_max != s.U_max || pl.V != s.V) return false;
   if (pl.num_states < pl.B || pl.num_arcs < 0 || pl.num_levels < pl.B || pl.num_row_arcs < 0 ||
-      pl.num_extra_rows < 0)
+      pl.num_extra_rows < 0 || pl.num_slots[0] < pl.num_arcs || pl.num_slots[1] < pl.num_arcs)
     return false;
   const int64_t R = static_cast<int64_t>(pl.B) * pl.T_max * (static_cast<int64_t>(pl.U_max) + 1);
   if (R >= 0x7fffffffLL || pl.blank < 0 || pl.blank >= pl.V) return false;
@@ -357,34 +361,35 @@ bool plan_consistent(const rnnt_arc_plan_t& pl, const rnnt_shape_t& s) {
   return true;
 }
 
-template <int NC, int NS>
-hipError_t launch_sweep_ns(const ArcSweepParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL((k_arc_sweep<NC, NS>), dim3(2 * p.B), dim3(64), 0, stream, p);
+template <int NW, int DM>
+hipError_t launch_sweep_t(const ArcSweepParams& p, hipStream_t stream) {
+  hipLaunchKernelGGL((k_arc_sweep<NW, DM>), dim3(2 * p.B), dim3(64 * NW), 0, stream, p);
   return hipGetLastError();
 }
 
-template <int NC>
-hipError_t launch_sweep_nc(int ns, const ArcSweepParams& p, hipStream_t stream) {
-  switch (ns) {
-    case 1: return launch_sweep_ns<NC, 1>(p, stream);
-    case 2: return launch_sweep_ns<NC, 2>(p, stream);
-    case 4: return launch_sweep_ns<NC, 4>(p, stream);
-    default: return launch_sweep_ns<NC, 8>(p, stream);
+template <int NS>
+hipError_t launch_sweep_ns(int dm, const ArcSweepParams& p, hipStream_t stream) {
+  switch (dm) {
+    case 1: return launch_sweep_t<NS, 1>(p, stream);
+    case 2: return launch_sweep_t<NS, 2>(p, stream);
+    default: return launch_sweep_t<NS, 4>(p, stream);
   }
 }
 
-hipError_t launch_sweep(int nc, int ns, const ArcSweepParams& p, hipStream_t stream) {
-  switch (nc) {
-    case 1: return launch_sweep_nc<1>(ns, p, stream);
-    case 2: return launch_sweep_nc<2>(ns, p, stream);
-    case 4: return launch_sweep_nc<4>(ns, p, stream);
-    default: return launch_sweep_nc<8>(ns, p, stream);
+// one wavefront per chunk of 64 states of the plan's typical level, up to DM slots
+// per state held in registers
+hipError_t launch_sweep(int ns, int dm, const ArcSweepParams& p, hipStream_t stream) {
+  switch (ns) {
+    case 1: return launch_sweep_ns<1>(dm, p, stream);
+    case 2: return launch_sweep_ns<2>(dm, p, stream);
+    default: return launch_sweep_ns<4>(dm, p, stream);
   }
 }
 
 hipError_t launch_arc_populate(rnnt_dtype_t dt, const ArcPopulateParams& p, hipStream_t stream) {
-  if (p.n_arcs == 0) return hipSuccess;
-  const dim3 grid((p.n_arcs + 255) / 256);
+  const int n = p.n_slots0 > p.n_slots1 ? p.n_slots0 : p.n_slots1;
+  if (n == 0) return hipSuccess;
+  const dim3 grid((n + 255) / 256);
   switch (dt) {
     case RNNT_DTYPE_F32: hipLaunchKernelGGL((k_arc_populate<float>), grid, dim3(256), 0, stream, p); break;
     case RNNT_DTYPE_BF16: hipLaunchKernelGGL((k_arc_populate<bf16_t>), grid, dim3(256), 0, stream, p); break;
@@ -675,6 +680,7 @@ rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const 
   p1.label_lens = label_lens;
   p1.n_elem = n_rows * shape.V;
   p1.lse2_rows = reinterpret_cast<double*>(ws + L.lse2);
+  p1.clear_flags = reinterpret_cast<int32_t*>(ws + L.bad);
   if (launch_k1_dtype<kK1Rows>(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(1) != hipSuccess) return RNNT_ERR_HIP;
 
@@ -685,16 +691,20 @@ rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const 
   pp.T_max = shape.T_max;
   pp.U_max = shape.U_max;
   pp.V = shape.V;
-  pp.n_arcs = plan->num_arcs;
+  pp.n_slots0 = plan->num_slots[0];
+  pp.n_slots1 = plan->num_slots[1];
   pp.n_rows = static_cast<int32_t>(n_rows);
   pp.logit_lens = logit_lens;
   pp.label_lens = label_lens;
   pp.arcs = reinterpret_cast<const int4*>(arr(kImgArcs));
   pp.score = reinterpret_cast<const float*>(arr(kImgScore));
   pp.perm = reinterpret_cast<const int32_t*>(arr(kImgPerm));
+  pp.loc0 = reinterpret_cast<const int32_t*>(arr(kImgLoc0));
+  pp.loc1 = reinterpret_cast<const int32_t*>(arr(kImgLoc1));
   pp.lse2_rows = p1.lse2_rows;
-  pp.w0 = reinterpret_cast<double*>(ws + L.w0);
-  pp.w1 = reinterpret_cast<double*>(ws + L.w1);
+  pp.bad = p1.clear_flags;
+  pp.rec0 = reinterpret_cast<int32_t*>(ws + L.w0);
+  pp.rec1 = reinterpret_cast<int32_t*>(ws + L.w1);
   if (launch_arc_populate(shape.dtype, pp, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(2) != hipSuccess) return RNNT_ERR_HIP;
 
@@ -707,18 +717,19 @@ rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const 
   ps.label_lens = label_lens;
   ps.utt = reinterpret_cast<const int4*>(arr(kImgUtt));
   ps.ends = reinterpret_cast<const int4*>(arr(kImgEnds));
+  ps.slots = reinterpret_cast<const int4*>(arr(kImgSlots));
   for (int g = 0; g < 2; ++g) {
     ps.level[g] = reinterpret_cast<const int4*>(arr(g ? kImgLevel1 : kImgLevel0));
     ps.seg[g] = reinterpret_cast<const int32_t*>(arr(g ? kImgSeg1 : kImgSeg0));
     ps.pin[g] = reinterpret_cast<const int32_t*>(arr(g ? kImgPin1 : kImgPin0));
-    ps.loc[g] = reinterpret_cast<const int32_t*>(arr(g ? kImgLoc1 : kImgLoc0));
-    ps.w[g] = g ? pp.w1 : pp.w0;
+    ps.rec[g] = g ? pp.rec1 : pp.rec0;
     ps.val[g] = reinterpret_cast<double*>(ws + (g ? L.val1 : L.val0));
   }
   ps.lnp2 = reinterpret_cast<double*>(ws + L.lnp);
+  ps.bad = p1.clear_flags;
   ps.status = reinterpret_cast<int32_t*>(ws + L.status);
   ps.loss = loss_out;
-  if (launch_sweep(plan->arc_chunks, plan->state_chunks, ps, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (launch_sweep(plan->state_chunks, plan->slots_per_state, ps, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(3) != hipSuccess) return RNNT_ERR_HIP;
 
   ArcRowParams pr{};
@@ -726,7 +737,7 @@ rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const 
   pr.U_max = shape.U_max;
   pr.blank = plan->blank;
   pr.n_rows = static_cast<int32_t>(n_rows);
-  pr.n_arcs = plan->num_arcs;
+  pr.n_arcs = plan->num_slots[0];
   pr.n_row_arcs = plan->num_row_arcs;
   pr.n_states = plan->num_states;
   pr.logit_lens = logit_lens;
@@ -735,7 +746,7 @@ rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const 
   pr.arcs = pp.arcs;
   pr.row_seg = reinterpret_cast<const int32_t*>(arr(kImgRowSeg));
   pr.row_arc = reinterpret_cast<const int32_t*>(arr(kImgRowArc));
-  pr.w0 = pp.w0;
+  pr.rec0 = pp.rec0;
   pr.val0 = ps.val[0];
   pr.val1 = ps.val[1];
   pr.lnp2 = ps.lnp2;

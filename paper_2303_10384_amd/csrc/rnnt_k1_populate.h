@@ -79,6 +79,7 @@ struct PopulateParams {
   double* lp_label_out;
   // rows form
   double* lse2_rows;       // (B, T_max, U_max+1): lse * log2(e)
+  int32_t* clear_flags;    // (B) set to 0 by block 0 (the arc-list loss's bad-data flags), or null
 };
 
 // (max, sum of exp) of one batch of register-held values, merged into the
@@ -273,6 +274,8 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   __shared__ float s_zb[kMaxRowsPerBlock];
   __shared__ float s_zy[kMaxRowsPerBlock];
 
+  if (OUT == kK1Rows && p.clear_flags && blockIdx.x == 0)
+    for (int i = threadIdx.x; i < p.B; i += blockDim.x) p.clear_flags[i] = 0;
   const int ND = p.T_max + p.U_max;  // anti-diagonals per utterance
   // block order: runs of kXcdRun consecutive (b, d, ublk) are dealt to the XCDs in
   // turn; XCD x holds physical blocks x, x+8, ..., and its k-th block is element

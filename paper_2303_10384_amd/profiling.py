@@ -7,8 +7,9 @@ to HBM per launch: each counter is scaled by the factor that makes the copy's
 reading equal its known size.  The gradient kernel's figure is written, with the
 digest of the sources it was measured on, to profiles/k3_grad_<workload>_traffic.json,
 which bench.py reports as roofline.traffic while the sources are unchanged.
+--path arc reads the kernels of the arc-list loss (bench.py --mode arc).
 
-    python -m paper_2303_10384_amd.profiling --workload bpe \\
+    python -m paper_2303_10384_amd.profiling --workload bpe [--path loss|arc] \\
         --fetch DIR --write DIR --copy-fetch DIR --copy-write DIR [--out profiles]
 """
 import argparse
@@ -21,21 +22,42 @@ import statistics
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
-# the sources whose change invalidates a traffic figure
-KERNEL_SOURCES = [
-    "paper_2303_10384_amd/csrc/rnnt_api.hip",
-    "paper_2303_10384_amd/csrc/rnnt_device.h",
-    "paper_2303_10384_amd/csrc/rnnt_k1_populate.h",
-    "paper_2303_10384_amd/csrc/rnnt_k2_lattice.h",
-    "paper_2303_10384_amd/csrc/rnnt_k3_grad.h",
-]
-
-KERNELS = {  # short name -> substring of the demangled kernel name
-    "k1_populate": "rnnt::k1_populate",
-    "k2_lattice": "rnnt::k2_lattice",
-    "k2b_posteriors": "rnnt::k2b_posteriors",
-    "k3_grad": "rnnt::k3_grad",
+# the sources whose change invalidates a traffic figure, per path
+SOURCES = {
+    "loss": [
+        "paper_2303_10384_amd/csrc/rnnt_api.hip",
+        "paper_2303_10384_amd/csrc/rnnt_device.h",
+        "paper_2303_10384_amd/csrc/rnnt_k1_populate.h",
+        "paper_2303_10384_amd/csrc/rnnt_k2_lattice.h",
+        "paper_2303_10384_amd/csrc/rnnt_k3_grad.h",
+    ],
+    "arc": [
+        "paper_2303_10384_amd/csrc/rnnt_api.hip",
+        "paper_2303_10384_amd/csrc/rnnt_device.h",
+        "paper_2303_10384_amd/csrc/rnnt_k1_populate.h",
+        "paper_2303_10384_amd/csrc/rnnt_k3_grad.h",
+        "paper_2303_10384_amd/csrc/rnnt_arc_layout.h",
+        "paper_2303_10384_amd/csrc/rnnt_arc_kernels.h",
+    ],
 }
+KERNEL_SOURCES = SOURCES["loss"]
+
+KERNEL_SETS = {  # short name -> substring of the demangled kernel name
+    "loss": {
+        "k1_populate": "rnnt::k1_populate",
+        "k2_lattice": "rnnt::k2_lattice",
+        "k2b_posteriors": "rnnt::k2b_posteriors",
+        "k3_grad": "rnnt::k3_grad",
+    },
+    "arc": {
+        "k1_populate": "rnnt::k1_populate",
+        "arc_populate": "rnnt::k_arc_populate",
+        "arc_sweep": "rnnt::k_arc_sweep",
+        "arc_rows": "rnnt::k_arc_rows",
+        "k3_grad": "rnnt::k3_grad",
+    },
+}
+KERNELS = KERNEL_SETS["loss"]
 COPY_KERNEL = "copyBuffer"
 
 
@@ -83,6 +105,7 @@ def copy_scale(rows, copy_bytes, counter):
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--workload", required=True)
+    ap.add_argument("--path", default="loss", choices=sorted(SOURCES))
     ap.add_argument("--fetch", required=True, help="rocprofv3 --pmc FETCH_SIZE output of bench.py")
     ap.add_argument("--write", required=True, help="rocprofv3 --pmc WRITE_SIZE output of bench.py")
     ap.add_argument("--copy-fetch", required=True, help="FETCH_SIZE output of bench.py --copy-probe")
@@ -103,7 +126,7 @@ def main(argv=None):
             line = [ln for ln in f if ln.strip().startswith("{")][-1]
         algo = json.loads(line).get("algorithmic_bytes", {})
     kernels = {}
-    for short, substr in KERNELS.items():
+    for short, substr in KERNEL_SETS[a.path].items():
         fk, nf = per_kernel_kib(fetch, substr)
         wk, nw = per_kernel_kib(write, substr)
         kernels[short] = {
@@ -126,8 +149,9 @@ def main(argv=None):
             "write_kib_raw": w_copy, "write_bytes_per_kib": w_scale, "write_dispatches": w_n,
         },
         "commands": a.commands,
-        "sources": KERNEL_SOURCES,
-        "source_digest": source_digest(KERNEL_SOURCES),
+        "path": a.path,
+        "sources": SOURCES[a.path],
+        "source_digest": source_digest(SOURCES[a.path]),
     }
     os.makedirs(a.out, exist_ok=True)
     path = os.path.join(a.out, "k3_grad_%s_traffic.json" % a.workload)
