@@ -173,14 +173,22 @@ struct bf16_t {
   uint16_t bits;
 };
 
-__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 
-__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
-  const uint32_t u = __float_as_uint(f);
-  const uint32_t rounded = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-  const uint32_t quiet_nan = (u >> 16) | 0x40u;
-  return (f != f) ? quiet_nan : rounded;
+// Two floats rounded to nearest even and packed (the first in the low half):
+// one v_cvt_pk_bf16_f32 on gfx950.
+__device__ __forceinline__ uint32_t pack2_bf16(float a, float b) {
+  const f32x2_t v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
+__device__ __forceinline__ uint32_t pack2_f16(float a, float b) {
+  const f32x2_t v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, f16x2_t));
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
 
 template <>
 struct ElemTraits<bf16_t> {
@@ -196,13 +204,13 @@ struct ElemTraits<bf16_t> {
   __device__ static __forceinline__ uint4 pack(const float* f) {
     uint32_t w[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) w[i] = f32_to_bf16_rne(f[2 * i]) | (f32_to_bf16_rne(f[2 * i + 1]) << 16);
+    for (int i = 0; i < 4; ++i) w[i] = pack2_bf16(f[2 * i], f[2 * i + 1]);
     return make_uint4(w[0], w[1], w[2], w[3]);
   }
   __device__ static __forceinline__ float load1(const bf16_t* p) { return bf16_to_f32(p->bits); }
   __device__ static __forceinline__ float from_bits(uint32_t b) { return bf16_to_f32(b & 0xffffu); }
   __device__ static __forceinline__ void store1(bf16_t* p, float v) {
-    p->bits = static_cast<uint16_t>(f32_to_bf16_rne(v));
+    p->bits = static_cast<uint16_t>(pack2_bf16(v, 0.f) & 0xffffu);
   }
 };
 
@@ -239,7 +247,7 @@ struct ElemTraits<f16_t> {
   __device__ static __forceinline__ uint4 pack(const float* f) {
     uint32_t w[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) w[i] = f32_to_f16(f[2 * i]) | (f32_to_f16(f[2 * i + 1]) << 16);
+    for (int i = 0; i < 4; ++i) w[i] = pack2_f16(f[2 * i], f[2 * i + 1]);
     return make_uint4(w[0], w[1], w[2], w[3]);
   }
   __device__ static __forceinline__ float load1(const f16_t* p) { return f16_to_f32(p->bits); }
