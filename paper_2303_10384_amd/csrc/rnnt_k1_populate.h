@@ -112,19 +112,44 @@ struct RowGeom {
   int y;       // label y_{u+1}, or kNoLabel
 };
 
-template <typename T, int NB>
+// Elements per lane of a row's (at most two) partial boundary chunks, spread
+// over the G lanes of the group.
+template <typename T, int G>
+constexpr int kBndPerLane = (2 * ElemTraits<T>::kPerChunk + G - 1) / G;
+
+template <typename T, int G, int NB>
 struct RowRegs {
-  u32x4 raw[NB];  // interior chunks
-  u32x4 rawb;     // boundary chunk (lanes 0 and 1)
-  float zb, zy;   // z[blank], z[y]
+  u32x4 raw[NB];                 // interior chunks
+  float xb[kBndPerLane<T, G>];   // boundary elements (0 where the slot holds none)
+  float zb, zy;                  // z[blank], z[y]
 };
+
+// Boundary slot e (0 .. 2*EPC-1) of a row: element e % EPC of its first partial
+// chunk (e < EPC) or of its last; the chunk index and the column, and whether
+// the slot holds an element of the row.
+struct BndSlot {
+  int chunk, col;
+  bool ok;
+};
+template <int EPC>
+__device__ __forceinline__ BndSlot bnd_slot(const RowGeom& g, int V, int e) {
+  const bool first_partial = g.mis != 0;
+  const bool last_partial = ((g.mis + V) % EPC) != 0;
+  const int kb0 = first_partial ? 0 : -1;
+  const int kb1 = (last_partial && g.nch - 1 != kb0) ? g.nch - 1 : -1;
+  BndSlot b;
+  b.chunk = (e < EPC) ? kb0 : kb1;
+  b.col = b.chunk * EPC + (e & (EPC - 1)) - g.mis;
+  b.ok = e < 2 * EPC && b.chunk >= 0 && b.col >= 0 && b.col < V;
+  return b;
+}
 
 // Issue every load of one row (all lanes, unconditionally).  Offsets are
 // unsigned: a row that is not live starts at kOutOfRange, and every offset
 // derived from it stays at or above 2^31, past the buffer.
 template <typename T, int G, int NB>
 __device__ __forceinline__ void issue_row(__amdgpu_buffer_rsrc_t rsrc, const RowGeom& g, int V, int blank, int lg,
-                                          RowRegs<T, NB>& R) {
+                                          RowRegs<T, G, NB>& R) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
   constexpr uint32_t S = sizeof(T);
   const bool first_partial = g.mis != 0;
@@ -139,11 +164,13 @@ __device__ __forceinline__ void issue_row(__amdgpu_buffer_rsrc_t rsrc, const Row
     const int k = min(max(kf + q * G + lg, kint_lo), kint_hi);
     R.raw[q] = buffer_load16<kK1StreamLoads>(rsrc, static_cast<int>(rb + static_cast<uint32_t>(k) * 16u));
   }
-  const int kb0 = first_partial ? 0 : -1;
-  const int kb1 = (last_partial && g.nch - 1 != kb0) ? g.nch - 1 : -1;
-  const int kbnd = (lg == 0) ? kb0 : (lg == 1 ? kb1 : -1);
-  const uint32_t ob = kbnd >= 0 ? rb + static_cast<uint32_t>(kbnd) * 16u : static_cast<uint32_t>(kOutOfRange);
-  R.rawb = buffer_load16<kK1StreamLoads>(rsrc, static_cast<int>(ob));
+  // the partial boundary chunks, one element per lane (their lines come in with the interior loads)
+#pragma unroll
+  for (int i = 0; i < kBndPerLane<T, G>; ++i) {
+    const BndSlot b = bnd_slot<ElemTraits<T>::kPerChunk>(g, V, lg + i * G);
+    const uint32_t ob = b.ok ? rb + static_cast<uint32_t>(b.col + g.mis) * S : static_cast<uint32_t>(kOutOfRange);
+    R.xb[i] = buffer_load_elem<T>(rsrc, static_cast<int>(ob));
+  }
   // the same address in every lane of the group: one request, a line the chunk loads bring in
   R.zb = buffer_load_elem<T>(rsrc, static_cast<int>(rb + static_cast<uint32_t>(g.mis + blank) * S));
   const bool y_ok = g.y >= 0 && g.y < V;
@@ -153,7 +180,7 @@ __device__ __forceinline__ void issue_row(__amdgpu_buffer_rsrc_t rsrc, const Row
 
 // (group max, group sum of exp(z - max)) of a row from its registers, in every lane.
 template <typename T, int G, int NB>
-__device__ __forceinline__ void reduce_row(const RowRegs<T, NB>& R, const RowGeom& g, int V, int lg, float& mg,
+__device__ __forceinline__ void reduce_row(const RowRegs<T, G, NB>& R, const RowGeom& g, int V, int lg, float& mg,
                                            double& sg) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
   const float kNegInf = -__builtin_inff();
@@ -162,20 +189,11 @@ __device__ __forceinline__ void reduce_row(const RowRegs<T, NB>& R, const RowGeo
   const int kf = first_partial ? 1 : 0;
   const int kl = g.nch - 1 - (last_partial ? 1 : 0);
   const int n_int = kl - kf + 1;  // may be <= 0 for tiny rows
-  const int kb0 = first_partial ? 0 : -1;
-  const int kb1 = (last_partial && g.nch - 1 != kb0) ? g.nch - 1 : -1;
-  const int kbnd = (lg == 0) ? kb0 : (lg == 1 ? kb1 : -1);
+  constexpr int BPL = kBndPerLane<T, G>;
 
-  float xb[EPC];
-  {
-    float f[EPC];
-    ElemTraits<T>::unpack(make_uint4(R.rawb.x, R.rawb.y, R.rawb.z, R.rawb.w), f);
+  float xb[BPL];
 #pragma unroll
-    for (int j = 0; j < EPC; ++j) {
-      const int v = kbnd * EPC + j - g.mis;
-      xb[j] = (kbnd >= 0 && v >= 0 && v < V) ? f[j] : kNegInf;
-    }
-  }
+  for (int i = 0; i < BPL; ++i) xb[i] = bnd_slot<EPC>(g, V, lg + i * G).ok ? R.xb[i] : kNegInf;
   float x[NB * EPC];
 #pragma unroll
   for (int q = 0; q < NB; ++q) ElemTraits<T>::unpack(make_uint4(R.raw[q].x, R.raw[q].y, R.raw[q].z, R.raw[q].w),
@@ -183,7 +201,7 @@ __device__ __forceinline__ void reduce_row(const RowRegs<T, NB>& R, const RowGeo
   // pass 1: maximum (interior duplicates are harmless; no interior chunks -> skip them)
   float m = kNegInf;
 #pragma unroll
-  for (int j = 0; j < EPC; ++j) m = fmaxf(m, xb[j]);
+  for (int i = 0; i < BPL; ++i) m = fmaxf(m, xb[i]);
   if (n_int > 0) {
 #pragma unroll
     for (int i = 0; i < NB * EPC; ++i) m = fmaxf(m, x[i]);
@@ -193,7 +211,7 @@ __device__ __forceinline__ void reduce_row(const RowRegs<T, NB>& R, const RowGeo
   const float sh = (mg == kNegInf) ? 0.f : mg * kLog2eF;
   float s = 0.f;
 #pragma unroll
-  for (int j = 0; j < EPC; ++j) s += fast_exp2(fmaf(xb[j], kLog2eF, -sh));
+  for (int i = 0; i < BPL; ++i) s += fast_exp2(fmaf(xb[i], kLog2eF, -sh));
   if (n_int > 0) {
 #pragma unroll
     for (int q = 0; q < NB; ++q) {
@@ -337,7 +355,7 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
       g.y = s_label[g.j];
       return g;
     };
-    auto finish = [&](const RowRegs<T, NB>& R, const RowGeom& g) {
+    auto finish = [&](const RowRegs<T, G, NB>& R, const RowGeom& g) {
       float mg;
       double sg;
       reduce_row<T, G, NB>(R, g, p.V, lg, mg, sg);
@@ -350,7 +368,7 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
     };
     // two register sets in turn (a copy between them would wait for the loads in flight)
     RowGeom g0 = geom(0), g1;
-    RowRegs<T, NB> R0, R1;
+    RowRegs<T, G, NB> R0, R1;
     issue_row<T, G, NB>(rsrc, g0, p.V, p.blank, lg, R0);
     for (int it = 0; it < n_iter; it += 2) {
       g1 = geom(it + 1);  // past the block's rows: not live, no memory access
