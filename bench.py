@@ -140,7 +140,7 @@ def cpu_baseline(w, tl, ul, labels, budget_s, mode="loss"):
         log("[bench] cpu oracle: one round of %d utterances took %.1f s; timing %d utterance evaluations"
             % (min(cores, len(jobs)), t_round, len(sample)))
         t0 = time.perf_counter()
-        pool.map(cpu_oracle_worker, sample)
+        per_eval = pool.map(cpu_oracle_worker, sample)  # each evaluation's own time, in its worker
         dt = time.perf_counter() - t0
     n = len(sample)
     return {
@@ -148,6 +148,7 @@ def cpu_baseline(w, tl, ul, labels, budget_s, mode="loss"):
         "unit": "joint-logit elements/s",
         "cores": min(cores, n),
         "kind": "oracle",
+        "single_core_value": n * per_utt_elems / sum(per_eval),
         "sample": "%d utterance evaluations cycling through the %d utterances of the batch (their lengths and "
                   "labels, N(0,%g) logits), float64 %s, %d worker processes, %.1f s; elements counted as padded "
                   "rows x V like the GPU value" % (n, w.B, w.sigma,
@@ -211,6 +212,7 @@ def viterbi_bench(args, w, tl, ul, logits, labels_d, tl_d, ul_d, cpu):
     result = {
         "metric": "forced-alignment joint-logit elements/sec (best path and its frames) and achieved HBM GB/s vs peak",
         "value": elems / (ms_per_step * 1e-3),
+        "valid_elements_per_s": ab["valid_rows"] * w.V / (ms_per_step * 1e-3),
         "unit": "joint-logit elements/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -293,6 +295,7 @@ def arc_bench(args, w, tl, ul, labels, logits, tl_d, ul_d, cpu):
     result = {
         "metric": "arc-list lattice loss+grad joint-logit elements/sec and achieved HBM GB/s vs peak",
         "value": elems / (ms_per_step * 1e-3),
+        "valid_elements_per_s": ab["valid_rows"] * w.V / (ms_per_step * 1e-3),
         "unit": "joint-logit elements/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -435,6 +438,7 @@ def main():
     result = {
         "metric": "joint-logit elements/sec (loss+grad fwd/bwd) and achieved HBM GB/s vs peak",
         "value": elems / (ms_per_step * 1e-3),
+        "valid_elements_per_s": r_valid * V / (ms_per_step * 1e-3),
         "unit": "joint-logit elements/s",
         "n_gpus": 1,
         "steps": args.steps,

@@ -35,6 +35,17 @@ def test_algorithmic_bytes_of_the_bpe_workload():
     assert ab2["k3_grad"] == r_valid * 1025 * 2 + 648000 * 1025 * 4 + 648000 * 16
 
 
+def test_cpu_baseline_reports_pool_and_single_core_rates():
+    w = WORKLOADS["tiny"]
+    tl, ul, labels = make_lengths_labels(w)
+    for mode in ("loss", "viterbi", "arc"):
+        cb = bench.cpu_baseline(w, tl, ul, labels, budget_s=0.2, mode=mode)
+        assert cb["kind"] == "oracle" and cb["unit"] == "joint-logit elements/s"
+        assert cb["value"] > 0 and cb["single_core_value"] > 0 and 1 <= cb["cores"] <= 16
+        # the pool's rate cannot exceed its workers' summed single-core rates
+        assert cb["value"] <= cb["single_core_value"] * cb["cores"] * 1.5
+
+
 def _counter_csv(path, rows):
     os.makedirs(path, exist_ok=True)
     with open(os.path.join(path, "x_counter_collection.csv"), "w", newline="") as f:
