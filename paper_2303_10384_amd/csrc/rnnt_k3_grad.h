@@ -149,6 +149,7 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
   const __amdgpu_buffer_rsrc_t rsrc = make_buffer(static_cast<const uint4*>(p.logits) + tile0, tile_bytes);
   u32x4 raw[Q];
   bool store[Q];
+  bool any_row[Q];  // some lane's chunk q touches a row with a gradient
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
     const int cl = q * kGradThreads + static_cast<int>(threadIdx.x);
@@ -156,6 +157,7 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
     const bool split = v[q] + EPC > p.V;
     const bool zero = ri0[q].label == kZeroRow && (!split || ri1[q].label == kZeroRow);
     store[q] = live;
+    any_row[q] = __builtin_amdgcn_ballot_w64(live && !zero) != 0;
     const int off = (live && !zero) ? cl * 16 : kOutOfRange;
     raw[q] = buffer_load16<kK3StreamLoads>(rsrc, off);
   }
@@ -164,11 +166,16 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
   for (int q = 0; q < Q; ++q) {
     float f[EPC], out[EPC];
     ElemTraits<T>::unpack(make_uint4(raw[q].x, raw[q].y, raw[q].z, raw[q].w), f);
+    if (any_row[q]) {
 #pragma unroll
-    for (int j = 0; j < EPC; ++j) {
-      const int vj = v[q] + j;
-      const bool second = vj >= p.V;
-      out[j] = second ? grad_elem(f[j], vj - p.V, ri1[q], p.blank) : grad_elem(f[j], vj, ri0[q], p.blank);
+      for (int j = 0; j < EPC; ++j) {
+        const int vj = v[q] + j;
+        const bool second = vj >= p.V;
+        out[j] = second ? grad_elem(f[j], vj - p.V, ri1[q], p.blank) : grad_elem(f[j], vj, ri0[q], p.blank);
+      }
+    } else {  // the wave's chunks q all lie in zero rows (padding, bad utterances)
+#pragma unroll
+      for (int j = 0; j < EPC; ++j) out[j] = 0.f;
     }
     if (store[q]) store_chunk<Tout, EPC>(p.grad, (tile0 + q * kGradThreads + static_cast<int>(threadIdx.x)) * EPC, out);
   }
