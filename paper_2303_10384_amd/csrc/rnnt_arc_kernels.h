@@ -328,7 +328,7 @@ __global__ __launch_bounds__(kWave * NW) void k_arc_sweep(ArcSweepParams p) {
     };
     Pre cur = read_pre(k0);
     for (int k = k0; k < k1; ++k) {
-      const Pre nxt = read_pre(k + 1 < k1 ? k + 1 : k);
+      Pre nxt;
       const int4 li = cur.li;
       const int s_lo = li.x;
       const int ns = li.y & (kArcGenericLevel - 1);
@@ -353,6 +353,10 @@ __global__ __launch_bounds__(kWave * NW) void k_arc_sweep(ArcSweepParams p) {
         for (int q = 0; q < DM; ++q)
           src[q] = s_val[cur.loc[q] >= 0 ? min(static_cast<unsigned>(cur.loc[q]), static_cast<unsigned>(kArcDummy))
                                          : kArcDummy];
+        // the sources' reads go out first: LDS answers in order, and the next level's
+        // records are not needed before the barrier
+        __builtin_amdgcn_sched_barrier(0);
+        nxt = read_pre(k + 1 < k1 ? k + 1 : k);
         double v = kNoArc;
 #pragma unroll
         for (int q = 0; q < DM; ++q) {
@@ -361,6 +365,7 @@ __global__ __launch_bounds__(kWave * NW) void k_arc_sweep(ArcSweepParams p) {
         }
         finish(s_lo + j, j < ns, v, cur.pin);
       } else if (padded) {
+        nxt = read_pre(k + 1 < k1 ? k + 1 : k);
         for (int c = wv; c * kWave < ns; c += NW) {
           const int j = c * kWave + lane;
           const bool ok = j < ns;
@@ -369,6 +374,7 @@ __global__ __launch_bounds__(kWave * NW) void k_arc_sweep(ArcSweepParams p) {
           finish(s_lo + j, ok, v, pin_of(j));
         }
       } else {
+        nxt = read_pre(k + 1 < k1 ? k + 1 : k);
         // generic level: one lane per entering arc forms its term, then one lane per state sums its run
         for (int c = wv; c * kWave < nslots; c += NW) {
           const int i = c * kWave + lane;

@@ -166,7 +166,11 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
   for (int q = 0; q < Q; ++q) {
     float f[EPC], out[EPC];
     ElemTraits<T>::unpack(make_uint4(raw[q].x, raw[q].y, raw[q].z, raw[q].w), f);
-    if (any_row[q]) {
+    if (any_row[q] && __builtin_amdgcn_ballot_w64(v[q] + EPC > p.V) == 0) {
+      // no chunk q of the wave reaches past its row's end: one record per lane
+#pragma unroll
+      for (int j = 0; j < EPC; ++j) out[j] = grad_elem(f[j], v[q] + j, ri0[q], p.blank);
+    } else if (any_row[q]) {
 #pragma unroll
       for (int j = 0; j < EPC; ++j) {
         const int vj = v[q] + j;
