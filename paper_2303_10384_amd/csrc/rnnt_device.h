@@ -97,9 +97,10 @@ __device__ __forceinline__ double dpp_f64(double x, double fill) {
   return __hiloint2double(hi, lo);
 }
 
-struct MaxOp {
+struct MaxOp {  // a NaN operand is dropped (callers see NaN through their sums instead)
   template <typename V>
-  __device__ static V apply(V a, V b) { return a > b ? a : b; }
+  __device__ static V apply(V a, V b) { return __builtin_fmax(a, b); }
+  __device__ static float apply(float a, float b) { return __builtin_fmaxf(a, b); }
 };
 struct SumOp {
   template <typename V>
@@ -110,6 +111,20 @@ template <typename V, int CTRL, int ROW_MASK = 0xf>
 __device__ __forceinline__ V dpp_any(V x, V fill) {
   if constexpr (sizeof(V) == 8) return dpp_f64<CTRL, ROW_MASK>(x, fill);
   else return dpp_f32<CTRL, ROW_MASK>(x, fill);
+}
+
+// A permutation inside each row of 16 lanes (every lane reads a lane of its own
+// row): no fill value, so the compiler may fold the move into the operation
+// that uses it.
+template <typename V, int CTRL>
+__device__ __forceinline__ V dpp_perm(V x) {
+  if constexpr (sizeof(V) == 8) {
+    const int lo = __builtin_amdgcn_mov_dpp(__double2loint(x), CTRL, 0xf, 0xf, false);
+    const int hi = __builtin_amdgcn_mov_dpp(__double2hiint(x), CTRL, 0xf, 0xf, false);
+    return __hiloint2double(hi, lo);
+  } else {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
+  }
 }
 
 template <typename V>
@@ -127,10 +142,10 @@ __device__ __forceinline__ V readlane_any(V x, int lane) {
 // the operation's identity.  All 64 lanes must be active.
 template <int G, typename Op, typename V>
 __device__ __forceinline__ V group_reduce(V x, V ident) {
-  if constexpr (G >= 2) x = Op::apply(x, dpp_any<V, dpp::kQuadSwap1>(x, ident));
-  if constexpr (G >= 4) x = Op::apply(x, dpp_any<V, dpp::kQuadSwap2>(x, ident));
-  if constexpr (G >= 8) x = Op::apply(x, dpp_any<V, dpp::kHalfMirror>(x, ident));
-  if constexpr (G >= 16) x = Op::apply(x, dpp_any<V, dpp::kRowMirror>(x, ident));
+  if constexpr (G >= 2) x = Op::apply(x, dpp_perm<V, dpp::kQuadSwap1>(x));
+  if constexpr (G >= 4) x = Op::apply(x, dpp_perm<V, dpp::kQuadSwap2>(x));
+  if constexpr (G >= 8) x = Op::apply(x, dpp_perm<V, dpp::kHalfMirror>(x));
+  if constexpr (G >= 16) x = Op::apply(x, dpp_perm<V, dpp::kRowMirror>(x));
   if constexpr (G >= 32) {
     // rows 1 and 3 add rows 0 and 2: lanes 31 and 63 hold the 32-lane totals
     x = Op::apply(x, dpp_any<V, dpp::kRowBcast15, 0xa>(x, ident));

@@ -221,7 +221,7 @@ __device__ __forceinline__ void reduce_row(const RowRegs<T, G, NB>& R, const Row
       s += (kf + q * G + lg <= kl) ? sq : 0.f;
     }
   }
-  sg = group_reduce<G, SumOp>(static_cast<double>(s), 0.0);
+  sg = static_cast<double>(group_reduce<G, SumOp>(s, 0.f));  // a pairwise tree of the lanes' partial sums
 }
 
 // Row statistics for any row: batches of NB chunks per lane with a running
@@ -267,7 +267,7 @@ __device__ __forceinline__ void row_stats_general(const T* __restrict__ base, in
   }
   mg = group_reduce<G, MaxOp>(mloc, kNegInf);
   const float scale = (mloc == kNegInf) ? 0.f : fast_exp2((mloc - mg) * kLog2eF);
-  sg = group_reduce<G, SumOp>(static_cast<double>(sloc * scale), 0.0);
+  sg = static_cast<double>(group_reduce<G, SumOp>(sloc * scale, 0.f));
 }
 
 // FAST: blocks whose rows lie in whole chunks take the pipelined path (the
