@@ -350,7 +350,7 @@ def full_size_case(torch, pkg, name, loss_utts, grad_utts, grad_dtype=None):
     tl, ul, labels = W.make_lengths_labels(w)
     lg = W.make_logits(w, "cuda:0")
     gdt = grad_dtype or w.dtype
-    # NaN everywhere first: every element must be written (padding rows by the fill blocks)
+    # NaN everywhere first: every element must be written (padding rows as exact zeros)
     grad_out = torch.full(lg.shape, float("nan"), dtype=W.torch_dtype(gdt), device=lg.device)
     loss, grad = pkg.rnnt_loss(lg, to_dev(torch, labels), to_dev(torch, tl), to_dev(torch, ul), variant=w.variant,
                                grad_out=grad_out, grad_dtype=W.torch_dtype(gdt))
