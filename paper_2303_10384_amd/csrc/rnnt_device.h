@@ -1,5 +1,5 @@
-// Device helpers shared by the three kernels of the RNN-T / W-Transducer path
-// (gfx950, wave64).  No host code here.
+// Device helpers shared by the library's kernels (loss, forced alignment,
+// arc-list lattices; gfx950, wave64).  No host code here.
 #pragma once
 
 #include <hip/hip_runtime.h>

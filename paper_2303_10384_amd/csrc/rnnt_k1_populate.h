@@ -29,11 +29,12 @@
 // the row ("interior") are spread NB per lane (G and NB picked from V so that
 // G*NB just covers them) and need no element masks: a lane with no chunk of its
 // own reloads an interior chunk, which cannot raise the maximum, and drops it
-// from the sum with one select.  The at most two chunks that straddle the
-// row's ends go to lanes 0 and 1 with element masks.  Then two passes over the
+// from the sum with one select.  The elements of the at most two chunks that
+// straddle the row's ends are spread over the group, one element per lane
+// (two when G is 8), each with its own mask.  Then two passes over the
 // registers: the group maximum (DPP reduction), then the sum of
-// 2^(z*log2 e - max*log2 e) per lane in float32 and across the group in
-// float64.
+// 2^(z*log2 e - max*log2 e) per lane in float32 and across the group by a
+// pairwise float32 tree.
 //
 // Fast path (every block whose rows lie in whole chunks): the loads of a
 // group's next row are issued before its current row is reduced, as buffer
