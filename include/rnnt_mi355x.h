@@ -326,7 +326,7 @@ rnnt_status_t rnnt_arc_loss(const void* logits, rnnt_shape_t shape, const int32_
 
 /* rnnt_arc_loss, recording events[0..5] (caller-created) on `stream`: before the
  * row normaliser, after it, after the arc populate kernel, after the sweep, after
- * the row records, and after the gradient kernels. */
+ * the arc posteriors and row records, and after the gradient kernels. */
 rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const int32_t* logit_lens,
                                   const int32_t* label_lens, const rnnt_arc_plan_t* plan, const void* plan_image,
                                   float* loss_out, void* grad_out, void* workspace, size_t workspace_bytes,

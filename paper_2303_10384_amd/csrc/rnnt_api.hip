@@ -314,8 +314,9 @@ rnnt_status_t take_workspace(void* workspace, size_t workspace_bytes, size_t nee
 //   status   B int32
 //   bad      B int32    bad-data flags of the populate kernel
 //   rowinfo  R RowInfo  (with a gradient)
+//   occ      A0 x 8 bytes  {posterior, label} per graph-0 slot (with a gradient)
 struct ArcLayout {
-  size_t lse2, w0, w1, val0, val1, lnp, status, bad, rowinfo, total;
+  size_t lse2, w0, w1, val0, val1, lnp, status, bad, rowinfo, occ, total;
 };
 
 ArcLayout make_arc_layout(const rnnt_arc_plan_t& pl) {
@@ -342,6 +343,8 @@ ArcLayout make_arc_layout(const rnnt_arc_plan_t& pl) {
   o = align256(o + static_cast<size_t>(pl.B) * sizeof(int32_t));
   L.rowinfo = o;
   o = align256(o + R * sizeof(RowInfo));
+  L.occ = o;
+  o = align256(o + A0 * sizeof(int2));
   L.total = o;
   return L;
 }
@@ -753,7 +756,12 @@ rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const 
   pr.status = ps.status;
   pr.lse2_rows = p1.lse2_rows;
   pr.rowinfo = reinterpret_cast<RowInfo*>(ws + L.rowinfo);
+  pr.occ = reinterpret_cast<int2*>(ws + L.occ);
   if (grad_out) {
+    if (pr.n_arcs > 0) {
+      hipLaunchKernelGGL(k_arc_occ, dim3(static_cast<uint32_t>((pr.n_arcs + 255) / 256)), dim3(256), 0, stream, pr);
+      if (hipGetLastError() != hipSuccess) return RNNT_ERR_HIP;
+    }
     hipLaunchKernelGGL(k_arc_rows, dim3(static_cast<uint32_t>((n_rows + 255) / 256)), dim3(256), 0, stream, pr);
     if (hipGetLastError() != hipSuccess) return RNNT_ERR_HIP;
   }

@@ -17,7 +17,9 @@
 //              LDS and sums the terms in the log semiring; on a generic level one
 //              lane per entering arc first forms the terms in LDS, then one lane
 //              per state sums its run.
-//   rows       one thread per logits row: the arc posteriors of the row's label
+//   posteriors one thread per arc slot: the posterior of each label arc, in
+//              slot order, with its label.
+//   rows       one thread per logits row: the posteriors of the row's label
 //              arcs, summed into the row record of kernel 3 (blank occupancy,
 //              occupancy of the row's one non-blank label).
 //   extra rows one block per row whose arcs carry two or more distinct
@@ -443,16 +445,37 @@ struct ArcRowParams {
   const double* lnp2;
   const int32_t* status;
   const double* lse2_rows;
+  int2* occ;        // per graph-0 slot: {posterior bits, label}, written by the posterior kernel
   RowInfo* rowinfo;
 };
 
-// Posterior of graph-0 arc i of utterance b (mirror = s_begin + s_end - 1).
-__device__ __forceinline__ float arc_occupancy(const ArcRowParams& p, int i, int mirror, double lnp, int& label) {
+// Posterior of every graph-0 label arc, exp2(alpha(src) + w + beta(dst) - log2 P),
+// computed in slot order: the slot's arc and record are read where consecutive
+// threads read consecutive slots, and the scores of consecutive states mostly lie
+// together too.  The row kernels then read one 8-byte pair per arc.  Padding,
+// wild-card arcs and arcs of utterances without valid scores get {0, kNoLabel}.
+__global__ __launch_bounds__(256) void k_arc_occ(ArcRowParams p) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= p.n_arcs) return;
   const int4 a = p.arcs[i];
-  label = a.w;
-  const double e = p.val0[clamp_index(a.x, p.n_states)] + slot_weight(p.rec0, i) +
-                   p.val1[clamp_index(mirror - a.y, p.n_states)] - lnp;
-  return fast_exp2(static_cast<float>(e));
+  int2 out = make_int2(0, kNoLabel);
+  if (a.x >= 0 && a.w >= 0) {
+    const int b = row_pos(clamp_index(a.z, p.n_rows), p.T_max, p.U_max).b;
+    if (p.status[b] == 0) {
+      const int4 ut = p.utt[b];
+      const double e = p.val0[clamp_index(a.x, p.n_states)] + slot_weight(p.rec0, i) +
+                       p.val1[clamp_index(ut.x + ut.y - 1 - a.y, p.n_states)] - p.lnp2[b];
+      out = make_int2(__float_as_int(fast_exp2(static_cast<float>(e))), a.w);
+    }
+  }
+  p.occ[i] = out;
+}
+
+// Posterior and label of graph-0 arc i (from the posterior kernel).
+__device__ __forceinline__ float arc_occupancy(const ArcRowParams& p, int i, int& label) {
+  const int2 o = p.occ[i];
+  label = o.y;
+  return __int_as_float(o.x);
 }
 
 __global__ __launch_bounds__(256) void k_arc_rows(ArcRowParams p) {
@@ -465,17 +488,13 @@ __global__ __launch_bounds__(256) void k_arc_rows(ArcRowParams p) {
   ri.occ_label = 0.f;
   ri.label = kZeroRow;
   if (p.status[q.b] == 0 && q.t < p.logit_lens[q.b] && q.u <= p.label_lens[q.b]) {
-    const double lnp = p.lnp2[q.b];
-    const int4 ut = p.utt[q.b];
-    const int mirror = ut.x + ut.y - 1;
     const int j0 = p.row_seg[r], j1 = p.row_seg[r + 1];
     float ob = 0.f, ol = 0.f;
     int primary = kNoLabel;
     bool extra = false;
     for (int j = j0; j < j1; ++j) {
       int label;
-      const float occ = arc_occupancy(p, clamp_index(p.row_arc[clamp_index(j, p.n_row_arcs)], p.n_arcs), mirror,
-                                      lnp, label);
+      const float occ = arc_occupancy(p, clamp_index(p.row_arc[clamp_index(j, p.n_row_arcs)], p.n_arcs), label);
       if (label == p.blank) {
         ob += occ;
       } else if (primary == kNoLabel || primary == label) {
@@ -514,15 +533,11 @@ __global__ __launch_bounds__(256) void k_arc_extra_rows(ArcExtraParams p) {
   const int r = clamp_index(p.xrows[blockIdx.x], rp.n_rows);
   const RowPos q = row_pos(r, rp.T_max, rp.U_max);
   if (!(rp.status[q.b] == 0 && q.t < rp.logit_lens[q.b] && q.u <= rp.label_lens[q.b])) return;  // stays zero
-  const double lnp = rp.lnp2[q.b];
-  const int4 ut = rp.utt[q.b];
-  const int mirror = ut.x + ut.y - 1;
   const int j0 = rp.row_seg[r];
   const int n = min(rp.row_seg[r + 1] - j0, kArcRowArcsMax);
   for (int k = threadIdx.x; k < n; k += blockDim.x) {
     int label;
-    s_occ[k] = arc_occupancy(rp, clamp_index(rp.row_arc[clamp_index(j0 + k, rp.n_row_arcs)], rp.n_arcs), mirror,
-                             lnp, label);
+    s_occ[k] = arc_occupancy(rp, clamp_index(rp.row_arc[clamp_index(j0 + k, rp.n_row_arcs)], rp.n_arcs), label);
     s_label[k] = label;
   }
   __syncthreads();
