@@ -35,7 +35,7 @@ struct GradParams {
 };
 
 constexpr int kGradThreads = 256;
-constexpr int kGradChunksPerThread = 4;
+constexpr int kGradChunksPerThread = 2;
 constexpr int kGradTileChunks = kGradThreads * kGradChunksPerThread;
 
 __device__ __forceinline__ float grad_elem(float z, int v, const RowInfo& ri, int blank) {

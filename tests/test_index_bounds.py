@@ -123,7 +123,7 @@ def test_gradient_kernel_chunk_mapping(B, T, U, V, dt):
     epc = EPC[dt]
     n_elem = B * T * (U + 1) * V
     n_rows = B * T * (U + 1)
-    tile = 256 * 4
+    tile = 256 * 2  # threads x chunks per thread
     chunks = -(-n_elem // epc)
     blocks = -(-chunks // tile)
     assert blocks < 2**31
@@ -197,7 +197,7 @@ def test_gradient_kernel_fast_path_buffer(B, T, U, V, dt):
     epc = EPC[dt]
     n_elem = B * T * (U + 1) * V
     n_rows = B * T * (U + 1)
-    tile = 256 * 4
+    tile = 256 * 2  # threads x chunks per thread
     n_chunks = -(-n_elem // epc)
     n_full = n_elem // epc
     blocks = -(-n_chunks // tile)
