@@ -259,13 +259,13 @@ template <typename Tin, typename Tout>
 hipError_t launch_k3(const GradParams& p, hipStream_t stream) {
   constexpr int EPC = ElemTraits<Tin>::kPerChunk;
   const int64_t chunks = (p.n_elem + EPC - 1) / EPC;
-  const int64_t blocks = (chunks + kGradTileChunks - 1) / kGradTileChunks;
+  const int64_t blocks = (chunks + kGradTileChunks<Tin> - 1) / kGradTileChunks<Tin>;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   if (p.V < EPC)
-    hipLaunchKernelGGL((k3_grad<Tin, Tout, true>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads), 0,
+    hipLaunchKernelGGL((k3_grad<Tin, Tout, true>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads<Tin>), 0,
                        stream, p);
   else
-    hipLaunchKernelGGL((k3_grad<Tin, Tout, false>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads), 0,
+    hipLaunchKernelGGL((k3_grad<Tin, Tout, false>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads<Tin>), 0,
                        stream, p);
   return hipGetLastError();
 }

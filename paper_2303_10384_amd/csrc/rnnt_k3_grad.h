@@ -34,9 +34,13 @@ struct GradParams {
   int32_t V, blank;
 };
 
-constexpr int kGradThreads = 256;
 constexpr int kGradChunksPerThread = 2;
-constexpr int kGradTileChunks = kGradThreads * kGradChunksPerThread;
+// Threads per block: 128 for float32 logits (HBM-bound: small blocks balance
+// best), 256 for 16-bit logits (eight elements per chunk, issue-bound).
+template <typename Tin>
+constexpr int kGradThreads = sizeof(Tin) == 4 ? 128 : 256;
+template <typename Tin>
+constexpr int kGradTileChunks = kGradThreads<Tin> * kGradChunksPerThread;
 
 __device__ __forceinline__ float grad_elem(float z, int v, const RowInfo& ri, int blank) {
   const float pr = fast_exp2(fmaf(z, kLog2eF, -ri.lse2));
@@ -66,12 +70,13 @@ template <typename T, typename Tout, bool SMALLV>
 __device__ __forceinline__ void grad_chunks_general(const GradParams& p, int64_t tile0, int64_t r_tile,
                                                     uint32_t v_tile) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
+  constexpr int kThreads = kGradThreads<T>;
   const uint32_t uV = static_cast<uint32_t>(p.V);
   const uint4* __restrict__ src = static_cast<const uint4*>(p.logits);
   const T* __restrict__ src_e = static_cast<const T*>(p.logits);
   Tout* __restrict__ dst_e = static_cast<Tout*>(p.grad);
   for (int q = 0; q < kGradChunksPerThread; ++q) {
-    const int cl = q * kGradThreads + static_cast<int>(threadIdx.x);
+    const int cl = q * kThreads + static_cast<int>(threadIdx.x);
     const int64_t c = tile0 + cl;
     const int64_t e0 = c * EPC;
     if (e0 >= p.n_elem) break;
@@ -109,7 +114,7 @@ __device__ __forceinline__ void grad_chunks_general(const GradParams& p, int64_t
 }
 
 // Tin: logits element type; Tout: gradient element type (Tin or float).
-// A block covers kGradTileChunks consecutive chunks.  Every block but the one
+// A block covers kGradTileChunks<Tin> consecutive chunks.  Every block but the one
 // holding the tensor's final partial chunk takes the fast path, in three phases
 // that keep all of a thread's memory requests in flight together: the row
 // records of its chunks; the logits of its chunks, as buffer loads issued
@@ -117,17 +122,19 @@ __device__ __forceinline__ void grad_chunks_general(const GradParams& p, int64_t
 // buffer's end, which reads zero without touching memory); arithmetic and
 // stores.
 template <typename Tin, typename Tout, bool SMALLV>
-__global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
+__global__ __launch_bounds__(kGradThreads<Tin>) void k3_grad(GradParams p) {
   using T = Tin;
   constexpr int EPC = ElemTraits<T>::kPerChunk;
+  constexpr int kThreads = kGradThreads<Tin>;
+  constexpr int kTile = kGradTileChunks<Tin>;
   constexpr int Q = kGradChunksPerThread;
-  const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kGradTileChunks;
+  const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kTile;
   const int64_t e_tile = tile0 * EPC;
   const int64_t r_tile = e_tile / p.V;
   const uint32_t v_tile = static_cast<uint32_t>(e_tile - r_tile * p.V);
   const uint32_t uV = static_cast<uint32_t>(p.V);
   const int64_t n_full = p.n_elem / EPC;  // chunks wholly inside the tensor
-  if (SMALLV || (p.n_elem % EPC != 0 && tile0 + kGradTileChunks > n_full)) {
+  if (SMALLV || (p.n_elem % EPC != 0 && tile0 + kTile > n_full)) {
     grad_chunks_general<T, Tout, SMALLV>(p, tile0, r_tile, v_tile);
     return;
   }
@@ -137,7 +144,7 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
   RowInfo ri0[Q], ri1[Q];
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
-    const uint32_t off = v_tile + static_cast<uint32_t>(q * kGradThreads + static_cast<int>(threadIdx.x)) * EPC;
+    const uint32_t off = v_tile + static_cast<uint32_t>(q * kThreads + static_cast<int>(threadIdx.x)) * EPC;
     const uint32_t dr = off / uV;
     r[q] = min(r_tile + dr, p.n_rows - 1);  // chunks past the end read a valid record and store nothing
     v[q] = static_cast<int>(off - dr * uV);
@@ -145,14 +152,14 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
     ri1[q] = p.rowinfo[min(r[q] + 1, p.n_rows - 1)];
   }
   __builtin_amdgcn_sched_barrier(0);  // all record loads issue before any of them is used
-  const int64_t tile_bytes = min<int64_t>(kGradTileChunks, n_full - tile0) * 16;
+  const int64_t tile_bytes = min<int64_t>(kTile, n_full - tile0) * 16;
   const __amdgpu_buffer_rsrc_t rsrc = make_buffer(static_cast<const uint4*>(p.logits) + tile0, tile_bytes);
   u32x4 raw[Q];
   bool store[Q];
   bool any_row[Q];  // some lane's chunk q touches a row with a gradient
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
-    const int cl = q * kGradThreads + static_cast<int>(threadIdx.x);
+    const int cl = q * kThreads + static_cast<int>(threadIdx.x);
     const bool live = tile0 + cl < n_full;
     const bool split = v[q] + EPC > p.V;
     const bool zero = ri0[q].label == kZeroRow && (!split || ri1[q].label == kZeroRow);
@@ -181,7 +188,7 @@ __global__ __launch_bounds__(kGradThreads) void k3_grad(GradParams p) {
 #pragma unroll
       for (int j = 0; j < EPC; ++j) out[j] = 0.f;
     }
-    if (store[q]) store_chunk<Tout, EPC>(p.grad, (tile0 + q * kGradThreads + static_cast<int>(threadIdx.x)) * EPC, out);
+    if (store[q]) store_chunk<Tout, EPC>(p.grad, (tile0 + q * kThreads + static_cast<int>(threadIdx.x)) * EPC, out);
   }
 }
 

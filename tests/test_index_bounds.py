@@ -123,7 +123,7 @@ def test_gradient_kernel_chunk_mapping(B, T, U, V, dt):
     epc = EPC[dt]
     n_elem = B * T * (U + 1) * V
     n_rows = B * T * (U + 1)
-    tile = 256 * 2  # threads x chunks per thread
+    tile = (128 if dt == "f32" else 256) * 2  # threads x chunks per thread
     chunks = -(-n_elem // epc)
     blocks = -(-chunks // tile)
     assert blocks < 2**31
@@ -135,7 +135,7 @@ def test_gradient_kernel_chunk_mapping(B, T, U, V, dt):
     r_tile = e_tile // V
     v_tile = e_tile - r_tile * V
     assert np.all(v_tile < V)
-    for cl in (0, 1, 255, 256, tile - 1):
+    for cl in (0, 1, tile // 2 - 1, tile // 2, tile - 1):
         c = tile0 + cl
         e0 = c * epc
         live = e0 < n_elem
@@ -197,7 +197,7 @@ def test_gradient_kernel_fast_path_buffer(B, T, U, V, dt):
     epc = EPC[dt]
     n_elem = B * T * (U + 1) * V
     n_rows = B * T * (U + 1)
-    tile = 256 * 2  # threads x chunks per thread
+    tile = (128 if dt == "f32" else 256) * 2  # threads x chunks per thread
     n_chunks = -(-n_elem // epc)
     n_full = n_elem // epc
     blocks = -(-n_chunks // tile)
