@@ -204,8 +204,11 @@ hipError_t launch_k2_v(const LatticeParams& p, hipStream_t stream) {
   switch (units_per_lane(p.U_max + 1)) {
     case 1: return launch_k2_k<1, VAR, MODE, DENSE_IN>(p, stream);
     case 2: return launch_k2_k<2, VAR, MODE, DENSE_IN>(p, stream);
+    case 3: return launch_k2_k<3, VAR, MODE, DENSE_IN>(p, stream);
     case 4: return launch_k2_k<4, VAR, MODE, DENSE_IN>(p, stream);
+    case 6: return launch_k2_k<6, VAR, MODE, DENSE_IN>(p, stream);
     case 8: return launch_k2_k<8, VAR, MODE, DENSE_IN>(p, stream);
+    case 12: return launch_k2_k<12, VAR, MODE, DENSE_IN>(p, stream);
     default: return launch_k2_k<16, VAR, MODE, DENSE_IN>(p, stream);
   }
 }
@@ -231,8 +234,11 @@ hipError_t launch_k2v_v(const ViterbiParams& p, hipStream_t stream) {
   switch (units_per_lane(p.U_max + 1)) {
     case 1: return launch_k2v_k<1, VAR>(p, stream);
     case 2: return launch_k2v_k<2, VAR>(p, stream);
+    case 3: return launch_k2v_k<3, VAR>(p, stream);
     case 4: return launch_k2v_k<4, VAR>(p, stream);
+    case 6: return launch_k2v_k<6, VAR>(p, stream);
     case 8: return launch_k2v_k<8, VAR>(p, stream);
+    case 12: return launch_k2v_k<12, VAR>(p, stream);
     default: return launch_k2v_k<16, VAR>(p, stream);
   }
 }

@@ -109,8 +109,11 @@ __device__ __forceinline__ double wave_shift_down(double x, double fill) {
 }
 
 // Number of units a lane owns so that 64 lanes cover U_max + 1 units.
+// Units per lane of the sweeps: the smallest of 1, 2, 3, 4, 6, 8, 12, 16 with 64
+// lanes covering U_max + 1 units (a lane's step costs about K cells).
 __host__ __device__ constexpr int units_per_lane(int units1) {
-  return units1 <= 64 ? 1 : units1 <= 128 ? 2 : units1 <= 256 ? 4 : units1 <= 512 ? 8 : 16;
+  return units1 <= 64 ? 1 : units1 <= 128 ? 2 : units1 <= 192 ? 3 : units1 <= 256 ? 4
+       : units1 <= 384 ? 6 : units1 <= 512 ? 8 : units1 <= 768 ? 12 : 16;
 }
 
 // The value of unit u in this lane's slots (x[k] holds unit lane*K + k), or

@@ -259,8 +259,9 @@ def test_random_shapes(torch, pkg, dtype, gdt, variant, B, T, U, V, blank, seed)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("variant", VARIANTS)
 @pytest.mark.parametrize("B,T,U,V,seed", [
-    (2, 4, 300, 6, 21),    # 8 units per lane of the sweep; a diagonal split over two populate blocks
-    (1, 3, 700, 5, 22),    # 16 units per lane
+    (2, 5, 150, 7, 24),    # 3 units per lane of the sweep
+    (2, 4, 300, 6, 21),    # 6 units per lane; a diagonal split over two populate blocks
+    (1, 3, 700, 5, 22),    # 12 units per lane
     (1, 2, 1023, 3, 23),   # the widest label axis the sweep takes (U_max + 1 = 1024)
 ])
 def test_wide_label_axis(torch, pkg, dtype, variant, B, T, U, V, seed):

@@ -160,7 +160,7 @@ def test_lattice_kernel_addresses(B, T, U, V, dt):
     u_pad = 64*K wide; the posterior kernel reads alpha, beta only at diagonals <= D."""
     U1 = U + 1
     ND = T + U
-    K = next(k for k in (1, 2, 4, 8, 16) if U1 <= 64 * k)
+    K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16) if U1 <= 64 * k)
     u_pad = 64 * K
     n_cells = B * ND * U1
     n_scores = B * (ND + 1) * u_pad
@@ -250,7 +250,7 @@ def test_viterbi_kernel_addresses(B, T, U, V, dt):
     word the walk reads lies in the current window."""
     U1 = U + 1
     ND = T + U
-    K = next(k for k in (1, 2, 4, 8, 16) if U1 <= 64 * k)
+    K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16) if U1 <= 64 * k)
     words = (ND + 1) * K
     for Tb, Ub in [(T, U), (1, 0), (max(1, T // 2), U // 2), (1, U), (T, 0)]:
         D = Tb - 1 + Ub
