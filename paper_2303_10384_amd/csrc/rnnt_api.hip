@@ -96,11 +96,12 @@ K1Shape k1_shape(int V) {
   const int interior = V / EPC;
   K1Shape best{64, 5, false};
   int best_slots = 1 << 30;
-  // ties go to the smaller G: more rows per wave share each reduction
+  // ties go to the larger G (fewer chunks per lane; measured faster on 16-bit
+  // rows of 1025, where G = 32 x NB = 4 and G = 64 x NB = 2 tie)
   for (int g : {8, 16, 32, 64}) {
     for (int nb = 1; nb <= 5; ++nb) {
       const int slots = g * nb;
-      if (slots >= interior && slots < best_slots) {
+      if (slots >= interior && slots <= best_slots) {
         best = K1Shape{g, nb, true};
         best_slots = slots;
       }

@@ -23,7 +23,7 @@ def k1_shape(V, epc):
     best, best_slots = (64, 5, False), 1 << 30
     for g in (8, 16, 32, 64):
         for nb in range(1, 6):
-            if g * nb >= interior and g * nb < best_slots:
+            if g * nb >= interior and g * nb <= best_slots:
                 best, best_slots = (g, nb, True), g * nb
     return best
 
