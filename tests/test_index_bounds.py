@@ -33,7 +33,7 @@ def test_populate_kernel_addresses(B, T, U, V, dt):
     epc = EPC[dt]
     n_elem = B * T * (U + 1) * V
     G, NB, fast = k1_shape(V, epc)
-    rows_per_block = min(U + 1, 256)
+    rows_per_block = min(U + 1, 32 if dt == "f32" else 256)  # units of a diagonal per block
     n_ublk = -(-(U + 1) // rows_per_block)
     ND = T + U
     DPB = 1  # anti-diagonals per block
