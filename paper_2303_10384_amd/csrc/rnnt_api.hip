@@ -197,8 +197,8 @@ ViterbiLayout make_viterbi_layout(const rnnt_shape_t& s) {
 template <int K, int VAR, int MODE, bool DENSE_IN>
 hipError_t launch_k2_k(const LatticeParams& p, hipStream_t stream) {
   constexpr int PF = (K >= 16) ? 2 : (48 / K > 24 ? 24 : 48 / K);  // diagonals of weights in flight
-  const int threads = (MODE == kLossOnly) ? 64 : 128;
-  hipLaunchKernelGGL((k2_lattice<K, PF, VAR, MODE, DENSE_IN>), dim3(p.B), dim3(threads), 0, stream, p);
+  const int sweeps = (MODE == kLossOnly) ? 1 : 2;  // forward only, or forward and backward
+  hipLaunchKernelGGL((k2_lattice<K, PF, VAR, MODE, DENSE_IN>), dim3(p.B, sweeps), dim3(64), 0, stream, p);
   return hipGetLastError();
 }
 

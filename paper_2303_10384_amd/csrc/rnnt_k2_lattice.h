@@ -16,7 +16,8 @@
 // d-1 (forward) or d+1 (backward).  One wavefront sweeps the diagonals, lane j
 // owning the K consecutive units u = K*j .. K*j+K-1, so a step exchanges one
 // value with the neighbouring lane (a DPP whole-wave shift).  The forward and
-// backward waves of an utterance run concurrently in one block.  The weights of
+// backward waves of an utterance run concurrently, each a one-wavefront block of
+// its own (blockIdx.y), so that the two chains do not share a compute unit.  The weights of
 // the next PF diagonals stay in flight in registers (one contiguous run per
 // diagonal in the anti-diagonal layout of kernel 1).  No node is masked:
 // absent arcs carry kNoArc, so a node outside the utterance accumulates only
@@ -131,7 +132,7 @@ __device__ __forceinline__ double at_unit(const double (&x)[K], int lane, int u,
 // VAR: 0 RNN-T, 1 W-Transducer force-final, 2 allow-ignore.
 // DENSE_IN: weights from the dense natural-log arrays instead of kernel 1.
 template <int K, int PF, int VAR, int MODE, bool DENSE_IN>
-__global__ __launch_bounds__(MODE == kLossOnly ? 64 : 128) void k2_lattice(LatticeParams p) {
+__global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   const int T = p.logit_lens[b];
@@ -149,6 +150,7 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 128) void k2_lattice(Latti
     }
   }
   bad = __syncthreads_or(bad);
+  // both sweeps of an utterance reach the same verdict and store the same values
   if (tid == 0) p.status[b] = (ok && !bad) ? 0 : 1;
   if (!ok || bad) {
     if (tid == 0) {
@@ -159,8 +161,8 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 128) void k2_lattice(Latti
     return;
   }
 
-  const int wave = tid >> 6;
-  const int lane = tid & 63;
+  const int wave = blockIdx.y;  // 0: forward, 1: backward (a block of its own, one wavefront)
+  const int lane = tid;
   const int D = T - 1 + U;  // last diagonal
   const int owner_top = U / K;  // lane owning u = U
   // weights of cell (e, u) clamped into the utterance: diagonal into [0, D], then the
@@ -202,9 +204,11 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 128) void k2_lattice(Latti
 
     double rb[PF][K], rl[PF][K];
 #pragma unroll
-    for (int s = 0; s < PF; ++s)
+    for (int s = 0; s < PF; ++s) {
 #pragma unroll
       for (int k = 0; k < K; ++k) load_w(s, k, rb[s][k], rl[s][k]);
+      __builtin_amdgcn_sched_barrier(0);  // issue order = use order (oldest first)
+    }
 
     // whole blocks of PF steps, no branch around loads or stores; the up to PF-1
     // steps past D touch only nodes outside the utterance and store into spare rows
@@ -267,9 +271,11 @@ __global__ __launch_bounds__(MODE == kLossOnly ? 64 : 128) void k2_lattice(Latti
 
     double rb[PF][K], rl[PF][K];
 #pragma unroll
-    for (int s = 0; s < PF; ++s)
+    for (int s = 0; s < PF; ++s) {
 #pragma unroll
       for (int k = 0; k < K; ++k) load_w(D - 1 - s, k, rb[s][k], rl[s][k]);
+      __builtin_amdgcn_sched_barrier(0);  // issue order = use order (oldest first)
+    }
 
     for (int d0 = D - 1; d0 >= 0; d0 -= PF) {
 #pragma unroll

@@ -113,9 +113,11 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
 
   double rb[PF][K], rl[PF][K];
 #pragma unroll
-  for (int s = 0; s < PF; ++s)
+  for (int s = 0; s < PF; ++s) {
 #pragma unroll
     for (int k = 0; k < K; ++k) load_w(s, k, rb[s][k], rl[s][k]);
+    __builtin_amdgcn_sched_barrier(0);  // issue order = use order (oldest first)
+  }
 
   for (int d0 = 1; d0 <= D; d0 += PF) {
 #pragma unroll
