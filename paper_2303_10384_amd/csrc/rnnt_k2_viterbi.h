@@ -198,10 +198,11 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
   // walks while its word lies in [lo, lo + 64); true once (0,0) is reached or the path jumped
   auto walk = [&](const uint64_t& win, int lo) {
     while (t + u > 0) {
-      const int widx = (t + u) * K + u % K;
+      const unsigned uu = static_cast<unsigned>(u);  // u >= 0: unsigned division by K is a shift or a multiply
+      const int widx = (t + u) * K + static_cast<int>(uu % K);
       if (widx < lo) return false;
       const uint64_t wd = readlane_u64(win, widx - lo);
-      const bool bit = (wd >> (u / K)) & 1u;
+      const bool bit = (wd >> (uu / K)) & 1u;
       // the move, without branches: the label arc (t,u-1)->(t,u) (the only way into (0,u))
       // emits unit u at frame t; at u = 0 a set bit is the initial wild-card arc from (0,0)
       const bool label = u > 0 && (bit || t == 0);
