@@ -202,15 +202,19 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
       const int widx = (t + u) * K + static_cast<int>(uu % K);
       if (widx < lo) return false;
       const uint64_t wd = readlane_u64(win, widx - lo);
-      const bool bit = (wd >> (uu / K)) & 1u;
-      // the move, without branches: the label arc (t,u-1)->(t,u) (the only way into (0,u))
-      // emits unit u at frame t; at u = 0 a set bit is the initial wild-card arc from (0,0)
-      const bool label = u > 0 && (bit || t == 0);
-      const bool jumped = VAR != 0 && u == 0 && bit;
+      // the move, without branches and in integer 0/1 flags (scalar arithmetic; boolean
+      // flags went through a vector select and back): the label arc (t,u-1)->(t,u) (the
+      // only way into (0,u)) emits unit u at frame t; at u = 0 a set bit is the initial
+      // wild-card arc from (0,0).  t, u >= 0 here.
+      const unsigned bit = static_cast<unsigned>(wd >> (uu / K)) & 1u;
+      const unsigned u_pos = static_cast<unsigned>(-u) >> 31;      // u > 0
+      const unsigned t_zero = static_cast<unsigned>(t - 1) >> 31;  // t == 0
+      const int label = static_cast<int>(u_pos & (bit | t_zero));
+      const bool jumped = VAR != 0 && (bit & (u_pos ^ 1u)) != 0;
       s_frames[label ? u - 1 : kViterbiMaxUnits1] = t;  // every lane the same value; a spare slot otherwise
       start_frame = jumped ? t : start_frame;
-      u -= label ? 1 : 0;
-      t = jumped ? 0 : t - (label ? 0 : 1);  // a jump ends the walk: (t,u) becomes (0,0)
+      u -= label;
+      t = jumped ? 0 : t - 1 + label;  // a jump ends the walk: (t,u) becomes (0,0)
     }
     return true;
   };
