@@ -348,7 +348,7 @@ struct PostParams {
   double* loss_bwd_out;
 };
 
-constexpr int kPostThreads = 256;
+constexpr int kPostThreads = 1024;
 constexpr int kPostTileT = 8;  // frames per block
 
 // One block per (utterance, kPostTileT frames t0 .. t0+7, every unit).  Its
