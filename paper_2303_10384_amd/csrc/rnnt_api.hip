@@ -6,12 +6,7 @@
 #include <cstdint>
 
 #include "rnnt_mi355x.h"
-#include "rnnt_device.h"
-#include "rnnt_k1_populate.h"
-#include "rnnt_k2_lattice.h"
-#include "rnnt_k3_grad.h"
-#include "rnnt_k2_viterbi.h"
-#include "rnnt_arc_kernels.h"
+#include "rnnt_launch.h"
 
 namespace rnnt {
 namespace {
@@ -80,96 +75,6 @@ Layout make_layout(const rnnt_shape_t& s, bool with_populate) {
   return L;
 }
 
-// ---- kernel 1 ---------------------------------------------------------------
-
-// Lanes per row G and interior chunks per lane NB: the smallest G*NB that
-// covers a row's interior chunks (at most V / EPC of them) with NB <= 5; rows
-// with more take the batched path (G = 64, NB = 5).
-struct K1Shape {
-  int G, NB;
-  bool fast;
-};
-
-template <typename T>
-K1Shape k1_shape(int V) {
-  constexpr int EPC = ElemTraits<T>::kPerChunk;
-  const int interior = V / EPC;
-  K1Shape best{64, 5, false};
-  int best_slots = 1 << 30;
-  // ties go to the larger G (fewer chunks per lane; measured faster on 16-bit
-  // rows of 1025, where G = 32 x NB = 4 and G = 64 x NB = 2 tie)
-  for (int g : {8, 16, 32, 64}) {
-    for (int nb = 1; nb <= 5; ++nb) {
-      const int slots = g * nb;
-      if (slots >= interior && slots <= best_slots) {
-        best = K1Shape{g, nb, true};
-        best_slots = slots;
-      }
-    }
-  }
-  return best;
-}
-
-// one block per anti-diagonal, split into blocks of at most 32 units for float32
-// rows (measured faster) and kMaxRowsPerBlock units for 16-bit ones
-void k1_blocking(PopulateParams& p, int elem_bytes) {
-  const int cap = elem_bytes == 4 ? 32 : kMaxRowsPerBlock;
-  p.rows_per_block = p.U_max + 1 < cap ? p.U_max + 1 : cap;
-  p.n_ublk = (p.U_max + 1 + p.rows_per_block - 1) / p.rows_per_block;
-}
-
-template <typename T, int G, int NB, int OUT, bool FAST>
-hipError_t launch_k1_g(PopulateParams p, hipStream_t stream) {
-  k1_blocking(p, static_cast<int>(sizeof(T)));
-  const int64_t blocks = static_cast<int64_t>(p.B) * (p.T_max + p.U_max) * p.n_ublk;
-  const int64_t runs = (blocks + kXcdRun - 1) / kXcdRun;  // whole rounds of the XCD-major numbering
-  const int64_t grid = (runs + kXcds - 1) / kXcds * kXcds * kXcdRun;
-  if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((k1_populate<T, G, NB, OUT, FAST>), dim3(static_cast<uint32_t>(grid)), dim3(256), 0,
-                     stream, p);
-  return hipGetLastError();
-}
-
-template <typename T, int G, int OUT>
-hipError_t launch_k1_nb(int nb, const PopulateParams& p, hipStream_t stream) {
-  switch (nb) {
-    case 1: return launch_k1_g<T, G, 1, OUT, true>(p, stream);
-    case 2: return launch_k1_g<T, G, 2, OUT, true>(p, stream);
-    case 3: return launch_k1_g<T, G, 3, OUT, true>(p, stream);
-    case 4: return launch_k1_g<T, G, 4, OUT, true>(p, stream);
-    default: return launch_k1_g<T, G, 5, OUT, true>(p, stream);
-  }
-}
-
-// A block's rows on one diagonal lie U_max rows apart; the fast path addresses
-// them through one buffer resource with 32-bit offsets.
-bool k1_span_fits(PopulateParams p, int elem_bytes) {
-  k1_blocking(p, elem_bytes);
-  const int64_t rows = static_cast<int64_t>(p.rows_per_block - 1) * p.U_max + 1;
-  return rows * p.V * elem_bytes + 64 < 0x7fffffffLL;
-}
-
-template <typename T, int OUT>
-hipError_t launch_k1(const PopulateParams& p, hipStream_t stream) {
-  const K1Shape ks = k1_shape<T>(p.V);
-  if (!ks.fast || !k1_span_fits(p, static_cast<int>(sizeof(T)))) return launch_k1_g<T, 64, 5, OUT, false>(p, stream);
-  switch (ks.G) {
-    case 8: return launch_k1_nb<T, 8, OUT>(ks.NB, p, stream);
-    case 16: return launch_k1_nb<T, 16, OUT>(ks.NB, p, stream);
-    case 32: return launch_k1_nb<T, 32, OUT>(ks.NB, p, stream);
-    default: return launch_k1_nb<T, 64, OUT>(ks.NB, p, stream);
-  }
-}
-
-template <int OUT>
-hipError_t launch_k1_dtype(rnnt_dtype_t dt, const PopulateParams& p, hipStream_t stream) {
-  switch (dt) {
-    case RNNT_DTYPE_F32: return launch_k1<float, OUT>(p, stream);
-    case RNNT_DTYPE_BF16: return launch_k1<bf16_t, OUT>(p, stream);
-    default: return launch_k1<f16_t, OUT>(p, stream);
-  }
-}
-
 // Workspace of the forced alignment: the lattice form (lp2, lse2) as in the loss,
 // the decision words B * (T_max+U_max+1) * K uint64, 256-byte aligned pieces.
 struct ViterbiLayout {
@@ -192,122 +97,26 @@ ViterbiLayout make_viterbi_layout(const rnnt_shape_t& s) {
   return L;
 }
 
-// ---- kernel 2 ---------------------------------------------------------------
-
-template <int K, int VAR, int MODE, bool DENSE_IN>
-hipError_t launch_k2_k(const LatticeParams& p, hipStream_t stream) {
-  constexpr int PF = (K >= 16) ? 2 : (48 / K > 24 ? 24 : 48 / K);  // diagonals of weights in flight
-  const int sweeps = (MODE == kLossOnly) ? 1 : 2;  // forward only, or forward and backward
-  hipLaunchKernelGGL((k2_lattice<K, PF, VAR, MODE, DENSE_IN>), dim3(p.B, sweeps), dim3(64), 0, stream, p);
-  return hipGetLastError();
-}
-
-template <int VAR, int MODE, bool DENSE_IN>
-hipError_t launch_k2_v(const LatticeParams& p, hipStream_t stream) {
-  switch (units_per_lane(p.U_max + 1)) {
-    case 1: return launch_k2_k<1, VAR, MODE, DENSE_IN>(p, stream);
-    case 2: return launch_k2_k<2, VAR, MODE, DENSE_IN>(p, stream);
-    case 3: return launch_k2_k<3, VAR, MODE, DENSE_IN>(p, stream);
-    case 4: return launch_k2_k<4, VAR, MODE, DENSE_IN>(p, stream);
-    case 6: return launch_k2_k<6, VAR, MODE, DENSE_IN>(p, stream);
-    case 8: return launch_k2_k<8, VAR, MODE, DENSE_IN>(p, stream);
-    case 12: return launch_k2_k<12, VAR, MODE, DENSE_IN>(p, stream);
-    default: return launch_k2_k<16, VAR, MODE, DENSE_IN>(p, stream);
-  }
-}
-
-template <int MODE, bool DENSE_IN>
-hipError_t launch_k2(int variant, const LatticeParams& p, hipStream_t stream) {
-  switch (variant) {
-    case RNNT_VARIANT_RNNT: return launch_k2_v<0, MODE, DENSE_IN>(p, stream);
-    case RNNT_VARIANT_WRNNT: return launch_k2_v<1, MODE, DENSE_IN>(p, stream);
-    default: return launch_k2_v<2, MODE, DENSE_IN>(p, stream);
-  }
-}
-
-template <int K, int VAR>
-hipError_t launch_k2v_k(const ViterbiParams& p, hipStream_t stream) {
-  constexpr int PF = (K >= 16) ? 2 : (48 / K > 24 ? 24 : 48 / K);
-  hipLaunchKernelGGL((k2_viterbi<K, PF, VAR>), dim3(p.B), dim3(64), 0, stream, p);
-  return hipGetLastError();
-}
-
-template <int VAR>
-hipError_t launch_k2v_v(const ViterbiParams& p, hipStream_t stream) {
-  switch (units_per_lane(p.U_max + 1)) {
-    case 1: return launch_k2v_k<1, VAR>(p, stream);
-    case 2: return launch_k2v_k<2, VAR>(p, stream);
-    case 3: return launch_k2v_k<3, VAR>(p, stream);
-    case 4: return launch_k2v_k<4, VAR>(p, stream);
-    case 6: return launch_k2v_k<6, VAR>(p, stream);
-    case 8: return launch_k2v_k<8, VAR>(p, stream);
-    case 12: return launch_k2v_k<12, VAR>(p, stream);
-    default: return launch_k2v_k<16, VAR>(p, stream);
-  }
-}
-
-hipError_t launch_k2v(int variant, const ViterbiParams& p, hipStream_t stream) {
-  switch (variant) {
-    case RNNT_VARIANT_RNNT: return launch_k2v_v<0>(p, stream);
-    case RNNT_VARIANT_WRNNT: return launch_k2v_v<1>(p, stream);
-    default: return launch_k2v_v<2>(p, stream);
-  }
-}
-
-template <bool DENSE>
-hipError_t launch_k2b(const PostParams& p, hipStream_t stream) {
-  const int64_t blocks = static_cast<int64_t>(p.B) * ((p.T_max + kPostTileT - 1) / kPostTileT);
-  if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((k2b_posteriors<DENSE>), dim3(static_cast<uint32_t>(blocks)), dim3(kPostThreads), 0, stream, p);
-  return hipGetLastError();
-}
-
-// ---- kernel 3 ---------------------------------------------------------------
-
-template <typename Tin, typename Tout>
-hipError_t launch_k3(const GradParams& p, hipStream_t stream) {
-  constexpr int EPC = ElemTraits<Tin>::kPerChunk;
-  const int64_t chunks = (p.n_elem + EPC - 1) / EPC;
-  const int64_t blocks = (chunks + kGradTileChunks<Tin> - 1) / kGradTileChunks<Tin>;
-  if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  if (p.V < EPC)
-    hipLaunchKernelGGL((k3_grad<Tin, Tout, true>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads<Tin>), 0,
-                       stream, p);
-  else
-    hipLaunchKernelGGL((k3_grad<Tin, Tout, false>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads<Tin>), 0,
-                       stream, p);
-  return hipGetLastError();
-}
-
-hipError_t launch_k3_dtype(rnnt_dtype_t dt, rnnt_dtype_t gdt, const GradParams& p, hipStream_t stream) {
-  const bool f32_out = gdt == RNNT_DTYPE_F32;
-  switch (dt) {
-    case RNNT_DTYPE_F32: return launch_k3<float, float>(p, stream);
-    case RNNT_DTYPE_BF16: return f32_out ? launch_k3<bf16_t, float>(p, stream) : launch_k3<bf16_t, bf16_t>(p, stream);
-    default: return f32_out ? launch_k3<f16_t, float>(p, stream) : launch_k3<f16_t, f16_t>(p, stream);
-  }
-}
-
 bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
 
-// Stream-ordered scratch when the caller passes no workspace.
-struct Scratch {
+// Stream-ordered workspace when the caller passes none.
+struct OwnedWorkspace {
   void* ptr = nullptr;
   hipStream_t stream = nullptr;
-  ~Scratch() {
+  ~OwnedWorkspace() {
     if (ptr) (void)hipFreeAsync(ptr, stream);
   }
 };
 
 rnnt_status_t take_workspace(void* workspace, size_t workspace_bytes, size_t need, hipStream_t stream,
-                             Scratch& scratch, char** ws) {
+                             OwnedWorkspace& owned, char** ws) {
   if (workspace && workspace_bytes < need) return RNNT_ERR_WORKSPACE;
   if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u)) return RNNT_ERR_ALIGNMENT;
   *ws = static_cast<char*>(workspace);
   if (!*ws) {
-    if (hipMallocAsync(&scratch.ptr, need, stream) != hipSuccess) return RNNT_ERR_HIP;
-    scratch.stream = stream;
-    *ws = static_cast<char*>(scratch.ptr);
+    if (hipMallocAsync(&owned.ptr, need, stream) != hipSuccess) return RNNT_ERR_HIP;
+    owned.stream = stream;
+    *ws = static_cast<char*>(owned.ptr);
   }
   return RNNT_OK;
 }
@@ -373,59 +182,19 @@ bool plan_consistent(const rnnt_arc_plan_t& pl, const rnnt_shape_t& s) {
   return true;
 }
 
-template <int NW, int DM>
-hipError_t launch_sweep_t(const ArcSweepParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL((k_arc_sweep<NW, DM>), dim3(2 * p.B), dim3(64 * NW), 0, stream, p);
-  return hipGetLastError();
-}
-
-template <int NS>
-hipError_t launch_sweep_ns(int dm, const ArcSweepParams& p, hipStream_t stream) {
-  switch (dm) {
-    case 1: return launch_sweep_t<NS, 1>(p, stream);
-    case 2: return launch_sweep_t<NS, 2>(p, stream);
-    default: return launch_sweep_t<NS, 4>(p, stream);
-  }
-}
-
-// one wavefront per chunk of 64 states of the plan's typical level, up to DM slots
-// per state held in registers
-hipError_t launch_sweep(int ns, int dm, const ArcSweepParams& p, hipStream_t stream) {
-  switch (ns) {
-    case 1: return launch_sweep_ns<1>(dm, p, stream);
-    case 2: return launch_sweep_ns<2>(dm, p, stream);
-    default: return launch_sweep_ns<4>(dm, p, stream);
-  }
-}
-
-hipError_t launch_arc_populate(rnnt_dtype_t dt, const ArcPopulateParams& p, hipStream_t stream) {
-  const int n = p.n_slots0 > p.n_slots1 ? p.n_slots0 : p.n_slots1;
-  if (n == 0) return hipSuccess;
-  const dim3 grid((n + 255) / 256);
-  switch (dt) {
-    case RNNT_DTYPE_F32: hipLaunchKernelGGL((k_arc_populate<float>), grid, dim3(256), 0, stream, p); break;
-    case RNNT_DTYPE_BF16: hipLaunchKernelGGL((k_arc_populate<bf16_t>), grid, dim3(256), 0, stream, p); break;
-    default: hipLaunchKernelGGL((k_arc_populate<f16_t>), grid, dim3(256), 0, stream, p); break;
-  }
-  return hipGetLastError();
-}
-
-template <typename Tin, typename Tout>
-hipError_t launch_extra_rows_t(const ArcExtraParams& p, int n, hipStream_t stream) {
-  hipLaunchKernelGGL((k_arc_extra_rows<Tin, Tout>), dim3(n), dim3(256), 0, stream, p);
-  return hipGetLastError();
-}
-
-hipError_t launch_extra_rows(rnnt_dtype_t dt, rnnt_dtype_t gdt, const ArcExtraParams& p, int n, hipStream_t stream) {
-  if (n == 0) return hipSuccess;
-  const bool f32_out = gdt == RNNT_DTYPE_F32;
-  switch (dt) {
-    case RNNT_DTYPE_F32: return launch_extra_rows_t<float, float>(p, n, stream);
-    case RNNT_DTYPE_BF16:
-      return f32_out ? launch_extra_rows_t<bf16_t, float>(p, n, stream) : launch_extra_rows_t<bf16_t, bf16_t>(p, n, stream);
-    default:
-      return f32_out ? launch_extra_rows_t<f16_t, float>(p, n, stream) : launch_extra_rows_t<f16_t, f16_t>(p, n, stream);
-  }
+// Checks of rnnt_loss's arguments that need no device.
+rnnt_status_t check_loss_args(const void* logits, const rnnt_shape_t& shape, const int32_t* labels,
+                              const int32_t* logit_lens, const int32_t* label_lens, int32_t blank, int variant,
+                              const float* loss_out, const void* grad_out) {
+  const rnnt_status_t st = check_shape(shape);
+  if (st != RNNT_OK) return st;
+  if (!logits || !logit_lens || !label_lens || !loss_out || (!labels && shape.U_max > 0))
+    return RNNT_ERR_NULL_PTR;
+  if (blank < 0 || blank >= shape.V) return RNNT_ERR_BAD_BLANK;
+  if (!variant_known(variant)) return RNNT_ERR_BAD_VARIANT;
+  if (!aligned16(logits) || (grad_out && !aligned16(grad_out))) return RNNT_ERR_ALIGNMENT;
+  if (shape.U_max + 1 > kMaxUnits1) return RNNT_ERR_UNSUPPORTED;
+  return RNNT_OK;
 }
 
 }  // namespace
@@ -471,18 +240,13 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
                               const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
                               rnnt_variant_t variant, float* loss_out, void* grad_out, void* workspace,
                               size_t workspace_bytes, hipStream_t stream, hipEvent_t* events) {
-  rnnt_status_t st = check_shape(shape);
+  rnnt_status_t st = check_loss_args(logits, shape, labels, logit_lens, label_lens, blank, variant, loss_out,
+                                     grad_out);
   if (st != RNNT_OK) return st;
-  if (!logits || !logit_lens || !label_lens || !loss_out || (!labels && shape.U_max > 0))
-    return RNNT_ERR_NULL_PTR;
-  if (blank < 0 || blank >= shape.V) return RNNT_ERR_BAD_BLANK;
-  if (!variant_known(variant)) return RNNT_ERR_BAD_VARIANT;
-  if (!aligned16(logits) || (grad_out && !aligned16(grad_out))) return RNNT_ERR_ALIGNMENT;
-  if (shape.U_max + 1 > kMaxUnits1) return RNNT_ERR_UNSUPPORTED;
   const Layout L = make_layout(shape, true);
-  Scratch scratch;
+  OwnedWorkspace owned;
   char* ws = nullptr;
-  st = take_workspace(workspace, workspace_bytes, L.total, stream, scratch, &ws);
+  st = take_workspace(workspace, workspace_bytes, L.total, stream, owned, &ws);
   if (st != RNNT_OK) return st;
 
   const int64_t U1 = shape.U_max + 1;
@@ -506,7 +270,7 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
   p1.n_elem = n_elem;
   p1.lp2 = reinterpret_cast<double2*>(ws + L.lp2);
   p1.lse2 = reinterpret_cast<float*>(ws + L.lse2);
-  if (launch_k1_dtype<kK1Lattice>(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (launch_populate_lattice(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(1) != hipSuccess) return RNNT_ERR_HIP;
 
   // kernel 2: forward / backward sweeps
@@ -527,8 +291,7 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
   p2.lnp2_bwd = p2.lnp2_fwd + shape.B;
   p2.status = reinterpret_cast<int32_t*>(ws + L.status);
   p2.loss_f32 = loss_out;
-  const hipError_t e2 = need_grad ? launch_k2<kScores, false>(variant, p2, stream)
-                                  : launch_k2<kLossOnly, false>(variant, p2, stream);
+  const hipError_t e2 = need_grad ? launch_lattice_scores(variant, p2, stream) : launch_lattice_loss_only(variant, p2, stream);
   if (e2 != hipSuccess) return RNNT_ERR_HIP;
   if (mark(2) != hipSuccess) return RNNT_ERR_HIP;
 
@@ -551,7 +314,7 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
     pb.lnp2_bwd = p2.lnp2_bwd;
     pb.n_rows = n_rows;
     pb.rowinfo = reinterpret_cast<RowInfo*>(ws + L.rowinfo);
-    if (launch_k2b<false>(pb, stream) != hipSuccess) return RNNT_ERR_HIP;
+    if (launch_posteriors_rows(pb, stream) != hipSuccess) return RNNT_ERR_HIP;
   }
   if (mark(3) != hipSuccess) return RNNT_ERR_HIP;
 
@@ -565,7 +328,7 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
     p3.n_rows = n_rows;
     p3.V = shape.V;
     p3.blank = blank;
-    if (launch_k3_dtype(shape.dtype, shape.grad_dtype, p3, stream) != hipSuccess) return RNNT_ERR_HIP;
+    if (launch_grad(shape.dtype, shape.grad_dtype, p3, stream) != hipSuccess) return RNNT_ERR_HIP;
   }
   if (mark(4) != hipSuccess) return RNNT_ERR_HIP;
   return RNNT_OK;
@@ -602,9 +365,9 @@ rnnt_status_t rnnt_viterbi_timed(const void* logits, rnnt_shape_t shape, const i
   if (!aligned16(logits)) return RNNT_ERR_ALIGNMENT;
   if (shape.U_max + 1 > kMaxUnits1) return RNNT_ERR_UNSUPPORTED;
   const ViterbiLayout L = make_viterbi_layout(shape);
-  Scratch scratch;
+  OwnedWorkspace owned;
   char* ws = nullptr;
-  st = take_workspace(workspace, workspace_bytes, L.total, stream, scratch, &ws);
+  st = take_workspace(workspace, workspace_bytes, L.total, stream, owned, &ws);
   if (st != RNNT_OK) return st;
   auto mark = [&](int i) { return events ? hipEventRecord(events[i], stream) : hipSuccess; };
   if (mark(0) != hipSuccess) return RNNT_ERR_HIP;
@@ -622,7 +385,7 @@ rnnt_status_t rnnt_viterbi_timed(const void* logits, rnnt_shape_t shape, const i
   p1.n_elem = static_cast<int64_t>(shape.B) * shape.T_max * (shape.U_max + 1) * shape.V;
   p1.lp2 = reinterpret_cast<double2*>(ws + L.lp2);
   p1.lse2 = reinterpret_cast<float*>(ws + L.lse2);
-  if (launch_k1_dtype<kK1Lattice>(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (launch_populate_lattice(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(1) != hipSuccess) return RNNT_ERR_HIP;
 
   ViterbiParams pv{};
@@ -639,7 +402,7 @@ rnnt_status_t rnnt_viterbi_timed(const void* logits, rnnt_shape_t shape, const i
   pv.score_out = score_out;
   pv.label_frames = label_frames_out;
   pv.span = span_out;
-  if (launch_k2v(variant, pv, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (launch_viterbi(variant, pv, stream) != hipSuccess) return RNNT_ERR_HIP;
   return mark(2) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
 }
 
@@ -667,9 +430,9 @@ rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const 
   if (!aligned16(logits) || (grad_out && !aligned16(grad_out)) || !aligned16(plan_image))
     return RNNT_ERR_ALIGNMENT;
   const ArcLayout L = make_arc_layout(*plan);
-  Scratch scratch;
+  OwnedWorkspace owned;
   char* ws = nullptr;
-  st = take_workspace(workspace, workspace_bytes, L.total, stream, scratch, &ws);
+  st = take_workspace(workspace, workspace_bytes, L.total, stream, owned, &ws);
   if (st != RNNT_OK) return st;
   const char* img = static_cast<const char*>(plan_image);
   auto arr = [&](int i) { return img + plan->off[i]; };
@@ -693,7 +456,7 @@ rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const 
   p1.n_elem = n_rows * shape.V;
   p1.lse2_rows = reinterpret_cast<double*>(ws + L.lse2);
   p1.clear_flags = reinterpret_cast<int32_t*>(ws + L.bad);
-  if (launch_k1_dtype<kK1Rows>(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (launch_populate_rows(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(1) != hipSuccess) return RNNT_ERR_HIP;
 
   // arc weights in both sweep orders
@@ -717,7 +480,7 @@ rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const 
   pp.bad = p1.clear_flags;
   pp.rec0 = reinterpret_cast<int32_t*>(ws + L.w0);
   pp.rec1 = reinterpret_cast<int32_t*>(ws + L.w1);
-  if (launch_arc_populate(shape.dtype, pp, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (launch_arc_weights(shape.dtype, pp, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(2) != hipSuccess) return RNNT_ERR_HIP;
 
   // forward and backward sweeps
@@ -741,7 +504,7 @@ rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const 
   ps.bad = p1.clear_flags;
   ps.status = reinterpret_cast<int32_t*>(ws + L.status);
   ps.loss = loss_out;
-  if (launch_sweep(plan->state_chunks, plan->slots_per_state, ps, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (launch_arc_sweep(plan->state_chunks, plan->slots_per_state, ps, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(3) != hipSuccess) return RNNT_ERR_HIP;
 
   ArcRowParams pr{};
@@ -766,14 +529,7 @@ rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const 
   pr.lse2_rows = p1.lse2_rows;
   pr.rowinfo = reinterpret_cast<RowInfo*>(ws + L.rowinfo);
   pr.occ = reinterpret_cast<int2*>(ws + L.occ);
-  if (grad_out) {
-    if (pr.n_arcs > 0) {
-      hipLaunchKernelGGL(k_arc_occ, dim3(static_cast<uint32_t>((pr.n_arcs + 255) / 256)), dim3(256), 0, stream, pr);
-      if (hipGetLastError() != hipSuccess) return RNNT_ERR_HIP;
-    }
-    hipLaunchKernelGGL(k_arc_rows, dim3(static_cast<uint32_t>((n_rows + 255) / 256)), dim3(256), 0, stream, pr);
-    if (hipGetLastError() != hipSuccess) return RNNT_ERR_HIP;
-  }
+  if (grad_out && launch_arc_posteriors(pr, n_rows, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(4) != hipSuccess) return RNNT_ERR_HIP;
 
   if (grad_out) {
@@ -785,14 +541,14 @@ rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const 
     p3.n_rows = n_rows;
     p3.V = shape.V;
     p3.blank = plan->blank;
-    if (launch_k3_dtype(shape.dtype, shape.grad_dtype, p3, stream) != hipSuccess) return RNNT_ERR_HIP;
+    if (launch_grad(shape.dtype, shape.grad_dtype, p3, stream) != hipSuccess) return RNNT_ERR_HIP;
     ArcExtraParams px{};
     px.rows = pr;
     px.logits = logits;
     px.grad = grad_out;
     px.xrows = reinterpret_cast<const int32_t*>(arr(kImgXrows));
     px.V = shape.V;
-    if (launch_extra_rows(shape.dtype, shape.grad_dtype, px, plan->num_extra_rows, stream) != hipSuccess)
+    if (launch_arc_extra_rows(shape.dtype, shape.grad_dtype, px, plan->num_extra_rows, stream) != hipSuccess)
       return RNNT_ERR_HIP;
   }
   if (mark(5) != hipSuccess) return RNNT_ERR_HIP;
@@ -832,7 +588,7 @@ rnnt_status_t rnnt_log_softmax_gather(const void* logits, rnnt_shape_t shape, co
   p1.lse_out = lse_out;
   p1.lp_blank_out = lp_blank_out;
   p1.lp_label_out = lp_label_out;
-  return launch_k1_dtype<kK1Dense>(shape.dtype, p1, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
+  return launch_populate_dense(shape.dtype, p1, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
 }
 
 rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label, rnnt_shape_t shape,
@@ -850,9 +606,9 @@ rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label
   if (!variant_known(variant)) return RNNT_ERR_BAD_VARIANT;
   if (s.U_max + 1 > kMaxUnits1) return RNNT_ERR_UNSUPPORTED;
   const Layout L = make_layout(s, false);
-  Scratch scratch;
+  OwnedWorkspace owned;
   char* ws = nullptr;
-  st = take_workspace(workspace, workspace_bytes, L.total, stream, scratch, &ws);
+  st = take_workspace(workspace, workspace_bytes, L.total, stream, owned, &ws);
   if (st != RNNT_OK) return st;
 
   LatticeParams p2{};
@@ -873,7 +629,7 @@ rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label
   p2.lnp2_bwd = p2.lnp2_fwd + s.B;
   p2.status = reinterpret_cast<int32_t*>(ws + L.status);
   p2.loss_f32 = nullptr;
-  if (launch_k2<kScores, true>(variant, p2, stream) != hipSuccess) return RNNT_ERR_HIP;
+  if (launch_lattice_dense(variant, p2, stream) != hipSuccess) return RNNT_ERR_HIP;
 
   PostParams pb{};
   pb.B = s.B;
@@ -897,7 +653,7 @@ rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label
   pb.occ_label_out = occ_label_out;
   pb.loss_out = loss_out;
   pb.loss_bwd_out = loss_bwd_out;
-  return launch_k2b<true>(pb, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
+  return launch_posteriors_dense(pb, stream) == hipSuccess ? RNNT_OK : RNNT_ERR_HIP;
 }
 
 }  // extern "C"

@@ -454,8 +454,9 @@ struct ArcRowParams {
 // threads read consecutive slots, and the scores of consecutive states mostly lie
 // together too.  The row kernels then read one 8-byte pair per arc.  Padding,
 // wild-card arcs and arcs of utterances without valid scores get {0, kNoLabel}.
-__global__ __launch_bounds__(256) void k_arc_occ(ArcRowParams p) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
+template <int NT>
+__global__ __launch_bounds__(NT) void k_arc_occ(ArcRowParams p) {
+  const int i = blockIdx.x * NT + threadIdx.x;
   if (i >= p.n_arcs) return;
   const int4 a = p.arcs[i];
   int2 out = make_int2(0, kNoLabel);
@@ -478,8 +479,9 @@ __device__ __forceinline__ float arc_occupancy(const ArcRowParams& p, int i, int
   return __int_as_float(o.x);
 }
 
-__global__ __launch_bounds__(256) void k_arc_rows(ArcRowParams p) {
-  const int r = blockIdx.x * 256 + threadIdx.x;
+template <int NT>
+__global__ __launch_bounds__(NT) void k_arc_rows(ArcRowParams p) {
+  const int r = blockIdx.x * NT + threadIdx.x;
   if (r >= p.n_rows) return;
   const RowPos q = row_pos(r, p.T_max, p.U_max);
   RowInfo ri;

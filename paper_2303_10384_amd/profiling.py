@@ -30,6 +30,12 @@ SOURCES = {
         "paper_2303_10384_amd/csrc/rnnt_k1_populate.h",
         "paper_2303_10384_amd/csrc/rnnt_k2_lattice.h",
         "paper_2303_10384_amd/csrc/rnnt_k3_grad.h",
+        "paper_2303_10384_amd/csrc/rnnt_launch.h",
+        "paper_2303_10384_amd/csrc/rnnt_launch_k1.h",
+        "paper_2303_10384_amd/csrc/rnnt_launch_k1_lattice.hip",
+        "paper_2303_10384_amd/csrc/rnnt_launch_k2.h",
+        "paper_2303_10384_amd/csrc/rnnt_launch_k2_scores.hip",
+        "paper_2303_10384_amd/csrc/rnnt_launch_k3.hip",
     ],
     "arc": [
         "paper_2303_10384_amd/csrc/rnnt_api.hip",
@@ -38,6 +44,10 @@ SOURCES = {
         "paper_2303_10384_amd/csrc/rnnt_k3_grad.h",
         "paper_2303_10384_amd/csrc/rnnt_arc_layout.h",
         "paper_2303_10384_amd/csrc/rnnt_arc_kernels.h",
+        "paper_2303_10384_amd/csrc/rnnt_launch.h",
+        "paper_2303_10384_amd/csrc/rnnt_launch_k1.h",
+        "paper_2303_10384_amd/csrc/rnnt_launch_k1_rows.hip",
+        "paper_2303_10384_amd/csrc/rnnt_launch_k3.hip",
     ],
 }
 KERNEL_SOURCES = SOURCES["loss"]

@@ -92,15 +92,16 @@ def torch_dtype(name):
     return {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[name]
 
 
-def make_logits(w, device, seed=None):
-    """Logits (B, T_max, U_max+1, V) ~ N(0, sigma^2) in w.dtype (rounded to nearest even
-    from float32), drawn by torch's generator on `device`."""
+def make_logits(w, device, seed=None, dtype=None):
+    """Logits (B, T_max, U_max+1, V) ~ N(0, sigma^2) in w.dtype, or in `dtype` when given
+    (rounded to nearest even from float32), drawn by torch's generator on `device`."""
     import torch
     g = torch.Generator(device=device)
     g.manual_seed(w.seed if seed is None else seed)
     shape = (w.B, w.T_max, w.U_max + 1, w.V)
-    out = torch.empty(shape, dtype=torch_dtype(w.dtype), device=device)
-    if w.dtype == "f32":
+    dtype = dtype or w.dtype
+    out = torch.empty(shape, dtype=torch_dtype(dtype), device=device)
+    if dtype == "f32":
         out.normal_(0.0, w.sigma, generator=g)
     else:
         # draw in float32 slabs to bound the temporary memory, then round

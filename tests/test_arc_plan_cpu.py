@@ -35,14 +35,45 @@ PAD_DEGREE = const("kArcPadDegree")
 DUMMY = RING + PINS
 
 
+# When RNNT_ARC_PLAN_SANITIZED names a build of rnnt_arc_plan.cpp alone with the
+# address and undefined-behaviour sanitizers (test_arc_plan_sanitized_cpu.py makes
+# one and reruns this file in a process that preloads the sanitizer runtime), every
+# planner call below goes to that build.
+SANITIZED = os.environ.get("RNNT_ARC_PLAN_SANITIZED")
+
+
+class SanitizedPlanner:
+    """The planner's entry points from the sanitizer build, standing in for the library
+    (the planner tests call nothing else; status strings come from the binding's names)."""
+
+    def __init__(self, path, BD):
+        lib = ctypes.CDLL(path)
+        i32, i64, vp, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
+        lib.rnnt_arc_plan_bytes_bound.argtypes = [i32, i32, i32, i64, i64]
+        lib.rnnt_arc_plan_bytes_bound.restype = sz
+        lib.rnnt_arc_plan.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, sz, ctypes.POINTER(BD.ArcPlanDesc)]
+        lib.rnnt_arc_plan.restype = ctypes.c_int
+        self.rnnt_arc_plan = lib.rnnt_arc_plan
+        self.rnnt_arc_plan_bytes_bound = lib.rnnt_arc_plan_bytes_bound
+        self.names = BD.STATUS_NAMES
+
+    def rnnt_status_string(self, status):
+        return self.names.get(int(status), "unknown status").encode()
+
+
 @pytest.fixture(scope="module")
 def binding():
     from paper_2303_10384_amd import binding as BD
+    if SANITIZED:
+        saved, BD._lib = BD._lib, SanitizedPlanner(SANITIZED, BD)
+        yield BD
+        BD._lib = saved
+        return
     if not os.path.exists(BD.LIB_PATH):
         from paper_2303_10384_amd import build
         build.build(verbose=False)
     BD.load_library()
-    return BD
+    yield BD
 
 
 GENERIC = 1 << 30
@@ -323,3 +354,97 @@ def test_sources_near_the_ring_edge(binding):
     labels = rng.integers(1, V, size=(1, U))
     lattices = TP.batch_grid_lattices([T], [U], labels, 0, "wrnnt")
     check_against_oracle(binding, lattices, logits, np.array([T]), np.array([U]), 0, grad_atol=1e-9)
+
+
+def raw_plan(binding, B, T, U, V, blank, num_states, arc_begin, arcs, image_bytes=None):
+    """rnnt_arc_plan on raw host arrays (any arc_begin, even a malformed one); returns
+    (status, descriptor)."""
+    lib = binding.load_library()
+    num_states = np.ascontiguousarray(num_states, np.int32)
+    arc_begin = np.ascontiguousarray(arc_begin, np.int64)
+    arcs = np.ascontiguousarray(arcs, TP.ARC_DTYPE)
+    if image_bytes is None:
+        bound = lib.rnnt_arc_plan_bytes_bound(B, T, U, int(max(0, num_states.sum())), int(max(0, len(arcs))))
+        image_bytes = int(bound) if bound else 256
+    image = np.zeros(max(image_bytes, 1), np.uint8)
+    desc = binding.ArcPlanDesc()
+    st = lib.rnnt_arc_plan(B, T, U, V, blank, num_states.ctypes.data, arc_begin.ctypes.data,
+                           arcs.ctypes.data if len(arcs) else None, image.ctypes.data, image_bytes,
+                           ctypes.byref(desc))
+    return st, desc
+
+
+MUTATIONS = ("src_not_below_dst", "dst_past_end", "negative_src", "label_past_vocab", "label_below_minus_one",
+             "row_t_past_end", "row_u_past_end", "score_nan", "score_inf", "no_states", "arc_begin_not_zero",
+             "arc_begin_decreasing", "image_short", "bad_shape", "bad_blank")
+
+
+def test_planner_fuzz_random_and_malformed(binding):
+    """Seeded fuzz: random valid batches of lattices must plan (every 8th one is also
+    replayed against the oracle); each planted defect must give its status code and
+    nothing else.  Stops at the first failure (the seed and the defect are in the
+    assertion message)."""
+    n_valid = 0
+    for seed in range(240):
+        rng = np.random.default_rng(10_000 + seed)
+        B = int(rng.integers(1, 4))
+        T_max, U_max, V = int(rng.integers(1, 6)), int(rng.integers(0, 4)), int(rng.integers(2, 9))
+        blank = int(rng.integers(0, V))
+        tl = rng.integers(1, T_max, size=B, endpoint=True)
+        ul = rng.integers(0, U_max, size=B, endpoint=True)
+        lattices = [W.random_arc_lattice(rng, int(tl[b]), int(ul[b]), V, int(rng.integers(1, 12)),
+                                         int(rng.integers(0, 30)), long_frac=0.3) for b in range(B)]
+        num_states = np.array([n for n, _ in lattices], np.int32)
+        counts = np.array([len(a) for _, a in lattices], np.int64)
+        arc_begin = np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
+        arcs = np.concatenate([a for _, a in lattices]) if counts.sum() else np.zeros(0, TP.ARC_DTYPE)
+        st, _ = raw_plan(binding, B, T_max, U_max, V, blank, num_states, arc_begin, arcs)
+        assert st == 0, ("valid batch refused", seed, st)
+        n_valid += 1
+        if seed % 8 == 0:
+            logits = rng.standard_normal((B, T_max, U_max + 1, V))
+            check_against_oracle(binding, lattices, logits, tl, ul, blank)
+        # one planted defect per seed
+        kind = MUTATIONS[seed % len(MUTATIONS)]
+        ns, ab, ar = num_states.copy(), arc_begin.copy(), arcs.copy()
+        T2, U2, V2, blank2, img = T_max, U_max, V, blank, None
+        expect = 10
+        have_arc = len(ar) > 0
+        i = int(rng.integers(0, len(ar))) if have_arc else 0
+        b_of_i = int(np.searchsorted(arc_begin, i, side="right") - 1) if have_arc else 0
+        if kind in ("src_not_below_dst", "dst_past_end", "negative_src", "label_past_vocab", "label_below_minus_one",
+                    "row_t_past_end", "row_u_past_end", "score_nan", "score_inf") and not have_arc:
+            kind = "no_states"
+        if kind == "src_not_below_dst":
+            ar[i]["src"] = ar[i]["dst"]
+        elif kind == "dst_past_end":
+            ar[i]["dst"] = ns[b_of_i]
+        elif kind == "negative_src":
+            ar[i]["src"] = -1
+        elif kind == "label_past_vocab":
+            ar[i]["label"] = V
+        elif kind == "label_below_minus_one":
+            ar[i]["label"] = -2
+        elif kind == "row_t_past_end":
+            ar[i]["label"], ar[i]["t"] = blank, T_max
+        elif kind == "row_u_past_end":
+            ar[i]["label"], ar[i]["u"] = blank, U_max + 1
+        elif kind == "score_nan":
+            ar[i]["score"] = np.nan
+        elif kind == "score_inf":
+            ar[i]["score"] = -np.inf
+        elif kind == "no_states":
+            ns[int(rng.integers(0, B))] = 0
+        elif kind == "arc_begin_not_zero":
+            ab[0] = 1
+        elif kind == "arc_begin_decreasing":
+            ab[int(rng.integers(1, B + 1))] = -1
+        elif kind == "image_short":
+            img, expect = 255, 6
+        elif kind == "bad_shape":
+            T2, expect = 0, 2
+        elif kind == "bad_blank":
+            blank2, expect = V, 3
+        st, _ = raw_plan(binding, B, T2, U2, V2, blank2, ns, ab, ar, image_bytes=img)
+        assert st == expect, ("defect", kind, "seed", seed, "status", st, "expected", expect)
+    assert n_valid == 240

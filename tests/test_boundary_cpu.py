@@ -45,7 +45,8 @@ def test_every_declared_symbol_is_exported(lib):
 def test_status_strings_and_version(lib):
     from paper_2303_10384_amd import binding
     for code in range(11):
-        assert binding.status_string(code)
+        assert binding.status_string(code) and binding.status_string(code) != "unknown status"
+    assert binding.status_string(11) == "unknown status"
     assert binding.status_string(0) == "ok"
     assert "gfx950" in binding.version()
 
