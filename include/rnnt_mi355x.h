@@ -19,7 +19,8 @@
  *
  * Conventions shared by every entry point
  *   - All pointers are DEVICE pointers unless a comment says otherwise, and
- *     belong to the caller.  The library keeps no state between calls and
+ *     belong to the caller.  The library keeps no state between calls (apart
+ *     from the per-GPU address of rnnt_loss_noalloc's static scratch) and
  *     never synchronises the stream: work is queued on `stream` and the call
  *     returns RNNT_OK before the results exist.
  *   - logits / grad are dense row-major (B, T_max, U_max+1, V), V innermost,
@@ -60,8 +61,10 @@ typedef enum {
   RNNT_ERR_HIP = 8,          /* a HIP runtime call failed (launch, allocation)   */
   RNNT_ERR_UNSUPPORTED = 9,  /* shape outside what this build handles (U_max+1 > 1024,
                                 or an arc-list lattice beyond the sweep's limits)   */
-  RNNT_ERR_BAD_LATTICE = 10  /* an arc list that breaks the numbering rules of
+  RNNT_ERR_BAD_LATTICE = 10, /* an arc list that breaks the numbering rules of
                                 rnnt_arc_plan, or a plan that does not match      */
+  RNNT_ERR_SCRATCH = 11      /* rnnt_loss_noalloc: the shape needs more workspace
+                                than the static scratch holds                     */
 } rnnt_status_t;
 
 typedef enum {
@@ -124,6 +127,33 @@ rnnt_status_t rnnt_loss(const void* logits, rnnt_shape_t shape, const int32_t* l
                         const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
                         rnnt_variant_t variant, float* loss_out, void* grad_out, void* workspace,
                         size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of the static device scratch of rnnt_loss_noalloc: one array of this
+ * size on every GPU the library runs on, held until the process ends. */
+#define RNNT_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/*
+ * rnnt_loss for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments (no workspace), kernels and results as rnnt_loss; the workspace is
+ * the library's static device array of RNNT_NOALLOC_SCRATCH_BYTES bytes on the
+ * GPU of `stream`.  No call allocates or frees memory (hipMalloc, hipFree,
+ * stream-ordered or library allocations); the first call on a GPU looks up the
+ * array's device address (hipGetSymbolAddress) and keeps it for later calls.
+ *   - A shape whose workspace (rnnt_loss_workspace_bytes) exceeds the array
+ *     returns RNNT_ERR_SCRATCH, checked on the host before any HIP call; the
+ *     bpe-sized batch (B = 32, T_max = 250, U_max = 80) needs about 49 MB.
+ *   - Every call on one GPU shares that GPU's array, which keeps the last
+ *     call's contents.  Nothing in it needs to start at zero (each call writes
+ *     every word it reads before reading it).  Calls that overlap in time on
+ *     one GPU (other streams, other host threads) race on the array: order
+ *     them on one stream or serialise them.
+ *   - RNNT_ERR_HIP if the stream's device cannot be found or the address
+ *     lookup fails.
+ */
+rnnt_status_t rnnt_loss_noalloc(const void* logits, rnnt_shape_t shape, const int32_t* labels,
+                                const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
+                                rnnt_variant_t variant, float* loss_out, void* grad_out, hipStream_t stream);
 
 /*
  * rnnt_loss that also records timing events on `stream`: events[0] before the

@@ -7,11 +7,11 @@ lattices, and the loss over any lattice given as an arc list); this package is
 the thin Python binding.
 """
 from .binding import (ArcPlan, RNNTError, arc_loss, arc_loss_workspace_bytes, arc_plan, lattice_scores,  # noqa: F401
-                      load_library, log_softmax_gather, loss_workspace_bytes, rnnt_loss, status_string, version,
-                      viterbi_align, viterbi_workspace_bytes)
+                      load_library, log_softmax_gather, loss_workspace_bytes, rnnt_loss, rnnt_loss_noalloc, status_string,
+                      version, viterbi_align, viterbi_workspace_bytes)
 from . import topologies  # noqa: F401
 from .autograd import RNNTLoss, rnnt_loss_autograd  # noqa: F401
 
-__all__ = ["rnnt_loss", "log_softmax_gather", "lattice_scores", "loss_workspace_bytes", "RNNTLoss",
+__all__ = ["rnnt_loss", "rnnt_loss_noalloc", "log_softmax_gather", "lattice_scores", "loss_workspace_bytes", "RNNTLoss",
            "rnnt_loss_autograd", "RNNTError", "load_library", "status_string", "version", "viterbi_align",
            "viterbi_workspace_bytes", "arc_plan", "arc_loss", "arc_loss_workspace_bytes", "ArcPlan", "topologies"]

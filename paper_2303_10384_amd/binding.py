@@ -15,8 +15,10 @@ RNNT_OK = 0
 STATUS_NAMES = {
     0: "RNNT_OK", 1: "RNNT_ERR_NULL_PTR", 2: "RNNT_ERR_BAD_SHAPE", 3: "RNNT_ERR_BAD_BLANK",
     4: "RNNT_ERR_BAD_DTYPE", 5: "RNNT_ERR_BAD_VARIANT", 6: "RNNT_ERR_WORKSPACE", 7: "RNNT_ERR_ALIGNMENT",
-    8: "RNNT_ERR_HIP", 9: "RNNT_ERR_UNSUPPORTED", 10: "RNNT_ERR_BAD_LATTICE",
+    8: "RNNT_ERR_HIP", 9: "RNNT_ERR_UNSUPPORTED", 10: "RNNT_ERR_BAD_LATTICE", 11: "RNNT_ERR_SCRATCH",
 }
+# bytes of rnnt_loss_noalloc's static device scratch (RNNT_NOALLOC_SCRATCH_BYTES)
+NOALLOC_SCRATCH_BYTES = 64 << 20
 VARIANTS = {"rnnt": 0, "wrnnt": 1, "wrnnt_allow_ignore": 2}
 DTYPE_F32, DTYPE_BF16, DTYPE_F16 = 0, 1, 2
 
@@ -24,7 +26,7 @@ DTYPE_F32, DTYPE_BF16, DTYPE_F16 = 0, 1, 2
 EXPORTED = ("rnnt_loss_workspace_bytes", "rnnt_loss", "rnnt_loss_timed", "rnnt_log_softmax_gather", "rnnt_lattice_workspace_bytes",
             "rnnt_lattice_scores", "rnnt_status_string", "rnnt_version", "rnnt_viterbi_workspace_bytes", "rnnt_viterbi",
             "rnnt_viterbi_timed", "rnnt_arc_plan_bytes_bound", "rnnt_arc_plan", "rnnt_arc_loss_workspace_bytes",
-            "rnnt_arc_loss", "rnnt_arc_loss_timed")
+            "rnnt_arc_loss", "rnnt_arc_loss_timed", "rnnt_loss_noalloc")
 
 
 class Shape(ctypes.Structure):
@@ -68,6 +70,8 @@ def load_library():
     lib.rnnt_loss.restype = ctypes.c_int
     lib.rnnt_loss_timed.argtypes = [vp, Shape, vp, vp, vp, i32, ctypes.c_int, vp, vp, vp, sz, vp, vp]
     lib.rnnt_loss_timed.restype = ctypes.c_int
+    lib.rnnt_loss_noalloc.argtypes = [vp, Shape, vp, vp, vp, i32, ctypes.c_int, vp, vp, vp]
+    lib.rnnt_loss_noalloc.restype = ctypes.c_int
     lib.rnnt_log_softmax_gather.argtypes = [vp, Shape, vp, vp, vp, i32, vp, vp, vp, vp]
     lib.rnnt_log_softmax_gather.restype = ctypes.c_int
     lib.rnnt_lattice_scores.argtypes = [vp, vp, Shape, vp, vp, ctypes.c_int, vp, vp, vp, vp, vp, vp, vp, sz, vp]
@@ -195,6 +199,38 @@ def rnnt_loss(logits, labels, logit_lens, label_lens, blank=0, variant="rnnt", n
     if st != RNNT_OK:
         raise RNNTError(st, "rnnt_loss")
     return loss, grad
+
+
+def rnnt_loss_noalloc(logits, labels, logit_lens, label_lens, loss_out, grad_out=None, blank=0, variant="rnnt"):
+    """rnnt_loss with the library's static device scratch as workspace (no device allocation
+    in the library): the caller passes every output, loss_out (B,) float32 and grad_out
+    (logits' shape, the logits' dtype or float32) or None for the loss alone.  Returns
+    (loss_out, grad_out)."""
+    torch = _torch()
+    lib = load_library()
+    _check_gpu("logits", logits)
+    _check_gpu("labels", labels, torch.int32)
+    _check_gpu("logit_lens", logit_lens, torch.int32)
+    _check_gpu("label_lens", label_lens, torch.int32)
+    _check_gpu("loss_out", loss_out, torch.float32)
+    if logits.dim() != 4:
+        raise ValueError("logits must be (B, T_max, U_max+1, V)")
+    shape = shape_of(logits, None if grad_out is None else grad_out.dtype)
+    if labels.shape != (shape.B, shape.U_max) or logit_lens.shape != (shape.B,) or label_lens.shape != (shape.B,):
+        raise ValueError("labels must be (B, U_max) and the length vectors (B,)")
+    if loss_out.shape != (shape.B,):
+        raise ValueError("loss_out must be (B,)")
+    if grad_out is not None:
+        _check_gpu("grad_out", grad_out)
+        if grad_out.shape != logits.shape:
+            raise ValueError("grad_out must have the logits' shape")
+    if variant not in VARIANTS:
+        raise ValueError("variant must be one of %s" % sorted(VARIANTS))
+    st = lib.rnnt_loss_noalloc(_ptr(logits), shape, _ptr(labels), _ptr(logit_lens), _ptr(label_lens), int(blank),
+                               VARIANTS[variant], _ptr(loss_out), _ptr(grad_out), _stream_handle(logits.device))
+    if st != RNNT_OK:
+        raise RNNTError(st, "rnnt_loss_noalloc")
+    return loss_out, grad_out
 
 
 def log_softmax_gather(logits, labels, logit_lens, label_lens, blank=0):

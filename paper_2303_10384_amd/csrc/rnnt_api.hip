@@ -3,10 +3,17 @@
 // workspace carve-up, kernel selection and launches on the caller's stream.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdint>
+#include <mutex>
 
 #include "rnnt_mi355x.h"
 #include "rnnt_launch.h"
+
+// Workspace of rnnt_loss_noalloc: one copy on every GPU the library runs on.  In
+// host code this name is only a stand-in for the array; its device address is
+// looked up per GPU (noalloc_scratch below) and only that address is used.
+static __device__ __align__(256) unsigned char scratch[RNNT_NOALLOC_SCRATCH_BYTES];
 
 namespace rnnt {
 namespace {
@@ -197,6 +204,39 @@ rnnt_status_t check_loss_args(const void* logits, const rnnt_shape_t& shape, con
   return RNNT_OK;
 }
 
+// Device address of `scratch` on each GPU, looked up once per GPU with that GPU
+// current and kept until the process ends.
+constexpr int kMaxDevices = 256;
+std::atomic<void*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+rnnt_status_t noalloc_scratch(hipStream_t stream, void** out) {
+  int dev = 0;
+  if (stream == nullptr) {
+    if (hipGetDevice(&dev) != hipSuccess) return RNNT_ERR_HIP;
+  } else if (hipStreamGetDevice(stream, &dev) != hipSuccess) {
+    return RNNT_ERR_HIP;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return RNNT_ERR_HIP;
+  void* ptr = g_scratch[dev].load(std::memory_order_acquire);
+  if (ptr == nullptr) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    ptr = g_scratch[dev].load(std::memory_order_relaxed);
+    if (ptr == nullptr) {
+      int cur = 0;
+      if (hipGetDevice(&cur) != hipSuccess) return RNNT_ERR_HIP;
+      if (cur != dev && hipSetDevice(dev) != hipSuccess) return RNNT_ERR_HIP;
+      const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+      const hipError_t e_back = (cur != dev) ? hipSetDevice(cur) : hipSuccess;
+      if (e != hipSuccess || e_back != hipSuccess || ptr == nullptr) return RNNT_ERR_HIP;
+      if (reinterpret_cast<uintptr_t>(ptr) & 255u) return RNNT_ERR_HIP;
+      g_scratch[dev].store(ptr, std::memory_order_release);
+    }
+  }
+  *out = ptr;
+  return RNNT_OK;
+}
+
 }  // namespace
 }  // namespace rnnt
 
@@ -217,6 +257,8 @@ const char* rnnt_status_string(rnnt_status_t status) {
     case RNNT_ERR_HIP: return "HIP runtime error";
     case RNNT_ERR_UNSUPPORTED: return "unsupported shape (U_max + 1 > 1024, or a lattice past the sweep's limits)";
     case RNNT_ERR_BAD_LATTICE: return "arc list breaks the numbering rules, or the plan does not match the call";
+    case RNNT_ERR_SCRATCH:
+      return "the shape needs more workspace than the static scratch of rnnt_loss_noalloc (RNNT_NOALLOC_SCRATCH_BYTES)";
   }
   return "unknown status";
 }
@@ -340,6 +382,24 @@ rnnt_status_t rnnt_loss(const void* logits, rnnt_shape_t shape, const int32_t* l
                         size_t workspace_bytes, hipStream_t stream) {
   return rnnt_loss_timed(logits, shape, labels, logit_lens, label_lens, blank, variant, loss_out, grad_out,
                          workspace, workspace_bytes, stream, nullptr);
+}
+
+rnnt_status_t rnnt_loss_noalloc(const void* logits, rnnt_shape_t shape, const int32_t* labels,
+                                const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
+                                rnnt_variant_t variant, float* loss_out, void* grad_out, hipStream_t stream) {
+  // every host check first: argument errors and a shape too large for the
+  // scratch return before any HIP call
+  const rnnt_status_t st = check_loss_args(logits, shape, labels, logit_lens, label_lens, blank, variant, loss_out,
+                                           grad_out);
+  if (st != RNNT_OK) return st;
+  const size_t need = make_layout(shape, true).total;
+  if (need > RNNT_NOALLOC_SCRATCH_BYTES) return RNNT_ERR_SCRATCH;
+  void* ws = nullptr;
+  const rnnt_status_t sst = noalloc_scratch(stream, &ws);
+  if (sst != RNNT_OK) return sst;
+  // a non-null workspace of sufficient size: rnnt_loss_timed allocates nothing
+  return rnnt_loss_timed(logits, shape, labels, logit_lens, label_lens, blank, variant, loss_out, grad_out, ws,
+                         RNNT_NOALLOC_SCRATCH_BYTES, stream, nullptr);
 }
 
 size_t rnnt_viterbi_workspace_bytes(rnnt_shape_t shape) {

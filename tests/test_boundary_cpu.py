@@ -32,7 +32,8 @@ def test_header_declares_the_documented_entry_points():
                             "rnnt_lattice_workspace_bytes", "rnnt_lattice_scores", "rnnt_status_string",
                             "rnnt_version", "rnnt_viterbi_workspace_bytes", "rnnt_viterbi",
                             "rnnt_viterbi_timed", "rnnt_arc_plan_bytes_bound", "rnnt_arc_plan",
-                            "rnnt_arc_loss_workspace_bytes", "rnnt_arc_loss", "rnnt_arc_loss_timed"])
+                            "rnnt_arc_loss_workspace_bytes", "rnnt_arc_loss", "rnnt_arc_loss_timed",
+                            "rnnt_loss_noalloc"])
 
 
 def test_every_declared_symbol_is_exported(lib):
@@ -44,9 +45,9 @@ def test_every_declared_symbol_is_exported(lib):
 
 def test_status_strings_and_version(lib):
     from paper_2303_10384_amd import binding
-    for code in range(11):
+    for code in range(12):
         assert binding.status_string(code) and binding.status_string(code) != "unknown status"
-    assert binding.status_string(11) == "unknown status"
+    assert binding.status_string(12) == "unknown status"
     assert binding.status_string(0) == "ok"
     assert "gfx950" in binding.version()
 
@@ -114,6 +115,40 @@ def test_rnnt_loss_host_errors(lib):
     need = lib.rnnt_loss_workspace_bytes(shape())
     assert call_loss(lib, shape(), ws=FAKE, ws_bytes=need - 1) == 6
     assert call_loss(lib, shape(), ws=FAKE + 16, ws_bytes=need) == 7
+
+
+def call_noalloc(lib, sh, logits=FAKE, labels=FAKE, tl=FAKE, ul=FAKE, blank=0, variant=0, loss=FAKE, grad=FAKE):
+    vp = ctypes.c_void_p
+    return lib.rnnt_loss_noalloc(vp(logits), sh, vp(labels), vp(tl), vp(ul), blank, variant, vp(loss), vp(grad),
+                                 vp(0))
+
+
+def test_noalloc_scratch_size_matches_header():
+    from paper_2303_10384_amd import binding
+    m = re.search(r"#define RNNT_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", open(HEADER).read())
+    assert m and int(m.group(1)) << int(m.group(2)) == binding.NOALLOC_SCRATCH_BYTES
+
+
+def test_noalloc_host_errors(lib):
+    # every check below returns before any HIP call (there is no device here)
+    from paper_2303_10384_amd import binding
+    assert call_noalloc(lib, shape(B=0)) == 2
+    assert call_noalloc(lib, shape(dt=3)) == 4
+    assert call_noalloc(lib, shape(), logits=0) == 1
+    assert call_noalloc(lib, shape(), loss=0) == 1
+    assert call_noalloc(lib, shape(), blank=7) == 3
+    assert call_noalloc(lib, shape(), variant=3) == 5
+    assert call_noalloc(lib, shape(), grad=FAKE + 8) == 7
+    assert call_noalloc(lib, shape(U=1024)) == 9
+    # the largest batch of bpe rows that fits, and one utterance more
+    cap = binding.NOALLOC_SCRATCH_BYTES
+    assert lib.rnnt_loss_workspace_bytes(shape(32, 250, 80, 1025)) <= cap
+    B = 32
+    while lib.rnnt_loss_workspace_bytes(shape(B + 1, 250, 80, 1025)) <= cap:
+        B += 1
+    assert call_noalloc(lib, shape(B + 1, 250, 80, 1025)) == 11
+    assert call_noalloc(lib, shape(64, 500, 150, 1025, dt=1)) == 11  # the large bf16 batch needs ~0.4 GB
+    assert "static scratch" in binding.status_string(11)
 
 
 def test_other_entry_points_host_errors(lib):
