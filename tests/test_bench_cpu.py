@@ -35,6 +35,19 @@ def test_algorithmic_bytes_of_the_bpe_workload():
     assert ab2["k3_grad"] == r_valid * 1025 * 2 + 648000 * 1025 * 4 + 648000 * 16
 
 
+def test_step_times_median_and_mean():
+    class Events:  # events are plain times in ms here
+        @staticmethod
+        def elapsed_ms(a, b):
+            return b - a
+    # four steps of 1.0, 1.2, 5.0 (an outlier) and 1.1 ms, back to back
+    starts, spans = [0.0, 1.0, 2.2, 7.2], [1.0, 1.2, 5.0, 1.1]
+    events = [[t, t + 0.3, t + d] for t, d in zip(starts, spans)]
+    median, mean = bench.step_times(Events, events, 2)
+    assert abs(median - 1.15) < 1e-12
+    assert abs(mean - 8.3 / 4) < 1e-12
+
+
 def test_cpu_baseline_reports_pool_and_single_core_rates():
     w = WORKLOADS["tiny"]
     tl, ul, labels = make_lengths_labels(w)
@@ -42,6 +55,8 @@ def test_cpu_baseline_reports_pool_and_single_core_rates():
         cb = bench.cpu_baseline(w, tl, ul, labels, budget_s=0.2, mode=mode)
         assert cb["kind"] == "oracle" and cb["unit"] == "joint-logit elements/s"
         assert cb["value"] > 0 and cb["single_core_value"] > 0 and 1 <= cb["cores"] <= 16
+        assert cb["cores_available"] == len(os.sched_getaffinity(0))
+        assert "freshly drawn" in cb["sample"]
         # the pool's rate cannot exceed its workers' summed single-core rates
         assert cb["value"] <= cb["single_core_value"] * cb["cores"] * 1.5
 
