@@ -40,8 +40,8 @@ rnnt_status_t check_shape(const rnnt_shape_t& s) {
   return RNNT_OK;
 }
 
-// Workspace, all pieces 256-byte aligned (C = B * (T_max+U_max) * (U_max+1)
-// anti-diagonal cells, S = B * (T_max+U_max+1) * u_pad score cells, u_pad =
+// Workspace, all pieces 256-byte aligned (C = B * T_max * (U_max+1) lattice
+// cells, one per logits row; S = B * (T_max+U_max+1) * u_pad score cells, u_pad =
 // 64 * units per lane of the lattice sweep):
 //   rowinfo  B*T_max*(U_max+1) RowInfo        (rnnt_loss)
 //   lp2      C double2 {lp_blank, lp_label}    (rnnt_loss)
@@ -57,7 +57,7 @@ struct Layout {
 Layout make_layout(const rnnt_shape_t& s, bool with_populate) {
   const size_t U1 = static_cast<size_t>(s.U_max) + 1;
   const size_t rows = static_cast<size_t>(s.B) * s.T_max * U1;
-  const size_t cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max) * U1;
+  const size_t cells = static_cast<size_t>(s.B) * s.T_max * U1;
   const size_t u_pad = 64 * static_cast<size_t>(units_per_lane(s.U_max + 1));
   const size_t score_cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max + 1) * u_pad;
   Layout L{};
@@ -90,7 +90,7 @@ struct ViterbiLayout {
 
 ViterbiLayout make_viterbi_layout(const rnnt_shape_t& s) {
   const size_t U1 = static_cast<size_t>(s.U_max) + 1;
-  const size_t cells = static_cast<size_t>(s.B) * (s.T_max + s.U_max) * U1;
+  const size_t cells = static_cast<size_t>(s.B) * s.T_max * U1;
   const size_t words = static_cast<size_t>(s.B) * (s.T_max + s.U_max + 1) * units_per_lane(s.U_max + 1);
   ViterbiLayout L{};
   size_t o = 0;

@@ -9,22 +9,21 @@
 //
 // Three output forms (OUT):
 //  * kK1Lattice (the fused loss): arc weights in log2 units, stored as
-//    {lp_blank, lp_label} pairs by anti-diagonal (cell (t, u) of utterance b at
-//    (b*(T_max+U_max) + t+u)*(U_max+1) + u), where the lattice kernel reads a
-//    diagonal as one contiguous run; absent arcs (the label arc of the top row,
-//    the blank arcs of the last frame below the top row) carry kNoArc; plus
-//    lse * log2(e) as float32 at the same index.
+//    {lp_blank, lp_label} pairs per row, (B, T_max, U_max+1) like the logits'
+//    rows; absent arcs (the label arc of the top row, the blank arcs of the last
+//    frame below the top row) carry kNoArc; plus lse * log2(e) as float32 at the
+//    same index.
 //  * kK1Dense: natural-log lse / lp_blank / lp_label, (B, T_max, U_max+1)
 //    float64 (the populate step on its own);
 //  * kK1Rows: lse * log2(e) per row, (B, T_max, U_max+1) float64, and no
 //    labels read (the loss over arc-list lattices, whose arcs select their own
 //    labels).
 //
-// Mapping: a block owns up to `rows_per_block` consecutive units u of one
-// anti-diagonal d of one utterance; blocks are numbered so that consecutive
-// diagonals of an utterance run on the same XCD (dispatch deals blocks to the 8
-// XCDs round robin), where rows (t, u) and (t, u+1), adjacent in memory but on
-// diagonals d and d+1, share the L2 copy of the line between them.  A group of
+// Mapping: a block owns up to `rows_per_block` consecutive units u of one frame
+// t of one utterance, so its rows are consecutive in memory; blocks are numbered
+// so that runs of consecutive frames of an utterance go to the same XCD
+// (dispatch deals blocks to the 8 XCDs round robin), where the lines shared by
+// neighbouring blocks' boundary rows meet in one L2.  A group of
 // G lanes reads one row as aligned 16-byte chunks.  The chunks entirely inside
 // the row ("interior") are spread NB per lane (G and NB picked from V so that
 // G*NB just covers them) and need no element masks: a lane with no chunk of its
@@ -37,7 +36,8 @@
 // pairwise float32 tree.
 //
 // Fast path (every block whose rows lie in whole chunks): the loads of a
-// group's next row are issued before its current row is reduced, as buffer
+// group's first row are issued before the block stages its labels in LDS, and
+// the loads of its next row before its current row is reduced, as buffer
 // loads on a per-block buffer resource; a row past the block's last gets
 // offsets past the buffer's end (zeros, no memory access), so every load is
 // issued unconditionally and the compiler's wait counts stay exact.  Results
@@ -69,10 +69,10 @@ struct PopulateParams {
   const int32_t* logit_lens;
   const int32_t* label_lens;
   int64_t n_elem;          // B * T_max * (U_max+1) * V
-  int32_t n_ublk;          // blocks per anti-diagonal
+  int32_t n_ublk;          // blocks per frame
   int32_t rows_per_block;  // consecutive units u per block (<= kMaxRowsPerBlock)
   // lattice form
-  double2* lp2;            // (B, T_max+U_max, U_max+1) {lp_blank, lp_label} * log2(e)
+  double2* lp2;            // (B, T_max, U_max+1) {lp_blank, lp_label} * log2(e)
   float* lse2;             // same index: lse * log2(e)
   // dense form
   double* lse_out;         // (B, T_max, U_max+1) or null
@@ -145,10 +145,20 @@ __device__ __forceinline__ BndSlot bnd_slot(const RowGeom& g, int V, int e) {
   return b;
 }
 
-// Issue every load of one row (all lanes, unconditionally).  Offsets are
-// unsigned: a row that is not live starts at kOutOfRange, and every offset
-// derived from it stays at or above 2^31, past the buffer.
-template <typename T, int G, int NB>
+// The load of z[y_{u+1}] of one row (same address in every lane of the group).
+template <typename T>
+__device__ __forceinline__ float issue_label_elem(__amdgpu_buffer_rsrc_t rsrc, const RowGeom& g, int V) {
+  const uint32_t rb = g.live ? static_cast<uint32_t>(g.off0) : static_cast<uint32_t>(kOutOfRange);
+  const bool y_ok = g.y >= 0 && g.y < V;
+  const uint32_t oy = y_ok ? rb + static_cast<uint32_t>(g.mis + g.y) * sizeof(T) : static_cast<uint32_t>(kOutOfRange);
+  return buffer_load_elem<T>(rsrc, static_cast<int>(oy));
+}
+
+// Issue every load of one row (all lanes, unconditionally); WITH_LABEL false
+// leaves z[y] for a later issue_label_elem.  Offsets are unsigned: a row that
+// is not live starts at kOutOfRange, and every offset derived from it stays at
+// or above 2^31, past the buffer.
+template <typename T, int G, int NB, bool WITH_LABEL = true>
 __device__ __forceinline__ void issue_row(__amdgpu_buffer_rsrc_t rsrc, const RowGeom& g, int V, int blank, int lg,
                                           RowRegs<T, G, NB>& R) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
@@ -174,9 +184,7 @@ __device__ __forceinline__ void issue_row(__amdgpu_buffer_rsrc_t rsrc, const Row
   }
   // the same address in every lane of the group: one request, a line the chunk loads bring in
   R.zb = buffer_load_elem<T>(rsrc, static_cast<int>(rb + static_cast<uint32_t>(g.mis + blank) * S));
-  const bool y_ok = g.y >= 0 && g.y < V;
-  const uint32_t oy = y_ok ? rb + static_cast<uint32_t>(g.mis + g.y) * S : static_cast<uint32_t>(kOutOfRange);
-  R.zy = buffer_load_elem<T>(rsrc, static_cast<int>(oy));
+  if (WITH_LABEL) R.zy = issue_label_elem<T>(rsrc, g, V);
 }
 
 // (group max, group sum of exp(z - max)) of a row from its registers, in every lane.
@@ -295,24 +303,22 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
 
   if (OUT == kK1Rows && p.clear_flags && blockIdx.x == 0)
     for (int i = threadIdx.x; i < p.B; i += blockDim.x) p.clear_flags[i] = 0;
-  const int ND = p.T_max + p.U_max;  // anti-diagonals per utterance
-  // block order: runs of kXcdRun consecutive (b, d, ublk) are dealt to the XCDs in
+  // block order: runs of kXcdRun consecutive (b, t, ublk) are dealt to the XCDs in
   // turn; XCD x holds physical blocks x, x+8, ..., and its k-th block is element
   // k % kXcdRun of its (k / kXcdRun)-th run
-  const int64_t n_blocks = static_cast<int64_t>(p.B) * ND * p.n_ublk;
+  const int64_t n_blocks = static_cast<int64_t>(p.B) * p.T_max * p.n_ublk;
   const int64_t kx = blockIdx.x / kXcds;
   const int64_t lb = ((kx / kXcdRun) * kXcds + blockIdx.x % kXcds) * kXcdRun + kx % kXcdRun;
   if (lb >= n_blocks) return;
-  const int diag = static_cast<int>(lb / p.n_ublk);  // b * ND + d
-  const int ublk = static_cast<int>(lb - static_cast<int64_t>(diag) * p.n_ublk);
-  const int b = diag / ND;
-  const int d = diag - b * ND;
+  const int64_t frame = lb / p.n_ublk;  // b * T_max + t
+  const int ublk = static_cast<int>(lb - frame * p.n_ublk);
+  const int b = static_cast<int>(frame / p.T_max);
+  const int t = static_cast<int>(frame - static_cast<int64_t>(b) * p.T_max);
   const int Tb = p.logit_lens[b];
   const int Ub = p.label_lens[b];
-  if (Tb < 1 || Tb > p.T_max || Ub < 0 || Ub > p.U_max) return;
-  const int u_first = ublk * p.rows_per_block;
-  const int u_lo = max(u_first, d - (Tb - 1));  // t = d - u <= T_b - 1
-  const int u_hi = min(u_first + p.rows_per_block, min(d, Ub) + 1);
+  if (Tb < 1 || Tb > p.T_max || Ub < 0 || Ub > p.U_max || t >= Tb) return;
+  const int u_lo = ublk * p.rows_per_block;
+  const int u_hi = min(u_lo + p.rows_per_block, Ub + 1);
   const int U1 = p.U_max + 1;
   if (u_lo >= u_hi) return;
   const int n_rows = u_hi - u_lo;
@@ -320,22 +326,21 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   const int lg = threadIdx.x % G;  // lane inside the row group
   const int grp = threadIdx.x / G;
   // the block's labels go through LDS, so no label load waits inside the row loop
-  for (int i = threadIdx.x; i < n_rows; i += blockDim.x) {
-    const int u = u_lo + i;
-    s_label[i] = (OUT != kK1Rows && u < Ub) ? p.labels[static_cast<int64_t>(b) * p.U_max + u] : kNoLabel;
-  }
-  __syncthreads();
+  auto stage_labels = [&]() {
+    for (int i = threadIdx.x; i < n_rows; i += blockDim.x) {
+      const int u = u_lo + i;
+      s_label[i] = (OUT != kK1Rows && u < Ub) ? p.labels[static_cast<int64_t>(b) * p.U_max + u] : kNoLabel;
+    }
+    __syncthreads();
+  };
 
   const T* __restrict__ base = static_cast<const T*>(p.logits);
   const int64_t full_chunks = p.n_elem / EPC;
-  // row j of the block is unit u_lo + j; rows of a diagonal lie U_max rows apart,
-  // the first (u_lo) at the highest address
-  const int64_t row_lo = (static_cast<int64_t>(b) * p.T_max + (d - u_lo)) * U1 + u_lo;
+  // row j of the block is unit u_lo + j, V elements after row j - 1
+  const int64_t row_lo = frame * U1 + u_lo;
   const int64_t e_first = row_lo * p.V;
-  const int64_t row_step = static_cast<int64_t>(p.U_max) * p.V;  // elements between consecutive rows
-  const int64_t c_end = (e_first + p.V + EPC - 1) / EPC;
-  const int64_t e_base = e_first - (n_rows - 1) * row_step;  // the lowest row (u_hi - 1)
-  const int64_t c_base = e_base / EPC;
+  const int64_t c_base = e_first / EPC;
+  const int64_t c_end = (e_first + static_cast<int64_t>(n_rows) * p.V + EPC - 1) / EPC;
   const int n_iter = (n_rows + GROUPS - 1) / GROUPS;
 
   if (FAST && c_end <= full_chunks) {
@@ -343,17 +348,17 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
         make_buffer(reinterpret_cast<const uint4*>(base) + c_base, (c_end - c_base) * 16);
     // element offset of row j from the block's first chunk (fits 32 bits: the span is checked)
     const int e_rel0 = static_cast<int>(e_first - c_base * EPC);
-    const int step = static_cast<int>(row_step);
-    auto geom = [&](int it) {
+    // the row's geometry; its label comes from LDS once the labels are staged
+    auto geom = [&](int it, bool with_label) {
       RowGeom g;
       const int j = it * GROUPS + grp;
       g.live = j < n_rows;
       g.j = g.live ? j : 0;
-      const int e_rel = e_rel0 - g.j * step;
+      const int e_rel = e_rel0 + g.j * p.V;
       g.mis = e_rel & (EPC - 1);
       g.nch = (g.mis + p.V + EPC - 1) / EPC;
       g.off0 = (e_rel - g.mis) * static_cast<int>(sizeof(T));
-      g.y = s_label[g.j];
+      g.y = with_label ? s_label[g.j] : kNoLabel;
       return g;
     };
     auto finish = [&](const RowRegs<T, G, NB>& R, const RowGeom& g) {
@@ -367,28 +372,34 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
         s_zy[g.j] = R.zy;
       }
     };
-    // two register sets in turn (a copy between them would wait for the loads in flight)
-    RowGeom g0 = geom(0), g1;
+    // two register sets in turn (a copy between them would wait for the loads in flight);
+    // the first row's chunks go out before the labels are staged, its z[y] after
+    RowGeom g0 = geom(0, false), g1;
     RowRegs<T, G, NB> R0, R1;
-    issue_row<T, G, NB>(rsrc, g0, p.V, p.blank, lg, R0);
+    issue_row<T, G, NB, false>(rsrc, g0, p.V, p.blank, lg, R0);
+    __builtin_amdgcn_sched_barrier(0);
+    stage_labels();
+    g0.y = s_label[g0.j];
+    R0.zy = issue_label_elem<T>(rsrc, g0, p.V);
     for (int it = 0; it < n_iter; it += 2) {
-      g1 = geom(it + 1);  // past the block's rows: not live, no memory access
+      g1 = geom(it + 1, true);  // past the block's rows: not live, no memory access
       issue_row<T, G, NB>(rsrc, g1, p.V, p.blank, lg, R1);
       __builtin_amdgcn_sched_barrier(0);  // the next row's loads go out before this row is reduced
       finish(R0, g0);
-      g0 = geom(it + 2);
+      g0 = geom(it + 2, true);
       issue_row<T, G, NB>(rsrc, g0, p.V, p.blank, lg, R0);
       __builtin_amdgcn_sched_barrier(0);
       finish(R1, g1);
     }
   } else {
+    stage_labels();
     // all lanes of a wave stay in the loop (the group reductions use every lane);
     // a group past the block's last row computes a row it does not keep
     for (int it = 0; it < n_iter; ++it) {
       const int j_raw = it * GROUPS + grp;
       const bool live = j_raw < n_rows;
       const int j = live ? j_raw : 0;
-      const int64_t e0 = e_first - j * row_step;
+      const int64_t e0 = e_first + static_cast<int64_t>(j) * p.V;
       const int64_t c0 = e0 / EPC;
       const int mis = static_cast<int>(e0 - c0 * EPC);
       const int nch = (mis + p.V + EPC - 1) / EPC;
@@ -410,27 +421,25 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   __syncthreads();
 
   // one thread per row: lse = max + ln(sum), the arc weights in float64, and the
-  // block's results leave in one pass (a contiguous run in the lattice form)
+  // block's results leave in one pass (a contiguous run of rows)
   for (int j = threadIdx.x; j < n_rows; j += blockDim.x) {
     const int u = u_lo + j;
-    const int t = d - u;
+    const int64_t row = row_lo + j;
     const int y = s_label[j];
     const bool y_ok = y >= 0 && y < p.V;
     const double lse = static_cast<double>(s_max[j]) + log(s_sum[j]);
     const double lpb = static_cast<double>(s_zb[j]) - lse;
     const double lpl = (u < Ub) ? (y_ok ? static_cast<double>(s_zy[j]) - lse : __builtin_nan("")) : -__builtin_inf();
     if (OUT == kK1Lattice) {
-      const int64_t sc = static_cast<int64_t>(diag) * U1 + u;
       const bool blank_arc = (t < Tb - 1) || (u == Ub);  // absent: last frame below the top row
       double2 w;
       w.x = blank_arc ? clamp_no_arc(lpb * kLog2eD) : kNoArc;
       w.y = (u < Ub) ? clamp_no_arc(lpl * kLog2eD) : kNoArc;
-      p.lp2[sc] = w;
-      p.lse2[sc] = static_cast<float>(lse * kLog2eD);
+      p.lp2[row] = w;
+      p.lse2[row] = static_cast<float>(lse * kLog2eD);
     } else if (OUT == kK1Rows) {
-      p.lse2_rows[row_lo - static_cast<int64_t>(j) * p.U_max] = lse * kLog2eD;
+      p.lse2_rows[row] = lse * kLog2eD;
     } else {
-      const int64_t row = row_lo - static_cast<int64_t>(j) * p.U_max;
       if (p.lse_out) p.lse_out[row] = lse;
       p.lp_blank_out[row] = lpb;
       p.lp_label_out[row] = lpl;

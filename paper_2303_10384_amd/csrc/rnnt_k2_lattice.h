@@ -18,12 +18,14 @@
 // value with the neighbouring lane (a DPP whole-wave shift).  The forward and
 // backward waves of an utterance run concurrently, each a one-wavefront block of
 // its own (blockIdx.y), so that the two chains do not share a compute unit.  The weights of
-// the next PF diagonals stay in flight in registers (one contiguous run per
-// diagonal in the anti-diagonal layout of kernel 1).  No node is masked:
+// the next PF diagonals stay in flight in registers (one load per unit and
+// diagonal).  No node is masked:
 // absent arcs carry kNoArc, so a node outside the utterance accumulates only
 // kNoArc or never feeds a node inside it; weights of cells outside the
 // utterance are read from a cell clamped into it (a wave-uniform diagonal and
-// two per-lane min/max on the unit), so every value stays finite.  alpha and
+// two per-lane min/max on the unit), so every value stays finite.  Kernel 1
+// stores the weights by row, so a diagonal's cells lie U_max rows apart and a
+// 128-byte line of them serves eight consecutive diagonals.  alpha and
 // beta rows are 64*K wide, one column per lane slot, and the
 // steps past the utterance's last diagonal (or before the first) store into
 // spare rows, so every load and store goes through a wave-uniform row pointer
@@ -53,7 +55,7 @@ struct LatticeParams {
   const int32_t* labels;  // (B, U_max) or null (lattice-only entry point)
   const int32_t* logit_lens;
   const int32_t* label_lens;
-  const double2* lp2;       // kernel 1's lattice form (log2 units, by diagonal, kNoArc marks), or
+  const double2* lp2;       // kernel 1's lattice form (log2 units, (B, T_max, U_max+1), kNoArc marks), or
   const double* lp_blank;   // dense natural-log weights (B, T_max, U_max+1)
   const double* lp_label;
   double* alpha;  // (B, T_max+U_max+1, u_pad), by diagonal, log2 units; rows past D_b + 1: spare
@@ -73,8 +75,8 @@ __device__ __forceinline__ void load_cell(const LatticeParams& p, int b, int d, 
   const int dc = min(max(d, 0), D);
   const int uc = min(max(u, dc - (T - 1)), min(dc, U));
   if (!DENSE_IN) {
-    const int64_t sc = (static_cast<int64_t>(b) * (p.T_max + p.U_max) + dc) * (p.U_max + 1) + uc;
-    const double2 w = p.lp2[sc];
+    const int64_t row = (static_cast<int64_t>(b) * p.T_max + (dc - uc)) * (p.U_max + 1) + uc;
+    const double2 w = p.lp2[row];
     wb = w.x;
     wl = w.y;
   } else {
@@ -167,12 +169,12 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
   const int owner_top = U / K;  // lane owning u = U
   // weights of cell (e, u) clamped into the utterance: diagonal into [0, D], then the
   // unit into [e - (T-1), min(e, U)] (t = e - u in [0, T-1]); the row pointer is wave-uniform
-  const double2* __restrict__ w_utt = p.lp2 + static_cast<int64_t>(b) * ND * U1;
+  const double2* __restrict__ w_utt = p.lp2 + static_cast<int64_t>(b) * p.T_max * U1;
   auto load_w = [&](int e, int k, double& wb, double& wl) {
     if (!DENSE_IN) {
       const int ec = min(max(e, 0), D);
       const int uc = min(max(lane * K + k, ec - (T - 1)), min(ec, U));
-      const double2 w = w_utt[ec * U1 + uc];
+      const double2 w = w_utt[(ec - uc) * U1 + uc];  // row (t, u) = (ec - uc, uc)
       wb = w.x;
       wl = w.y;
     } else {
@@ -186,7 +188,7 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
   // weight of the closing blank, lp_blank(T-1, U)
   double w_close, w_unused;
   if (!DENSE_IN) {
-    w_close = w_utt[D * U1 + U].x;
+    w_close = w_utt[(T - 1) * U1 + U].x;
   } else {
     load_cell<true>(p, b, D, U, T, U, D, w_close, w_unused);
     w_close = to_lattice(w_close, true);
@@ -354,8 +356,9 @@ constexpr int kPostTileT = 8;  // frames per block
 // One block per (utterance, kPostTileT frames t0 .. t0+7, every unit).  Its
 // threads walk the tile's cells diagonal by diagonal (consecutive threads:
 // consecutive t, so consecutive cells of one diagonal), which makes the loads
-// of alpha, beta and the lattice form contiguous; the tile's row records are
-// one contiguous range of memory, completed by the block.
+// of alpha and beta contiguous; the tile's rows of lattice weights and of row
+// records are one contiguous range of memory each, read and completed by the
+// block.
 template <bool DENSE>
 __global__ __launch_bounds__(kPostThreads) void k2b_posteriors(PostParams p) {
   const int U1 = p.U_max + 1;
@@ -382,7 +385,7 @@ __global__ __launch_bounds__(kPostThreads) void k2b_posteriors(PostParams p) {
   }
   const double lnP2 = p.lnp2_fwd[b];
   const int64_t ab0 = static_cast<int64_t>(b) * (p.T_max + p.U_max + 1) * p.u_pad;
-  const int64_t sc0 = static_cast<int64_t>(b) * (p.T_max + p.U_max) * U1;
+
   const int n_items = kPostTileT * (kPostTileT - 1 + U1);
   for (int i = threadIdx.x; i < n_items; i += kPostThreads) {
     const int t = t0 + i % kPostTileT;
@@ -398,11 +401,10 @@ __global__ __launch_bounds__(kPostThreads) void k2b_posteriors(PostParams p) {
     double wb, wl;
     float lse2 = 0.f;
     if (!DENSE) {
-      const int64_t sc = sc0 + static_cast<int64_t>(d) * U1 + u;
-      const double2 w = p.lp2[sc];
+      const double2 w = p.lp2[r];
       wb = w.x;
       wl = w.y;
-      lse2 = p.lse2[sc];
+      lse2 = p.lse2[r];
     } else {
       wb = to_lattice(p.lp_blank[r], true);
       wl = to_lattice(u < U ? p.lp_label[r] : 0.0, u < U);

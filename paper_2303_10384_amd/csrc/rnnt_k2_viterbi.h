@@ -32,7 +32,7 @@ struct ViterbiParams {
   const int32_t* labels;  // (B, U_max)
   const int32_t* logit_lens;
   const int32_t* label_lens;
-  const double2* lp2;      // kernel 1's lattice form (log2 units, by diagonal)
+  const double2* lp2;      // kernel 1's lattice form (log2 units, (B, T_max, U_max+1))
   uint64_t* decisions;     // (B, T_max+U_max+1, K) ballot words
   float* score_out;        // (B) best path log-probability (natural log), NaN for bad data
   int32_t* label_frames;   // (B, U_max): frame of unit i+1, -1 past U_b or for bad data
@@ -87,16 +87,16 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
 
   const int D = T - 1 + U;
   const int owner_top = U / K;
-  const double2* __restrict__ w_utt = p.lp2 + static_cast<int64_t>(b) * ND * U1;
+  const double2* __restrict__ w_utt = p.lp2 + static_cast<int64_t>(b) * p.T_max * U1;
   auto load_w = [&](int e, int k, double& wb, double& wl) {
     const int ec = min(max(e, 0), D);
     const int uc = min(max(lane * K + k, ec - (T - 1)), min(ec, U));
-    const double2 w = w_utt[ec * U1 + uc];
+    const double2 w = w_utt[(ec - uc) * U1 + uc];  // row (t, u) = (ec - uc, uc)
     wb = w.x;
     wl = w.y;
   };
   uint64_t* __restrict__ dec_utt = p.decisions + static_cast<int64_t>(b) * (ND + 1) * K;
-  const double w_close = w_utt[D * U1 + U].x;
+  const double w_close = w_utt[(T - 1) * U1 + U].x;
 
   // ---------------- forward max-plus sweep ----------------
   double a[K];

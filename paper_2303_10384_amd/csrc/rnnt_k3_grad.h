@@ -192,4 +192,126 @@ __global__ __launch_bounds__(kGradThreads<Tin>) void k3_grad(GradParams p) {
   }
 }
 
+// ---- rows of at least 64 chunks ---------------------------------------------
+//
+// The 64 consecutive chunks a wavefront takes at once (a "group") then span at
+// most two rows, a and a+1, so everything that depends on the row is the same
+// across the wave: the two row records (scalar loads), whether a row is a zero
+// row, and where the corrected elements -- the blank and the label y_{u+1} of
+// each row -- fall.  Each lane picks (lse2, g_b + g_l) by the row its chunk
+// lies in, and an element costs exp2(z log2 e - lse2) * (g_b + g_l) alone.
+// The one lane whose chunk straddles the row end (if any) redoes its chunk
+// element by element under a wave-uniform branch, where an element of a zero
+// row is set to 0 whatever its logits hold (padding logits may be NaN).  The at
+// most four corrections -g_b at v = blank and -g_l at v = y_{u+1} are applied
+// by the lane owning the element, at a position known to the whole wave.
+template <typename Tin>
+constexpr int kWideMinV = kWave * ElemTraits<Tin>::kPerChunk - 1;
+
+// out[j] -= corr in lane `owner` for the wave-uniform slot js (no run-time index
+// into out: the slot is matched against each constant j)
+template <int EPC>
+__device__ __forceinline__ void fix_element(float (&out)[EPC], int lane, int owner, int js, float corr) {
+#pragma unroll
+  for (int j = 0; j < EPC; ++j)
+    if (j == js) out[j] = (lane == owner) ? out[j] - corr : out[j];
+}
+
+// The correction of column `col` of the group's row a (pos = col - va) or row b
+// (pos = V - va + col), if that element lies in the group.
+template <int EPC>
+__device__ __forceinline__ void fix_column(float (&out)[EPC], int lane, int pos, float corr) {
+  if (pos >= 0 && pos < kWave * EPC) fix_element<EPC>(out, lane, pos / EPC, pos % EPC, corr);
+}
+
+template <typename Tin, typename Tout>
+__global__ __launch_bounds__(kGradThreads<Tin>) void k3_grad_wide(GradParams p) {
+  using T = Tin;
+  constexpr int EPC = ElemTraits<T>::kPerChunk;
+  constexpr int kThreads = kGradThreads<Tin>;
+  constexpr int kTile = kGradTileChunks<Tin>;
+  constexpr int Q = kGradChunksPerThread;
+  const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kTile;
+  const int64_t e_tile = tile0 * EPC;
+  const int64_t r_tile = e_tile / p.V;
+  const int v_tile = static_cast<int>(e_tile - r_tile * p.V);
+  const int64_t n_full = p.n_elem / EPC;  // chunks wholly inside the tensor
+  if (p.n_elem % EPC != 0 && tile0 + kTile > n_full) {
+    grad_chunks_general<T, Tout, false>(p, tile0, r_tile, static_cast<uint32_t>(v_tile));
+    return;
+  }
+  const int lane = static_cast<int>(threadIdx.x) & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
+  const RowInfo* __restrict__ rows = p.rowinfo;
+
+  // group q of this wave: chunks tile0 + q*kThreads + 64*wave + lane; its first
+  // element is column va of row ra (wave-uniform)
+  int va[Q];
+  RowInfo Ra[Q], Rb[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int off = v_tile + (q * kThreads + wave * kWave) * EPC;
+    const int dr = off / p.V;
+    va[q] = off - dr * p.V;
+    const int64_t ra = min(r_tile + dr, p.n_rows - 1);  // groups past the end store nothing
+    Ra[q] = rows[ra];
+    Rb[q] = rows[min(ra + 1, p.n_rows - 1)];
+  }
+  __builtin_amdgcn_sched_barrier(0);  // all record loads issue before any of them is used
+  const int64_t tile_bytes = min<int64_t>(kTile, n_full - tile0) * 16;
+  const __amdgpu_buffer_rsrc_t rsrc = make_buffer(static_cast<const uint4*>(p.logits) + tile0, tile_bytes);
+  u32x4 raw[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int cl = q * kThreads + static_cast<int>(threadIdx.x);
+    const bool live = tile0 + cl < n_full;
+    const int v = va[q] + lane * EPC;  // column of the chunk's first element in row a (>= V: in row b)
+    const bool za = Ra[q].label == kZeroRow, zb = Rb[q].label == kZeroRow;
+    const bool zero = v >= p.V ? zb : (v + EPC > p.V ? za && zb : za);
+    raw[q] = buffer_load16<kK3StreamLoads>(rsrc, (live && !zero) ? cl * 16 : kOutOfRange);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int cl = q * kThreads + static_cast<int>(threadIdx.x);
+    const int v = va[q] + lane * EPC;
+    const int to_b = p.V - va[q];  // the group's first element of row b (>= 64*EPC: none)
+    const bool za = Ra[q].label == kZeroRow, zb = Rb[q].label == kZeroRow;
+    float out[EPC];
+    if (za && (zb || to_b >= kWave * EPC)) {  // the whole group lies in zero rows
+#pragma unroll
+      for (int j = 0; j < EPC; ++j) out[j] = 0.f;
+    } else {
+      float f[EPC];
+      ElemTraits<T>::unpack(make_uint4(raw[q].x, raw[q].y, raw[q].z, raw[q].w), f);
+      const bool in_b = v >= p.V;
+      const float lse2 = in_b ? Rb[q].lse2 : Ra[q].lse2;
+      const float occ = in_b ? Rb[q].occ_blank + Rb[q].occ_label : Ra[q].occ_blank + Ra[q].occ_label;
+#pragma unroll
+      for (int j = 0; j < EPC; ++j) out[j] = fast_exp2(fmaf(f[j], kLog2eF, -lse2)) * occ;
+      if (to_b % EPC != 0 && to_b < kWave * EPC) {  // one lane's chunk straddles the row end
+        if (v < p.V && v + EPC > p.V) {
+#pragma unroll
+          for (int j = 0; j < EPC; ++j) {
+            const bool bj = v + j >= p.V;
+            const float l2 = bj ? Rb[q].lse2 : Ra[q].lse2;
+            const float oc = bj ? Rb[q].occ_blank + Rb[q].occ_label : Ra[q].occ_blank + Ra[q].occ_label;
+            const float g = fast_exp2(fmaf(f[j], kLog2eF, -l2)) * oc;
+            out[j] = (bj ? zb : za) ? 0.f : g;
+          }
+        }
+      }
+      if (!za) {
+        fix_column<EPC>(out, lane, p.blank - va[q], Ra[q].occ_blank);
+        if (Ra[q].label >= 0) fix_column<EPC>(out, lane, Ra[q].label - va[q], Ra[q].occ_label);
+      }
+      if (!zb && to_b < kWave * EPC) {
+        fix_column<EPC>(out, lane, to_b + p.blank, Rb[q].occ_blank);
+        if (Rb[q].label >= 0) fix_column<EPC>(out, lane, to_b + Rb[q].label, Rb[q].occ_label);
+      }
+    }
+    if (tile0 + cl < n_full) store_chunk<Tout, EPC>(p.grad, (tile0 + cl) * EPC, out);
+  }
+}
+
 }  // namespace rnnt

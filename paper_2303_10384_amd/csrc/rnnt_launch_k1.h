@@ -44,8 +44,8 @@ K1Shape k1_shape(int V) {
   return best;
 }
 
-// one block per anti-diagonal, split into blocks of at most 32 units for float32
-// rows (measured faster) and kMaxRowsPerBlock units for 16-bit ones
+// one block per frame of an utterance, split into blocks of at most 32 units for
+// float32 rows and kMaxRowsPerBlock units for 16-bit ones
 void k1_blocking(PopulateParams& p, int elem_bytes) {
   const int cap = elem_bytes == 4 ? 32 : kMaxRowsPerBlock;
   p.rows_per_block = p.U_max + 1 < cap ? p.U_max + 1 : cap;
@@ -55,7 +55,7 @@ void k1_blocking(PopulateParams& p, int elem_bytes) {
 template <typename T, int G, int NB, int OUT, bool FAST>
 hipError_t launch_k1_g(PopulateParams p, hipStream_t stream) {
   k1_blocking(p, static_cast<int>(sizeof(T)));
-  const int64_t blocks = static_cast<int64_t>(p.B) * (p.T_max + p.U_max) * p.n_ublk;
+  const int64_t blocks = static_cast<int64_t>(p.B) * p.T_max * p.n_ublk;
   const int64_t runs = (blocks + kXcdRun - 1) / kXcdRun;  // whole rounds of the XCD-major numbering
   const int64_t grid = (runs + kXcds - 1) / kXcds * kXcds * kXcdRun;
   if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
@@ -75,12 +75,11 @@ hipError_t launch_k1_nb(int nb, const PopulateParams& p, hipStream_t stream) {
   }
 }
 
-// A block's rows on one diagonal lie U_max rows apart; the fast path addresses
-// them through one buffer resource with 32-bit offsets.
+// A block's rows are consecutive; the fast path addresses them through one
+// buffer resource with 32-bit offsets.
 bool k1_span_fits(PopulateParams p, int elem_bytes) {
   k1_blocking(p, elem_bytes);
-  const int64_t rows = static_cast<int64_t>(p.rows_per_block - 1) * p.U_max + 1;
-  return rows * p.V * elem_bytes + 64 < 0x7fffffffLL;
+  return static_cast<int64_t>(p.rows_per_block) * p.V * elem_bytes + 64 < 0x7fffffffLL;
 }
 
 template <typename T, int OUT>

@@ -19,6 +19,9 @@ hipError_t launch_k3(const GradParams& p, hipStream_t stream) {
   if (p.V < EPC)
     hipLaunchKernelGGL((k3_grad<Tin, Tout, true>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads<Tin>), 0,
                        stream, p);
+  else if (p.V >= kWideMinV<Tin>)
+    hipLaunchKernelGGL((k3_grad_wide<Tin, Tout>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads<Tin>), 0,
+                       stream, p);
   else
     hipLaunchKernelGGL((k3_grad<Tin, Tout, false>), dim3(static_cast<uint32_t>(blocks)), dim3(kGradThreads<Tin>), 0,
                        stream, p);

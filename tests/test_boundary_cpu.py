@@ -60,7 +60,7 @@ def shape(B=2, T=5, U=3, V=7, dt=0, gdt=None):
 def expected_workspace(B, T, U, V):
     a = lambda x: (x + 255) // 256 * 256  # noqa: E731
     rows = B * T * (U + 1)
-    cells = B * (T + U) * (U + 1)            # anti-diagonal cells
+    cells = B * T * (U + 1)                  # lattice cells, one per logits row
     K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16) if U + 1 <= 64 * k or k == 16)  # units per lane of the sweep
     score_cells = B * (T + U + 1) * 64 * K  # rows 64*K wide, plus one spare diagonal per utterance
     o = a(rows * 16)               # row records
@@ -173,7 +173,7 @@ def test_other_entry_points_host_errors(lib):
 
 def expected_viterbi_workspace(B, T, U, V):
     a = lambda x: (x + 255) // 256 * 256  # noqa: E731
-    cells = B * (T + U) * (U + 1)
+    cells = B * T * (U + 1)
     K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16) if U + 1 <= 64 * k or k == 16)
     o = a(cells * 16)                    # {lp_blank, lp_label}
     o = a(o + cells * 4)                 # lse * log2 e

@@ -31,14 +31,12 @@ def k1_shape(V, epc):
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
 def test_populate_kernel_addresses(B, T, U, V, dt):
     epc = EPC[dt]
+    esz = {"f32": 4, "bf16": 2, "f16": 2}[dt]
     n_elem = B * T * (U + 1) * V
     G, NB, fast = k1_shape(V, epc)
-    rows_per_block = min(U + 1, 32 if dt == "f32" else 256)  # units of a diagonal per block
+    rows_per_block = min(U + 1, 32 if dt == "f32" else 256)  # consecutive units of one frame per block
     n_ublk = -(-(U + 1) // rows_per_block)
-    ND = T + U
-    DPB = 1  # anti-diagonals per block
-    n_dblk = -(-ND // DPB)
-    blocks = B * n_dblk * n_ublk
+    blocks = B * T * n_ublk
     run = 16  # consecutive blocks per XCD turn
     grid = -(-(-(-blocks // run)) // 8) * 8 * run
     assert grid < 2**31
@@ -50,14 +48,10 @@ def test_populate_kernel_addresses(B, T, U, V, dt):
     lb = ((k // run) * 8 + i % 8) * run + k % run
     kept = np.sort(lb[lb < blocks])
     assert np.array_equal(kept, np.arange(blocks))
-    span_rows = (DPB - 1) * (U + 1) + (rows_per_block - 1) * U + 1
-    span_fits = span_rows * V * {"f32": 4, "bf16": 2, "f16": 2}[dt] + 64 < 0x7fffffff
-    fast = fast and span_fits
-    # every (b, d, u) a block can reach with full lengths: t = d - u in [0, T), u in [0, U]
-    b, d, u = np.meshgrid(np.arange(B), np.arange(ND), np.arange(U + 1), indexing="ij")
-    t = d - u
-    ok = (t >= 0) & (t < T)
-    b, d, u, t = b[ok], d[ok], u[ok], t[ok]
+    fast = fast and rows_per_block * V * esz + 64 < 0x7fffffff
+    # every row a block can reach with full lengths (t < T, u <= U)
+    b, t, u = np.meshgrid(np.arange(B), np.arange(T), np.arange(U + 1), indexing="ij")
+    b, t, u = b.ravel(), t.ravel(), u.ravel()
     row = (b.astype(np.int64) * T + t) * (U + 1) + u
     e0 = row * V
     c0 = e0 // epc
@@ -78,44 +72,26 @@ def test_populate_kernel_addresses(B, T, U, V, dt):
     # only rows reaching into the tensor's final partial chunk read element-wise
     assert np.all((e0 + V > (n_elem // epc) * epc)[~whole])
     if fast:
-        # per-block buffer: from the block's lowest row to the end of its highest; the kernel
-        # finds them as the largest-u / smallest-u row of each of its diagonals
-        key = (b.astype(np.int64) * n_dblk + d // DPB) * n_ublk + u // rows_per_block
-        order = np.lexsort((u, d, key))
-        ks, ds, us, rs = key[order], d[order], u[order], row[order]
-        starts = np.r_[0, np.nonzero(np.diff(ks))[0] + 1]
-        r_lo_true = np.minimum.reduceat(rs, starts)
-        r_hi_true = np.maximum.reduceat(rs, starts)
-        dstarts = np.r_[0, np.nonzero(np.diff(ks * (ND + 1) + ds))[0] + 1]
-        dblk = np.searchsorted(starts, dstarts, side="right") - 1
-        d_of = ds[dstarts]
-        u_max = np.maximum.reduceat(us, dstarts)
-        u_min = np.minimum.reduceat(us, dstarts)
-        bb = b[order][dstarts].astype(np.int64)
-        cand_lo = (bb * T + d_of - u_max) * (U + 1) + u_max
-        cand_hi = (bb * T + d_of - u_min) * (U + 1) + u_min
-        r_lo = np.full(len(starts), np.iinfo(np.int64).max)
-        r_hi = np.full(len(starts), -1)
-        np.minimum.at(r_lo, dblk, cand_lo)
-        np.maximum.at(r_hi, dblk, cand_hi)
-        assert np.array_equal(r_lo, r_lo_true) and np.array_equal(r_hi, r_hi_true)
-        c_base = (r_lo * V) // epc
-        c_end = (r_hi * V + V + epc - 1) // epc
+        # per-block buffer: from the first chunk of the block's first row (unit u_lo) to
+        # the end of its last row; row j of the block at element e_rel0 + j * V
+        ublk = u // rows_per_block
+        u_lo = ublk * rows_per_block
+        n_rows = np.minimum(rows_per_block, U + 1 - u_lo)
+        j = u - u_lo
+        row_lo = (b.astype(np.int64) * T + t) * (U + 1) + u_lo
+        e_first = row_lo * V
+        c_base = e_first // epc
+        c_end = (e_first + n_rows * V + epc - 1) // epc
         assert np.all((c_end - c_base) * 16 < 2**31)
-        blk = np.repeat(np.arange(len(starts)), np.diff(np.r_[starts, len(ks)]))
-        cs = c0[order]
-        off0 = (cs - c_base[blk]) * 16
-        assert np.all(off0 >= 0) and np.all(off0 + nch[order] * 16 <= (c_end - c_base)[blk] * 16)
+        e_rel = (e_first - c_base * epc) + j * V
+        assert np.array_equal(e_rel, e0 - c_base * epc)
+        off0 = (e_rel - mis) * esz
+        assert np.all(off0 >= 0) and np.all(off0 + nch * 16 <= (c_end - c_base) * 16)
+        assert np.all(e_rel * esz < 2**31)
         # rows per block fit the LDS arrays
-        assert np.diff(np.r_[starts, len(ks)]).max() <= DPB * 256
-        # the kernel's 32-bit element offsets: row j at e_rel0 - j * U*V from the block's first chunk
-        e_rel = e0[order] - c_base[blk] * epc
-        assert np.all(e_rel >= 0) and np.all(e_rel * {"f32": 4, "bf16": 2, "f16": 2}[dt] < 2**31)
-        if U > 0:
-            assert U * V < 2**31
-    # lattice-form writes at (b*ND + d)*(U+1) + u inside the C-cell arrays
-    sc = (b.astype(np.int64) * ND + d) * (U + 1) + u
-    assert sc.max() < B * ND * (U + 1) and sc.min() >= 0
+        assert n_rows.max() <= 256
+    # lattice-form writes at the row index, inside the B * T * (U+1) cell arrays
+    assert row.max() < B * T * (U + 1) and row.min() >= 0
 
 
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
@@ -155,14 +131,15 @@ def test_gradient_kernel_chunk_mapping(B, T, U, V, dt):
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
 def test_lattice_kernel_addresses(B, T, U, V, dt):
     """Sweep kernel: weights of any step e read at the cell clamped into the utterance,
-    diagonal ec = clamp(e, 0, D), unit clamp(u, ec - (T_b-1), min(ec, U_b)), a valid cell;
+    diagonal ec = clamp(e, 0, D), unit clamp(u, ec - (T_b-1), min(ec, U_b)), a valid cell,
+    stored at its row (b, ec - u, u);
     alpha stored in row min(d, D+1), beta in row d (or the spare row ND when d < 0), each row
     u_pad = 64*K wide; the posterior kernel reads alpha, beta only at diagonals <= D."""
     U1 = U + 1
     ND = T + U
     K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16) if U1 <= 64 * k)
     u_pad = 64 * K
-    n_cells = B * ND * U1
+    n_cells = B * T * U1  # kernel 1's lattice form: one cell per logits row
     n_scores = B * (ND + 1) * u_pad
     lanes = np.arange(64)
     for Tb, Ub in [(T, U), (1, 0), (max(1, T // 2), U // 2), (1, U), (T, 0)]:
@@ -175,7 +152,7 @@ def test_lattice_kernel_addresses(B, T, U, V, dt):
                     uc = np.minimum(np.maximum(lanes * K + k, ec - (Tb - 1)), min(ec, Ub))
                     tc = ec - uc
                     assert np.all((tc >= 0) & (tc < Tb) & (uc >= 0) & (uc <= Ub))  # a cell kernel 1 wrote
-                    w = (bb * ND + ec) * U1 + uc
+                    w = (bb * T + tc) * U1 + uc  # row (t, u) of utterance bb
                     assert np.all(w >= 0) and np.all(w < n_cells)
                     rows = []
                     if 1 <= e <= D + PF - 1:  # forward steps d = 1 .. (last block's end)
