@@ -26,6 +26,21 @@ struct __attribute__((aligned(16))) RowInfo {
 constexpr int32_t kNoLabel = -1;
 constexpr int32_t kZeroRow = -2;
 
+// Where the posterior kernel computes the row records of the grid lattice
+// from: kernel 1's lattice form and the sweeps' scores.
+struct LatticeRecordSrc {
+  int32_t T_max, U_max, u_pad;  // u_pad: row width of alpha / beta
+  const int32_t* labels;        // (B, U_max), may be null when U_max == 0
+  const int32_t* logit_lens;    // (B)
+  const int32_t* label_lens;    // (B)
+  const int32_t* status;        // (B) 0: good utterance
+  const double2* lp2;           // (B, T_max, U_max+1) {lp_blank, lp_label} * log2 e
+  const float* lse2;            // (B, T_max, U_max+1) lse * log2 e
+  const double* alpha;          // (B, T_max+U_max+1, u_pad) by diagonal, log2 units
+  const double* beta;
+  const double* lnp2_fwd;       // (B) log2 P
+};
+
 // Lattice scores are kept in log2 units (x * log2 e).  An absent arc, and a
 // node that no path reaches, carry kNoArc: finite, so sums and maxima never
 // meet -inf - -inf, and so far below any real score that it is exactly
@@ -45,6 +60,35 @@ __device__ __forceinline__ double log_add2(double x, double y) {
   const float d = static_cast<float>(x - y);
   const float c = fast_log2(1.0f + fast_exp2(-__builtin_fabsf(d)));
   return m + static_cast<double>(c);
+}
+
+// Row record of the valid row r = (b, t, u) (t < T, u <= U) of a good utterance:
+//   occ_blank = 2^(alpha(t,u) + lp_blank(t,u) + beta(t+1,u) - log2 P)   (t < T-1)
+//   occ_blank = 2^(alpha(T-1,U) + lp_blank(T-1,U) - log2 P)            (closing blank)
+//   occ_label = 2^(alpha(t,u) + lp_label(t,u) + beta(t,u+1) - log2 P)   (u < U)
+// and 0 for an absent arc.  Every load is issued unconditionally, at an index
+// inside the arrays (beta's unit clamped into its row).
+__device__ __forceinline__ RowInfo lattice_row_record(const LatticeRecordSrc& s, int b, int t, int u, int64_t r,
+                                                      int T, int U, double lnP2) {
+  const int d = t + u;
+  const int64_t ab0 = static_cast<int64_t>(b) * (s.T_max + s.U_max + 1) * s.u_pad;
+  const double al = s.alpha[ab0 + static_cast<int64_t>(d) * s.u_pad + u];
+  const double* __restrict__ bt = s.beta + ab0 + static_cast<int64_t>(d + 1) * s.u_pad;
+  const double b_down = bt[u];                           // beta(t+1, u)
+  const double b_right = bt[min(u + 1, s.u_pad - 1)];    // beta(t, u+1)
+  const double2 w = s.lp2[r];
+  const float lse2 = s.lse2[r];
+  const int y = s.U_max > 0 ? s.labels[static_cast<int64_t>(b) * s.U_max + min(u, s.U_max - 1)] : kNoLabel;
+  double xb = kNoArc, xl = kNoArc;
+  if (t < T - 1) xb = al + w.x + b_down - lnP2;
+  else if (u == U) xb = al + w.x - lnP2;
+  if (u < U) xl = al + w.y + b_right - lnP2;
+  RowInfo o;
+  o.lse2 = lse2;
+  o.occ_blank = fast_exp2(static_cast<float>(xb));
+  o.occ_label = fast_exp2(static_cast<float>(xl));
+  o.label = (u < U) ? y : kNoLabel;
+  return o;
 }
 
 // ---- 16-byte global accesses, optionally with the nontemporal (streaming) hint

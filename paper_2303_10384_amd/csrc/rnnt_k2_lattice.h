@@ -385,6 +385,8 @@ __global__ __launch_bounds__(kPostThreads) void k2b_posteriors(PostParams p) {
   }
   const double lnP2 = p.lnp2_fwd[b];
   const int64_t ab0 = static_cast<int64_t>(b) * (p.T_max + p.U_max + 1) * p.u_pad;
+  const LatticeRecordSrc src{p.T_max, p.U_max, p.u_pad, p.labels, p.logit_lens, p.label_lens, p.status,
+                             p.lp2,   p.lse2,  p.alpha, p.beta,   p.lnp2_fwd};
 
   const int n_items = kPostTileT * (kPostTileT - 1 + U1);
   for (int i = threadIdx.x; i < n_items; i += kPostThreads) {
@@ -397,36 +399,22 @@ __global__ __launch_bounds__(kPostThreads) void k2b_posteriors(PostParams p) {
       if (!DENSE) p.rowinfo[r] = RowInfo{0.f, 0.f, 0.f, kZeroRow};
       continue;
     }
-    const double al = p.alpha[ab0 + static_cast<int64_t>(d) * p.u_pad + u];
-    double wb, wl;
-    float lse2 = 0.f;
     if (!DENSE) {
-      const double2 w = p.lp2[r];
-      wb = w.x;
-      wl = w.y;
-      lse2 = p.lse2[r];
-    } else {
-      wb = to_lattice(p.lp_blank[r], true);
-      wl = to_lattice(u < U ? p.lp_label[r] : 0.0, u < U);
+      p.rowinfo[r] = lattice_row_record(src, b, t, u, r, T, U, lnP2);
+      continue;
     }
+    const double al = p.alpha[ab0 + static_cast<int64_t>(d) * p.u_pad + u];
+    const double wb = to_lattice(p.lp_blank[r], true);
+    const double wl = to_lattice(u < U ? p.lp_label[r] : 0.0, u < U);
     double xb = kNoArc, xl = kNoArc;
     if (t < T - 1) xb = al + wb + p.beta[ab0 + static_cast<int64_t>(d + 1) * p.u_pad + u] - lnP2;
     else if (u == U) xb = al + wb - lnP2;
     if (u < U) xl = al + wl + p.beta[ab0 + static_cast<int64_t>(d + 1) * p.u_pad + u + 1] - lnP2;
-    if (!DENSE) {
-      RowInfo o;
-      o.lse2 = lse2;
-      o.occ_blank = fast_exp2(static_cast<float>(xb));
-      o.occ_label = fast_exp2(static_cast<float>(xl));
-      o.label = (u < U) ? p.labels[static_cast<int64_t>(b) * p.U_max + u] : kNoLabel;
-      p.rowinfo[r] = o;
-    } else {
-      const double ln2 = 1.0 / kLog2eD;
-      if (p.alpha_out) p.alpha_out[r] = al * ln2;
-      if (p.beta_out) p.beta_out[r] = p.beta[ab0 + static_cast<int64_t>(d) * p.u_pad + u] * ln2;
-      if (p.occ_blank_out) p.occ_blank_out[r] = exp2(xb);
-      if (p.occ_label_out) p.occ_label_out[r] = exp2(xl);
-    }
+    const double ln2 = 1.0 / kLog2eD;
+    if (p.alpha_out) p.alpha_out[r] = al * ln2;
+    if (p.beta_out) p.beta_out[r] = p.beta[ab0 + static_cast<int64_t>(d) * p.u_pad + u] * ln2;
+    if (p.occ_blank_out) p.occ_blank_out[r] = exp2(xb);
+    if (p.occ_label_out) p.occ_label_out[r] = exp2(xl);
   }
 }
 
