@@ -22,32 +22,27 @@ import statistics
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
-# the sources whose change invalidates a traffic figure, per path
+# the sources whose change invalidates a traffic figure, per path: the two
+# streaming kernels whose figures the record serves (the populate kernel and the
+# gradient kernel) and the arc-list kernels of that path
 SOURCES = {
     "loss": [
-        "paper_2303_10384_amd/csrc/rnnt_api.hip",
         "paper_2303_10384_amd/csrc/rnnt_device.h",
         "paper_2303_10384_amd/csrc/rnnt_k1_populate.h",
-        "paper_2303_10384_amd/csrc/rnnt_k2_lattice.h",
-        "paper_2303_10384_amd/csrc/rnnt_k3_grad.h",
-        "paper_2303_10384_amd/csrc/rnnt_launch.h",
         "paper_2303_10384_amd/csrc/rnnt_launch_k1.h",
         "paper_2303_10384_amd/csrc/rnnt_launch_k1_lattice.hip",
-        "paper_2303_10384_amd/csrc/rnnt_launch_k2.h",
-        "paper_2303_10384_amd/csrc/rnnt_launch_k2_scores.hip",
+        "paper_2303_10384_amd/csrc/rnnt_k3_grad.h",
         "paper_2303_10384_amd/csrc/rnnt_launch_k3.hip",
     ],
     "arc": [
-        "paper_2303_10384_amd/csrc/rnnt_api.hip",
         "paper_2303_10384_amd/csrc/rnnt_device.h",
         "paper_2303_10384_amd/csrc/rnnt_k1_populate.h",
-        "paper_2303_10384_amd/csrc/rnnt_k3_grad.h",
-        "paper_2303_10384_amd/csrc/rnnt_arc_layout.h",
-        "paper_2303_10384_amd/csrc/rnnt_arc_kernels.h",
-        "paper_2303_10384_amd/csrc/rnnt_launch.h",
         "paper_2303_10384_amd/csrc/rnnt_launch_k1.h",
         "paper_2303_10384_amd/csrc/rnnt_launch_k1_rows.hip",
+        "paper_2303_10384_amd/csrc/rnnt_k3_grad.h",
         "paper_2303_10384_amd/csrc/rnnt_launch_k3.hip",
+        "paper_2303_10384_amd/csrc/rnnt_arc_layout.h",
+        "paper_2303_10384_amd/csrc/rnnt_arc_kernels.h",
     ],
 }
 KERNEL_SOURCES = SOURCES["loss"]
