@@ -187,10 +187,22 @@ __device__ __forceinline__ void issue_row(__amdgpu_buffer_rsrc_t rsrc, const Row
   if (WITH_LABEL) R.zy = issue_label_elem<T>(rsrc, g, V);
 }
 
-// (group max, group sum of exp(z - max)) of a row from its registers, in every lane.
+// Shift window (log2 units) of a row's sum of exponentials: with no element more
+// than kShiftWindow above the shift, no term exceeds 2^64 and the sum of V terms
+// stays far inside float32; with some element no more than kShiftWindow below
+// it, the dominant terms are at least 2^-64, far above the subnormal range.
+constexpr float kShiftWindow = 64.f;
+
+// (shift, group sum of 2^(z log2 e - shift)) of a row from its registers, in
+// every lane; the row's lse is ln 2 * (shift + log2 sum).  The shift is the group
+// maximum * log2 e on a group's first row (`exact`), and kept for its later rows
+// while every group of the wave has its row's maximum inside the shift window;
+// otherwise the whole wave takes the group maximum again.  Either shift gives
+// the same lse up to rounding, and a row costs no cross-lane maximum unless its
+// range moved far from its group's first row.
 template <typename T, int G, int NB>
-__device__ __forceinline__ void reduce_row(const RowRegs<T, G, NB>& R, const RowGeom& g, int V, int lg, float& mg,
-                                           double& sg) {
+__device__ __forceinline__ void reduce_row(const RowRegs<T, G, NB>& R, const RowGeom& g, int V, int lg, bool exact,
+                                           float& sh2, double& sg) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
   const float kNegInf = -__builtin_inff();
   const bool first_partial = g.mis != 0;
@@ -215,9 +227,26 @@ __device__ __forceinline__ void reduce_row(const RowRegs<T, G, NB>& R, const Row
 #pragma unroll
     for (int i = 0; i < NB * EPC; ++i) m = fmaxf(m, x[i]);
   }
-  mg = group_reduce<G, MaxOp>(m, kNegInf);
-  // pass 2: sum of exp relative to the group maximum
-  const float sh = (mg == kNegInf) ? 0.f : mg * kLog2eF;
+  bool take_max = exact;
+  if (!exact) {
+    // a row past the block's last is ignored; a NaN or -inf lane maximum fails the test
+    const float m2 = m * kLog2eF;
+    const bool high = g.live && !(m2 <= sh2 + kShiftWindow);
+    const bool low_ok = !g.live || m2 >= sh2 - kShiftWindow;
+    const uint64_t hi_mask = __builtin_amdgcn_ballot_w64(high);
+    const uint64_t ok_mask = __builtin_amdgcn_ballot_w64(low_ok);
+    constexpr uint64_t kField = (G == 64) ? ~0ull : ((1ull << G) - 1);
+    bool fine = hi_mask == 0;
+#pragma unroll
+    for (int gi = 0; gi < kWave / G; ++gi) fine = fine && ((ok_mask >> (gi * G)) & kField) != 0;
+    take_max = !fine;  // wave-uniform
+  }
+  if (take_max) {
+    const float mg = group_reduce<G, MaxOp>(m, kNegInf);
+    sh2 = (mg == kNegInf) ? 0.f : mg * kLog2eF;
+  }
+  // pass 2: sum of 2^(z log2 e - shift)
+  const float sh = sh2;
   float s = 0.f;
 #pragma unroll
   for (int i = 0; i < BPL; ++i) s += fast_exp2(fmaf(xb[i], kLog2eF, -sh));
@@ -296,7 +325,7 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   constexpr int GROUPS = 256 / G;  // rows in flight per block
   // per row: the label, then the group results (max, sum of exp, z[blank], z[y])
   __shared__ int s_label[kMaxRowsPerBlock];
-  __shared__ float s_max[kMaxRowsPerBlock];
+  __shared__ double s_shift2[kMaxRowsPerBlock];
   __shared__ double s_sum[kMaxRowsPerBlock];
   __shared__ float s_zb[kMaxRowsPerBlock];
   __shared__ float s_zy[kMaxRowsPerBlock];
@@ -361,12 +390,12 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
       g.y = with_label ? s_label[g.j] : kNoLabel;
       return g;
     };
-    auto finish = [&](const RowRegs<T, G, NB>& R, const RowGeom& g) {
-      float mg;
+    float sh2 = 0.f;  // the group's shift (log2 units), set on its first row
+    auto finish = [&](const RowRegs<T, G, NB>& R, const RowGeom& g, bool first) {
       double sg;
-      reduce_row<T, G, NB>(R, g, p.V, lg, mg, sg);
+      reduce_row<T, G, NB>(R, g, p.V, lg, first, sh2, sg);
       if (g.live && lg == 0) {
-        s_max[g.j] = mg;
+        s_shift2[g.j] = sh2;
         s_sum[g.j] = sg;
         s_zb[g.j] = R.zb;
         s_zy[g.j] = R.zy;
@@ -385,11 +414,11 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
       g1 = geom(it + 1, true);  // past the block's rows: not live, no memory access
       issue_row<T, G, NB>(rsrc, g1, p.V, p.blank, lg, R1);
       __builtin_amdgcn_sched_barrier(0);  // the next row's loads go out before this row is reduced
-      finish(R0, g0);
+      finish(R0, g0, it == 0);
       g0 = geom(it + 2, true);
       issue_row<T, G, NB>(rsrc, g0, p.V, p.blank, lg, R0);
       __builtin_amdgcn_sched_barrier(0);
-      finish(R1, g1);
+      finish(R1, g1, false);
     }
   } else {
     stage_labels();
@@ -411,7 +440,7 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
       double sg;
       row_stats_general<T, G, NB>(base, e0, c0, mis, nch, p.V, full_chunks, lg, mg, sg);
       if (live && lg == 0) {
-        s_max[j] = mg;
+        s_shift2[j] = static_cast<double>(mg) * kLog2eD;  // the sum is relative to exp(mg)
         s_sum[j] = sg;
         s_zb[j] = zb;
         s_zy[j] = zy;
@@ -427,7 +456,7 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
     const int64_t row = row_lo + j;
     const int y = s_label[j];
     const bool y_ok = y >= 0 && y < p.V;
-    const double lse = static_cast<double>(s_max[j]) + log(s_sum[j]);
+    const double lse = (s_shift2[j] + log2(s_sum[j])) / kLog2eD;
     const double lpb = static_cast<double>(s_zb[j]) - lse;
     const double lpl = (u < Ub) ? (y_ok ? static_cast<double>(s_zy[j]) - lse : __builtin_nan("")) : -__builtin_inf();
     if (OUT == kK1Lattice) {
