@@ -84,7 +84,7 @@ struct ArcPopulateParams {
   const int32_t* perm;     // graph-0 slot -> graph-1 slot
   const int32_t* loc0;     // LDS slot of the source score, per graph-0 slot
   const int32_t* loc1;     // the same per graph-1 slot
-  const double* lse2_rows; // lse * log2(e) per valid row
+  const double* lse2_rows; // log2 sum_v 2^(z_v kLog2eF) per valid row (the populate kernel's lse2f)
   int32_t* bad;            // (B): set to 1 for an utterance with a NaN arc weight (cleared by kernel 1)
   int32_t* rec0;           // slot records of graph 0
   int32_t* rec1;           // slot records of graph 1
@@ -111,7 +111,8 @@ __global__ __launch_bounds__(256) void k_arc_populate(ArcPopulateParams p) {
                     a.w < p.V;
     if (ok) {
       const float z = ElemTraits<T>::load1(static_cast<const T*>(p.logits) + static_cast<int64_t>(a.z) * p.V + a.w);
-      w += static_cast<double>(z) * kLog2eD - p.lse2_rows[a.z];
+      // (z - lse) log2(e), with lse = lse2f / kLog2eF
+      w += (static_cast<double>(z) - p.lse2_rows[a.z] / static_cast<double>(kLog2eF)) * kLog2eD;
     } else {
       w = __builtin_nan("");
     }

@@ -13,7 +13,8 @@ constexpr double kLog2eD = 1.4426950408889634;
 constexpr int kWave = 64;
 
 // Per-row record handed from the posterior kernel to the gradient kernel.
-// lse2 = ln(sum_v exp z_v) * log2(e); occ_* are the blank / label arc
+// lse2 = log2 sum_v 2^(z_v kLog2eF), the normaliser of the exponentials the
+// gradient kernel forms (2^(z kLog2eF - lse2)); occ_* are the blank / label arc
 // posteriors leaving the row's node; label is y_{u+1}, or kNoLabel on the top
 // row, or kZeroRow for rows whose gradient is identically zero (padding, bad
 // utterances).
@@ -35,7 +36,7 @@ struct LatticeRecordSrc {
   const int32_t* label_lens;    // (B)
   const int32_t* status;        // (B) 0: good utterance
   const double2* lp2;           // (B, T_max, U_max+1) {lp_blank, lp_label} * log2 e
-  const float* lse2;            // (B, T_max, U_max+1) lse * log2 e
+  const float* lse2;            // (B, T_max, U_max+1) log2 sum_v 2^(z_v kLog2eF)
   const double* alpha;          // (B, T_max+U_max+1, u_pad) by diagonal, log2 units
   const double* beta;
   const double* lnp2_fwd;       // (B) log2 P

@@ -73,13 +73,13 @@ struct PopulateParams {
   int32_t rows_per_block;  // consecutive units u per block (<= kMaxRowsPerBlock)
   // lattice form
   double2* lp2;            // (B, T_max, U_max+1) {lp_blank, lp_label} * log2(e)
-  float* lse2;             // same index: lse * log2(e)
+  float* lse2;             // same index: lse2f = log2 sum_v 2^(z_v kLog2eF)
   // dense form
   double* lse_out;         // (B, T_max, U_max+1) or null
   double* lp_blank_out;
   double* lp_label_out;
   // rows form
-  double* lse2_rows;       // (B, T_max, U_max+1): lse * log2(e)
+  double* lse2_rows;       // (B, T_max, U_max+1): lse2f, as lse2
   int32_t* clear_flags;    // (B) set to 0 by block 0 (the arc-list loss's bad-data flags), or null
 };
 
@@ -187,19 +187,24 @@ __device__ __forceinline__ void issue_row(__amdgpu_buffer_rsrc_t rsrc, const Row
   if (WITH_LABEL) R.zy = issue_label_elem<T>(rsrc, g, V);
 }
 
-// Shift window (log2 units) of a row's sum of exponentials: with no element more
-// than kShiftWindow above the shift, no term exceeds 2^64 and the sum of V terms
-// stays far inside float32; with some element no more than kShiftWindow below
-// it, the dominant terms are at least 2^-64, far above the subnormal range.
-constexpr float kShiftWindow = 64.f;
+// Accepted range of a row's group sum when the sum used an earlier row's shift.
+// A sum of at most 2^16 bounds every term by 2^16 (no element more than 16 log2
+// units above the shift, and no overflow); a sum of at least 2^-16 puts the
+// largest term within 16 + log2 V units below the shift, so the terms that
+// underflow are far below float32 resolution of the sum.  The dominant terms'
+// exponents then stay small, which keeps the rounding of their arguments near
+// that of the exact-maximum shift.
+constexpr float kSumHi = 65536.f;
+constexpr float kSumLo = 1.f / 65536.f;
 
 // (shift, group sum of 2^(z log2 e - shift)) of a row from its registers, in
 // every lane; the row's lse is ln 2 * (shift + log2 sum).  The shift is the group
-// maximum * log2 e on a group's first row (`exact`), and kept for its later rows
-// while every group of the wave has its row's maximum inside the shift window;
-// otherwise the whole wave takes the group maximum again.  Either shift gives
-// the same lse up to rounding, and a row costs no cross-lane maximum unless its
-// range moved far from its group's first row.
+// maximum * log2 e on a group's first row (`exact`); later rows sum against the
+// shift they inherit, and keep it while every live row of the wave has its group
+// sum inside [kSumLo, kSumHi] (a NaN or an empty row fails the test); otherwise
+// the whole wave takes its rows' group maxima and sums again from the registers.
+// Either shift gives the same lse up to rounding, and a row costs no maximum pass
+// unless its range moved far from the shift.
 template <typename T, int G, int NB>
 __device__ __forceinline__ void reduce_row(const RowRegs<T, G, NB>& R, const RowGeom& g, int V, int lg, bool exact,
                                            float& sh2, double& sg) {
@@ -219,47 +224,44 @@ __device__ __forceinline__ void reduce_row(const RowRegs<T, G, NB>& R, const Row
 #pragma unroll
   for (int q = 0; q < NB; ++q) ElemTraits<T>::unpack(make_uint4(R.raw[q].x, R.raw[q].y, R.raw[q].z, R.raw[q].w),
                                                      x + q * EPC);
-  // pass 1: maximum (interior duplicates are harmless; no interior chunks -> skip them)
-  float m = kNegInf;
+  // group sum of 2^(z log2 e - sh) (interior duplicates masked)
+  auto group_sum = [&](float sh) {
+    float s = fast_exp2(fmaf(xb[0], kLog2eF, -sh));
 #pragma unroll
-  for (int i = 0; i < BPL; ++i) m = fmaxf(m, xb[i]);
-  if (n_int > 0) {
+    for (int i = 1; i < BPL; ++i) s += fast_exp2(fmaf(xb[i], kLog2eF, -sh));
+    if (n_int > 0) {
 #pragma unroll
-    for (int i = 0; i < NB * EPC; ++i) m = fmaxf(m, x[i]);
-  }
+      for (int q = 0; q < NB; ++q) {
+        float sq = fast_exp2(fmaf(x[q * EPC], kLog2eF, -sh));
+#pragma unroll
+        for (int j = 1; j < EPC; ++j) sq += fast_exp2(fmaf(x[q * EPC + j], kLog2eF, -sh));
+        s += (kf + q * G + lg <= kl) ? sq : 0.f;
+      }
+    }
+    return group_reduce<G, SumOp>(s, 0.f);  // a pairwise tree of the lanes' partial sums
+  };
+  float sgf = 0.f;
   bool take_max = exact;
   if (!exact) {
-    // a row past the block's last is ignored; a NaN or -inf lane maximum fails the test
-    const float m2 = m * kLog2eF;
-    const bool high = g.live && !(m2 <= sh2 + kShiftWindow);
-    const bool low_ok = !g.live || m2 >= sh2 - kShiftWindow;
-    const uint64_t hi_mask = __builtin_amdgcn_ballot_w64(high);
-    const uint64_t ok_mask = __builtin_amdgcn_ballot_w64(low_ok);
-    constexpr uint64_t kField = (G == 64) ? ~0ull : ((1ull << G) - 1);
-    bool fine = hi_mask == 0;
-#pragma unroll
-    for (int gi = 0; gi < kWave / G; ++gi) fine = fine && ((ok_mask >> (gi * G)) & kField) != 0;
-    take_max = !fine;  // wave-uniform
+    sgf = group_sum(sh2);
+    // a row past the block's last is ignored
+    const bool bad = g.live && !(sgf >= kSumLo && sgf <= kSumHi);
+    take_max = __builtin_amdgcn_ballot_w64(bad) != 0;  // wave-uniform
   }
   if (take_max) {
+    // lane maximum (interior duplicates are harmless; no interior chunks -> skip them)
+    float m = kNegInf;
+#pragma unroll
+    for (int i = 0; i < BPL; ++i) m = fmaxf(m, xb[i]);
+    if (n_int > 0) {
+#pragma unroll
+      for (int i = 0; i < NB * EPC; ++i) m = fmaxf(m, x[i]);
+    }
     const float mg = group_reduce<G, MaxOp>(m, kNegInf);
     sh2 = (mg == kNegInf) ? 0.f : mg * kLog2eF;
+    sgf = group_sum(sh2);
   }
-  // pass 2: sum of 2^(z log2 e - shift)
-  const float sh = sh2;
-  float s = 0.f;
-#pragma unroll
-  for (int i = 0; i < BPL; ++i) s += fast_exp2(fmaf(xb[i], kLog2eF, -sh));
-  if (n_int > 0) {
-#pragma unroll
-    for (int q = 0; q < NB; ++q) {
-      float sq = 0.f;
-#pragma unroll
-      for (int j = 0; j < EPC; ++j) sq += fast_exp2(fmaf(x[q * EPC + j], kLog2eF, -sh));
-      s += (kf + q * G + lg <= kl) ? sq : 0.f;
-    }
-  }
-  sg = static_cast<double>(group_reduce<G, SumOp>(s, 0.f));  // a pairwise tree of the lanes' partial sums
+  sg = static_cast<double>(sgf);
 }
 
 // Row statistics for any row: batches of NB chunks per lane with a running
@@ -353,7 +355,10 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   const int n_rows = u_hi - u_lo;
 
   const int lg = threadIdx.x % G;  // lane inside the row group
-  const int grp = threadIdx.x / G;
+  // a wave's group index (and with it a row's geometry) in scalar registers when
+  // a group is the whole wave
+  const int grp = (G == kWave) ? __builtin_amdgcn_readfirstlane(threadIdx.x / G) : threadIdx.x / G;
+  auto group_uniform = [](int v) { return (G == kWave) ? __builtin_amdgcn_readfirstlane(v) : v; };
   // the block's labels go through LDS, so no label load waits inside the row loop
   auto stage_labels = [&]() {
     for (int i = threadIdx.x; i < n_rows; i += blockDim.x) {
@@ -387,7 +392,7 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
       g.mis = e_rel & (EPC - 1);
       g.nch = (g.mis + p.V + EPC - 1) / EPC;
       g.off0 = (e_rel - g.mis) * static_cast<int>(sizeof(T));
-      g.y = with_label ? s_label[g.j] : kNoLabel;
+      g.y = with_label ? group_uniform(s_label[g.j]) : kNoLabel;
       return g;
     };
     float sh2 = 0.f;  // the group's shift (log2 units), set on its first row
@@ -408,7 +413,7 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
     issue_row<T, G, NB, false>(rsrc, g0, p.V, p.blank, lg, R0);
     __builtin_amdgcn_sched_barrier(0);
     stage_labels();
-    g0.y = s_label[g0.j];
+    g0.y = group_uniform(s_label[g0.j]);
     R0.zy = issue_label_elem<T>(rsrc, g0, p.V);
     for (int it = 0; it < n_iter; it += 2) {
       g1 = geom(it + 1, true);  // past the block's rows: not live, no memory access
@@ -440,7 +445,7 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
       double sg;
       row_stats_general<T, G, NB>(base, e0, c0, mis, nch, p.V, full_chunks, lg, mg, sg);
       if (live && lg == 0) {
-        s_shift2[j] = static_cast<double>(mg) * kLog2eD;  // the sum is relative to exp(mg)
+        s_shift2[j] = static_cast<double>(mg) * static_cast<double>(kLog2eF);  // the sum is relative to 2^(mg kLog2eF)
         s_sum[j] = sg;
         s_zb[j] = zb;
         s_zy[j] = zy;
@@ -449,14 +454,21 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   }
   __syncthreads();
 
-  // one thread per row: lse = max + ln(sum), the arc weights in float64, and the
-  // block's results leave in one pass (a contiguous run of rows)
+  // one thread per row: the arc weights in float64, and the block's results leave
+  // in one pass (a contiguous run of rows).  Every exponential above is
+  // 2^(z * kLog2eF), so shift + log2(sum) is lse2f = log2 sum 2^(z kLog2eF), the
+  // log-normaliser of softmax(c z) with c = kLog2eF / log2(e) = 1 - 1.3e-8.  The
+  // gradient kernels exponentiate the same way, so they take lse2f: their softmax
+  // then sums to one.  lse2f / kLog2eF = lse(z) + (1 - c) H(softmax z) (H the
+  // entropy, at most ln V), so the row's lse is within 1.3e-8 ln V of the exact
+  // one, where lse2f / log2(e) would be off by 1.3e-8 |lse|.
   for (int j = threadIdx.x; j < n_rows; j += blockDim.x) {
     const int u = u_lo + j;
     const int64_t row = row_lo + j;
     const int y = s_label[j];
     const bool y_ok = y >= 0 && y < p.V;
-    const double lse = (s_shift2[j] + log2(s_sum[j])) / kLog2eD;
+    const double lse2f = s_shift2[j] + log2(s_sum[j]);
+    const double lse = lse2f / static_cast<double>(kLog2eF);
     const double lpb = static_cast<double>(s_zb[j]) - lse;
     const double lpl = (u < Ub) ? (y_ok ? static_cast<double>(s_zy[j]) - lse : __builtin_nan("")) : -__builtin_inf();
     if (OUT == kK1Lattice) {
@@ -465,9 +477,9 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
       w.x = blank_arc ? clamp_no_arc(lpb * kLog2eD) : kNoArc;
       w.y = (u < Ub) ? clamp_no_arc(lpl * kLog2eD) : kNoArc;
       p.lp2[row] = w;
-      p.lse2[row] = static_cast<float>(lse * kLog2eD);
+      p.lse2[row] = static_cast<float>(lse2f);
     } else if (OUT == kK1Rows) {
-      p.lse2_rows[row] = lse * kLog2eD;
+      p.lse2_rows[row] = lse2f;
     } else {
       if (p.lse_out) p.lse_out[row] = lse;
       p.lp_blank_out[row] = lpb;

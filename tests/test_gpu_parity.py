@@ -218,9 +218,52 @@ def test_populate_kernel(torch, pkg, dtype, V, blank):
         assert np.all(np.isnan(lse[b, :, U_b + 1:].cpu().numpy()))
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("V", [300, 1025, 4100])
+def test_populate_kernel_rows_far_apart(torch, pkg, dtype, V):
+    # a frame's rows at offsets up to 150 nats apart and with spreads from 0.3 to 20:
+    # rows whose range leaves the shift a wave carries from row to row, so the
+    # populate kernel must notice and take their maxima again
+    B, T, U = 2, 5, 40
+    logits, tl, ul, labels = W.small_case(B, T, U, V, seed=V + 7, sigma=1.0, full=True)
+    rng = np.random.Generator(np.random.PCG64(V))
+    offset = rng.choice([-90.0, -40.0, 0.0, 0.0, 0.0, 35.0, 120.0], size=(B, T, U + 1, 1))
+    spread = rng.choice([0.3, 1.0, 3.0, 3.0, 20.0], size=(B, T, U + 1, 1))
+    if dtype == "f16":  # inside the float16 range
+        offset, spread = offset / 4, np.minimum(spread, 5.0)
+    logits = (logits * spread + offset).astype(np.float32)
+    lg = to_dev(torch, logits).to(W.torch_dtype(dtype))
+    lse, lpb, lpl = pkg.log_softmax_gather(lg, to_dev(torch, labels), to_dev(torch, tl), to_dev(torch, ul), 0)
+    torch.cuda.synchronize()
+    z = lg.float().cpu().numpy().astype(np.float64)
+    for b in range(B):
+        lse_r, pb_r, pl_r = R.lattice_weights(z[b], labels[b], 0)
+        np.testing.assert_allclose(lse[b].cpu().numpy(), lse_r, rtol=0, atol=1e-6)
+        np.testing.assert_allclose(lpb[b].cpu().numpy(), pb_r, rtol=0, atol=1e-6)
+        np.testing.assert_allclose(lpl[b, :, :U].cpu().numpy(), pl_r[:, :U], rtol=0, atol=1e-6)
+
+
 # ---------------------------------------------------------------------------
 # end to end: rnnt_loss against the oracle
 # ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,gdt", [("f32", "f32"), ("bf16", "f32")])
+@pytest.mark.parametrize("variant", ["rnnt", "wrnnt"])
+def test_loss_rows_far_apart(torch, pkg, dtype, gdt, variant):
+    # the loss and gradient over rows far apart in offset and spread (the row
+    # normaliser's shift is taken again wherever a row leaves its range); lse stays
+    # under ~110 nats, where the gradient kernel's float32 normaliser (log2 units)
+    # keeps the softmax within 5.3e-6 relative
+    B, T, U, V = 3, 6, 30, 1025
+    logits, tl, ul, labels = W.small_case(B, T, U, V, seed=31, sigma=1.0)
+    rng = np.random.Generator(np.random.PCG64(32))
+    offset = rng.choice([-60.0, -25.0, 0.0, 0.0, 25.0, 60.0], size=(B, T, U + 1, 1))
+    spread = rng.choice([0.3, 1.0, 3.0, 10.0], size=(B, T, U + 1, 1))
+    logits = (logits * spread + offset).astype(np.float32)
+    loss, grad, seen = run_case(torch, pkg, logits, tl, ul, labels, variant=variant, dtype=dtype, grad_dtype=gdt)
+    loss_ref, grad_ref = R.rnnt_loss_grad(seen, labels, tl, ul, 0, variant)
+    tol_check(loss, grad, loss_ref, grad_ref, dtype, tl, ul, grad_dtype=gdt)
+
 
 @pytest.mark.parametrize("variant", VARIANTS)
 def test_tiny_workload(torch, pkg, variant):
