@@ -316,7 +316,7 @@ __device__ __forceinline__ void row_stats_general(const T* __restrict__ base, in
 constexpr int kMaxRowsPerBlock = 256;
 constexpr int kXcds = 8;
 #ifndef RNNT_K1_XCD_RUN
-#define RNNT_K1_XCD_RUN 16
+#define RNNT_K1_XCD_RUN 4
 #endif
 constexpr int kXcdRun = RNNT_K1_XCD_RUN;  // consecutive blocks per XCD turn
 

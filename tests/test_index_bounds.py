@@ -6,10 +6,18 @@ gradient kernel's chunk -> (row, column) mapping reproduces the flat index
 exactly, and that 32-bit intermediates cannot overflow.  The formulas mirror
 the launch code in csrc/rnnt_api.hip and the kernels' index expressions.
 """
+import os
+import re
+
 import numpy as np
 import pytest
 
 from paper_2303_10384_amd.workloads import WORKLOADS
+
+_K1_SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                       "paper_2303_10384_amd", "csrc", "rnnt_k1_populate.h")
+# consecutive populate blocks per XCD turn, as the kernel source defines it
+K1_XCD_RUN = int(re.search(r"#define RNNT_K1_XCD_RUN (\d+)", open(_K1_SRC).read()).group(1))
 
 EPC = {"f32": 4, "bf16": 8, "f16": 8}
 SHAPES = [(w.B, w.T_max, w.U_max, w.V, w.dtype) for w in WORKLOADS.values()] + [
@@ -28,8 +36,9 @@ def k1_shape(V, epc):
     return best
 
 
+@pytest.mark.parametrize("run", sorted({1, K1_XCD_RUN, 16}))
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
-def test_populate_kernel_addresses(B, T, U, V, dt):
+def test_populate_kernel_addresses(B, T, U, V, dt, run):
     epc = EPC[dt]
     esz = {"f32": 4, "bf16": 2, "f16": 2}[dt]
     n_elem = B * T * (U + 1) * V
@@ -37,7 +46,6 @@ def test_populate_kernel_addresses(B, T, U, V, dt):
     rows_per_block = min(U + 1, 32 if dt == "f32" else 256)  # consecutive units of one frame per block
     n_ublk = -(-(U + 1) // rows_per_block)
     blocks = B * T * n_ublk
-    run = 16  # consecutive blocks per XCD turn
     grid = -(-(-(-blocks // run)) // 8) * 8 * run
     assert grid < 2**31
     # XCD-major numbering: physical block i (XCD i % 8, its k-th block, k = i // 8) ->
