@@ -44,12 +44,14 @@ K1Shape k1_shape(int V) {
   return best;
 }
 
-// one block per frame of an utterance, split into blocks of at most 32 units for
-// float32 rows and kMaxRowsPerBlock units for 16-bit ones
+// one block per frame of an utterance, split into the fewest blocks of at most 32
+// units for float32 rows and kMaxRowsPerBlock units for 16-bit ones, of equal size
+// up to one unit (81 units: 27 + 27 + 27, not 32 + 32 + 17)
 void k1_blocking(PopulateParams& p, int elem_bytes) {
   const int cap = elem_bytes == 4 ? 32 : kMaxRowsPerBlock;
-  p.rows_per_block = p.U_max + 1 < cap ? p.U_max + 1 : cap;
-  p.n_ublk = (p.U_max + 1 + p.rows_per_block - 1) / p.rows_per_block;
+  const int U1 = p.U_max + 1;
+  p.n_ublk = (U1 + cap - 1) / cap;
+  p.rows_per_block = (U1 + p.n_ublk - 1) / p.n_ublk;
 }
 
 template <typename T, int G, int NB, int OUT, bool FAST>

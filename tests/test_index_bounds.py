@@ -43,8 +43,10 @@ def test_populate_kernel_addresses(B, T, U, V, dt, run):
     esz = {"f32": 4, "bf16": 2, "f16": 2}[dt]
     n_elem = B * T * (U + 1) * V
     G, NB, fast = k1_shape(V, epc)
-    rows_per_block = min(U + 1, 32 if dt == "f32" else 256)  # consecutive units of one frame per block
-    n_ublk = -(-(U + 1) // rows_per_block)
+    cap = 32 if dt == "f32" else 256  # consecutive units of one frame per block, at most
+    n_ublk = -(-(U + 1) // cap)
+    rows_per_block = -(-(U + 1) // n_ublk)  # equal blocks up to one unit
+    assert rows_per_block <= cap and (n_ublk - 1) * rows_per_block < U + 1
     blocks = B * T * n_ublk
     grid = -(-(-(-blocks // run)) // 8) * 8 * run
     assert grid < 2**31
