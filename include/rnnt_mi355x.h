@@ -59,7 +59,7 @@ typedef enum {
   RNNT_ERR_WORKSPACE = 6,    /* workspace given but smaller than required        */
   RNNT_ERR_ALIGNMENT = 7,    /* logits or grad not 16-byte aligned               */
   RNNT_ERR_HIP = 8,          /* a HIP runtime call failed (launch, allocation)   */
-  RNNT_ERR_UNSUPPORTED = 9,  /* shape outside what this build handles (U_max+1 > 1024,
+  RNNT_ERR_UNSUPPORTED = 9,  /* shape outside what this build handles (U_max+1 > 2048,
                                 or an arc-list lattice beyond the sweep's limits)   */
   RNNT_ERR_BAD_LATTICE = 10, /* an arc list that breaks the numbering rules of
                                 rnnt_arc_plan, or a plan that does not match      */
@@ -238,7 +238,7 @@ rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label
  * blank wins a tie with the jump to the final state.  A bad utterance (as in
  * rnnt_loss) gets score NaN and frames / span -1.  Needs a workspace of
  * rnnt_viterbi_workspace_bytes(shape) bytes (256-byte aligned) or NULL (then
- * allocated stream-ordered).  U_max + 1 <= 1024 (else RNNT_ERR_UNSUPPORTED).
+ * allocated stream-ordered).  U_max + 1 <= 2048 (else RNNT_ERR_UNSUPPORTED).
  */
 size_t rnnt_viterbi_workspace_bytes(rnnt_shape_t shape);
 rnnt_status_t rnnt_viterbi(const void* logits, rnnt_shape_t shape, const int32_t* labels,

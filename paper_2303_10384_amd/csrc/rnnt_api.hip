@@ -18,7 +18,7 @@ static __device__ __align__(256) unsigned char scratch[RNNT_NOALLOC_SCRATCH_BYTE
 namespace rnnt {
 namespace {
 
-constexpr int kMaxUnits1 = 1024;  // U_max + 1 handled by one wavefront (16 units per lane)
+constexpr int kMaxUnits1 = 2048;  // U_max + 1 handled by one wavefront (32 units per lane)
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
@@ -255,7 +255,7 @@ const char* rnnt_status_string(rnnt_status_t status) {
     case RNNT_ERR_WORKSPACE: return "workspace smaller than required";
     case RNNT_ERR_ALIGNMENT: return "logits / grad must be 16-byte aligned, workspace 256-byte aligned";
     case RNNT_ERR_HIP: return "HIP runtime error";
-    case RNNT_ERR_UNSUPPORTED: return "unsupported shape (U_max + 1 > 1024, or a lattice past the sweep's limits)";
+    case RNNT_ERR_UNSUPPORTED: return "unsupported shape (U_max + 1 > 2048, or a lattice past the sweep's limits)";
     case RNNT_ERR_BAD_LATTICE: return "arc list breaks the numbering rules, or the plan does not match the call";
     case RNNT_ERR_SCRATCH:
       return "the shape needs more workspace than the static scratch of rnnt_loss_noalloc (RNNT_NOALLOC_SCRATCH_BYTES)";

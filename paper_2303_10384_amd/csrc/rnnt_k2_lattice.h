@@ -116,7 +116,8 @@ __device__ __forceinline__ double wave_shift_down(double x, double fill) {
 // lanes covering U_max + 1 units (a lane's step costs about K cells).
 __host__ __device__ constexpr int units_per_lane(int units1) {
   return units1 <= 64 ? 1 : units1 <= 128 ? 2 : units1 <= 192 ? 3 : units1 <= 256 ? 4
-       : units1 <= 384 ? 6 : units1 <= 512 ? 8 : units1 <= 768 ? 12 : 16;
+       : units1 <= 384 ? 6 : units1 <= 512 ? 8 : units1 <= 768 ? 12 : units1 <= 1024 ? 16
+       : units1 <= 1536 ? 24 : 32;
 }
 
 // The value of unit u in this lane's slots (x[k] holds unit lane*K + k), or

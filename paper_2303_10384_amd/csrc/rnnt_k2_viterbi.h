@@ -39,7 +39,7 @@ struct ViterbiParams {
   int32_t* span;           // (B, 2) start / end frame, or null
 };
 
-constexpr int kViterbiMaxUnits1 = 1024;
+constexpr int kViterbiMaxUnits1 = 2048;
 
 __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int lane) {
   const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(x), lane);

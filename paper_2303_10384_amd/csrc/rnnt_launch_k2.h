@@ -18,7 +18,7 @@ namespace {  // each including unit keeps its own copy
 
 template <int K, int VAR, int MODE, bool DENSE_IN>
 hipError_t launch_k2_k(const LatticeParams& p, hipStream_t stream) {
-  constexpr int PF = (K >= 16) ? 2 : (48 / K > 24 ? 24 : 48 / K);  // diagonals of weights in flight
+  constexpr int PF = (K >= 24) ? 1 : (K >= 16) ? 2 : (48 / K > 24 ? 24 : 48 / K);  // diagonals of weights in flight
   const int sweeps = (MODE == kLossOnly) ? 1 : 2;  // forward only, or forward and backward
   hipLaunchKernelGGL((k2_lattice<K, PF, VAR, MODE, DENSE_IN>), dim3(p.B, sweeps), dim3(64), 0, stream, p);
   return hipGetLastError();
@@ -34,7 +34,9 @@ hipError_t launch_k2_v(const LatticeParams& p, hipStream_t stream) {
     case 6: return launch_k2_k<6, VAR, MODE, DENSE_IN>(p, stream);
     case 8: return launch_k2_k<8, VAR, MODE, DENSE_IN>(p, stream);
     case 12: return launch_k2_k<12, VAR, MODE, DENSE_IN>(p, stream);
-    default: return launch_k2_k<16, VAR, MODE, DENSE_IN>(p, stream);
+    case 16: return launch_k2_k<16, VAR, MODE, DENSE_IN>(p, stream);
+    case 24: return launch_k2_k<24, VAR, MODE, DENSE_IN>(p, stream);
+    default: return launch_k2_k<32, VAR, MODE, DENSE_IN>(p, stream);
   }
 }
 
@@ -49,7 +51,7 @@ hipError_t launch_k2(int variant, const LatticeParams& p, hipStream_t stream) {
 
 template <int K, int VAR>
 hipError_t launch_k2v_k(const ViterbiParams& p, hipStream_t stream) {
-  constexpr int PF = (K >= 16) ? 2 : (48 / K > 24 ? 24 : 48 / K);
+  constexpr int PF = (K >= 24) ? 1 : (K >= 16) ? 2 : (48 / K > 24 ? 24 : 48 / K);
   hipLaunchKernelGGL((k2_viterbi<K, PF, VAR>), dim3(p.B), dim3(64), 0, stream, p);
   return hipGetLastError();
 }
@@ -64,7 +66,9 @@ hipError_t launch_k2v_v(const ViterbiParams& p, hipStream_t stream) {
     case 6: return launch_k2v_k<6, VAR>(p, stream);
     case 8: return launch_k2v_k<8, VAR>(p, stream);
     case 12: return launch_k2v_k<12, VAR>(p, stream);
-    default: return launch_k2v_k<16, VAR>(p, stream);
+    case 16: return launch_k2v_k<16, VAR>(p, stream);
+    case 24: return launch_k2v_k<24, VAR>(p, stream);
+    default: return launch_k2v_k<32, VAR>(p, stream);
   }
 }
 

@@ -61,18 +61,19 @@ def expected_workspace(B, T, U, V):
     a = lambda x: (x + 255) // 256 * 256  # noqa: E731
     rows = B * T * (U + 1)
     cells = B * T * (U + 1)                  # lattice cells, one per logits row
-    K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16) if U + 1 <= 64 * k or k == 16)  # units per lane of the sweep
+    K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16, 24, 32) if U + 1 <= 64 * k or k == 32)  # units per lane of the sweep
     score_cells = B * (T + U + 1) * 64 * K  # rows 64*K wide, plus one spare diagonal per utterance
     o = a(rows * 16)               # row records
     o = a(o + cells * 16)          # {lp_blank, lp_label}
-    o = a(o + cells * 4)           # lse * log2 e
+    o = a(o + cells * 4)           # lse2f
     o = a(o + score_cells * 8)     # alpha
     o = a(o + score_cells * 8)     # beta
     o = a(o + 2 * B * 8)           # log P forward / backward
     return a(o + B * 4)            # status
 
 
-@pytest.mark.parametrize("B,T,U,V", [(1, 1, 0, 2), (2, 20, 8, 16), (32, 250, 80, 1025), (64, 500, 150, 1025)])
+@pytest.mark.parametrize("B,T,U,V", [(1, 1, 0, 2), (2, 20, 8, 16), (32, 250, 80, 1025), (64, 500, 150, 1025),
+                                     (1, 3, 1535, 4), (1, 2, 2047, 3)])
 def test_workspace_size(lib, B, T, U, V):
     assert lib.rnnt_loss_workspace_bytes(shape(B, T, U, V)) == expected_workspace(B, T, U, V)
 
@@ -111,7 +112,7 @@ def test_rnnt_loss_host_errors(lib):
     assert call_loss(lib, shape(), variant=3) == 5
     assert call_loss(lib, shape(), logits=FAKE + 4) == 7
     assert call_loss(lib, shape(), grad=FAKE + 8) == 7
-    assert call_loss(lib, shape(U=1024)) == 9
+    assert call_loss(lib, shape(U=2048)) == 9
     need = lib.rnnt_loss_workspace_bytes(shape())
     assert call_loss(lib, shape(), ws=FAKE, ws_bytes=need - 1) == 6
     assert call_loss(lib, shape(), ws=FAKE + 16, ws_bytes=need) == 7
@@ -139,7 +140,7 @@ def test_noalloc_host_errors(lib):
     assert call_noalloc(lib, shape(), blank=7) == 3
     assert call_noalloc(lib, shape(), variant=3) == 5
     assert call_noalloc(lib, shape(), grad=FAKE + 8) == 7
-    assert call_noalloc(lib, shape(U=1024)) == 9
+    assert call_noalloc(lib, shape(U=2048)) == 9
     # the largest batch of bpe rows that fits, and one utterance more
     cap = binding.NOALLOC_SCRATCH_BYTES
     assert lib.rnnt_loss_workspace_bytes(shape(32, 250, 80, 1025)) <= cap
@@ -174,13 +175,14 @@ def test_other_entry_points_host_errors(lib):
 def expected_viterbi_workspace(B, T, U, V):
     a = lambda x: (x + 255) // 256 * 256  # noqa: E731
     cells = B * T * (U + 1)
-    K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16) if U + 1 <= 64 * k or k == 16)
+    K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16, 24, 32) if U + 1 <= 64 * k or k == 32)
     o = a(cells * 16)                    # {lp_blank, lp_label}
     o = a(o + cells * 4)                 # lse * log2 e
     return a(o + B * (T + U + 1) * K * 8)  # decision words
 
 
-@pytest.mark.parametrize("B,T,U,V", [(1, 1, 0, 2), (32, 250, 80, 1025), (3, 7, 200, 9), (2, 5, 1023, 3)])
+@pytest.mark.parametrize("B,T,U,V", [(1, 1, 0, 2), (32, 250, 80, 1025), (3, 7, 200, 9), (2, 5, 1023, 3),
+                                     (2, 5, 2047, 3)])
 def test_viterbi_workspace_size(lib, B, T, U, V):
     assert lib.rnnt_viterbi_workspace_bytes(shape(B, T, U, V)) == expected_viterbi_workspace(B, T, U, V)
     assert lib.rnnt_viterbi_workspace_bytes(shape(B=0)) == 0
@@ -206,7 +208,7 @@ def test_viterbi_host_errors(lib):
     assert call_viterbi(lib, shape(), blank=7) == 3
     assert call_viterbi(lib, shape(), variant=3) == 5
     assert call_viterbi(lib, shape(), logits=FAKE + 4) == 7
-    assert call_viterbi(lib, shape(U=1024)) == 9
+    assert call_viterbi(lib, shape(U=2048)) == 9
     assert call_viterbi(lib, shape()) == 6  # workspace one byte short
     need = lib.rnnt_viterbi_workspace_bytes(shape())
     assert call_viterbi(lib, shape(), ws=FAKE + 16, ws_bytes=need) == 7

@@ -169,7 +169,8 @@ def test_lattice_kernel_on_printed_figures(torch, pkg, variant, loader, ref):
 
 
 @pytest.mark.parametrize("variant", VARIANTS)
-@pytest.mark.parametrize("B,T,U", [(3, 7, 5), (2, 40, 70), (2, 6, 200), (1, 3, 300), (1, 2, 700), (4, 1, 0), (3, 9, 0)])
+@pytest.mark.parametrize("B,T,U", [(3, 7, 5), (2, 40, 70), (2, 6, 200), (1, 3, 300), (1, 2, 700), (1, 3, 1500),
+                                   (1, 2, 2047), (4, 1, 0), (3, 9, 0)])
 def test_lattice_kernel_random_weights(torch, pkg, variant, B, T, U):
     rng = np.random.default_rng(B * 1000 + T * 10 + U)
     lp_b = -rng.exponential(1.0, size=(B, T, U + 1))
@@ -305,7 +306,9 @@ def test_random_shapes(torch, pkg, dtype, gdt, variant, B, T, U, V, blank, seed)
     (2, 5, 150, 7, 24),    # 3 units per lane of the sweep
     (2, 4, 300, 6, 21),    # 6 units per lane; a diagonal split over two populate blocks
     (1, 3, 700, 5, 22),    # 12 units per lane
-    (1, 2, 1023, 3, 23),   # the widest label axis the sweep takes (U_max + 1 = 1024)
+    (1, 2, 1023, 3, 23),   # 16 units per lane (U_max + 1 = 1024)
+    (1, 3, 1535, 4, 25),   # 24 units per lane
+    (1, 2, 2047, 3, 26),   # the widest label axis the sweep takes (U_max + 1 = 2048)
 ])
 def test_wide_label_axis(torch, pkg, dtype, variant, B, T, U, V, seed):
     logits, tl, ul, labels = W.small_case(B, T, U, V, seed=seed, sigma=2.0)

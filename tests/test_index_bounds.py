@@ -23,7 +23,7 @@ EPC = {"f32": 4, "bf16": 8, "f16": 8}
 SHAPES = [(w.B, w.T_max, w.U_max, w.V, w.dtype) for w in WORKLOADS.values()] + [
     (3, 7, 0, 2, "f32"), (2, 5, 4, 3, "bf16"), (1, 1, 1023, 5, "f32"), (4, 9, 63, 4097, "f16"),
     (5, 3, 64, 7, "bf16"), (2, 2, 127, 8, "f32"), (2, 4, 300, 6, "f32"), (1, 3, 700, 5, "bf16"),
-    (1, 2, 1023, 3, "bf16"), (3, 7, 5, 4100, "f32"), (3, 7, 5, 8200, "bf16"), (3, 7, 5, 2600, "f16")]
+    (1, 2, 1023, 3, "bf16"), (1, 3, 1535, 4, "f32"), (1, 2, 2047, 3, "bf16"), (3, 7, 5, 4100, "f32"), (3, 7, 5, 8200, "bf16"), (3, 7, 5, 2600, "f16")]
 
 
 def k1_shape(V, epc):
@@ -147,14 +147,14 @@ def test_lattice_kernel_addresses(B, T, U, V, dt):
     u_pad = 64*K wide; the posterior kernel reads alpha, beta only at diagonals <= D."""
     U1 = U + 1
     ND = T + U
-    K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16) if U1 <= 64 * k)
+    K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16, 24, 32) if U1 <= 64 * k)
     u_pad = 64 * K
     n_cells = B * T * U1  # kernel 1's lattice form: one cell per logits row
     n_scores = B * (ND + 1) * u_pad
     lanes = np.arange(64)
     for Tb, Ub in [(T, U), (1, 0), (max(1, T // 2), U // 2), (1, U), (T, 0)]:
         D = Tb - 1 + Ub
-        PF = 2 if K >= 16 else min(24, 48 // K)
+        PF = 1 if K >= 24 else 2 if K >= 16 else min(24, 48 // K)
         for bb in {0, B - 1}:
             for e in range(-PF - 2, D + PF + 2):  # every diagonal a load or store step can name
                 ec = min(max(e, 0), D)
@@ -237,11 +237,11 @@ def test_viterbi_kernel_addresses(B, T, U, V, dt):
     word the walk reads lies in the current window."""
     U1 = U + 1
     ND = T + U
-    K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16) if U1 <= 64 * k)
+    K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16, 24, 32) if U1 <= 64 * k)
     words = (ND + 1) * K
     for Tb, Ub in [(T, U), (1, 0), (max(1, T // 2), U // 2), (1, U), (T, 0)]:
         D = Tb - 1 + Ub
-        PF = 2 if K >= 16 else min(24, 48 // K)
+        PF = 1 if K >= 24 else 2 if K >= 16 else min(24, 48 // K)
         for d in range(1, D + PF):
             row = min(d, D + 1)
             for lane in range(64):
