@@ -132,7 +132,7 @@ rnnt_status_t take_workspace(void* workspace, size_t workspace_bytes, size_t nee
 
 // Workspace of rnnt_arc_loss, 256-byte aligned pieces (R logits rows, A arcs,
 // S states of the plan):
-//   lse2     R double   lse * log2(e) per row
+//   lse2     R double   lse2f = log2 sum_v 2^(z_v kLog2eF) per row
 //   rec0/1   A0, A1 x 12 bytes  slot records (weight, source LDS slot) of the two sweeps
 //   val0/1   S double   forward / backward scores
 //   lnp      2*B double
@@ -502,7 +502,7 @@ rnnt_status_t rnnt_arc_loss_timed(const void* logits, rnnt_shape_t shape, const 
   auto mark = [&](int i) { return events ? hipEventRecord(events[i], stream) : hipSuccess; };
   if (mark(0) != hipSuccess) return RNNT_ERR_HIP;
 
-  // kernel 1 (rows form): lse * log2(e) of every valid row
+  // kernel 1 (rows form): lse2f of every valid row
   PopulateParams p1{};
   p1.logits = logits;
   p1.B = shape.B;

@@ -11,29 +11,29 @@
 //  * kK1Lattice (the fused loss): arc weights in log2 units, stored as
 //    {lp_blank, lp_label} pairs per row, (B, T_max, U_max+1) like the logits'
 //    rows; absent arcs (the label arc of the top row, the blank arcs of the last
-//    frame below the top row) carry kNoArc; plus lse * log2(e) as float32 at the
-//    same index.
+//    frame below the top row) carry kNoArc; plus lse2f (the log2 normaliser of
+//    the kernel's own exponentials, see the results loop) as float32 at the same
+//    index.
 //  * kK1Dense: natural-log lse / lp_blank / lp_label, (B, T_max, U_max+1)
 //    float64 (the populate step on its own);
-//  * kK1Rows: lse * log2(e) per row, (B, T_max, U_max+1) float64, and no
+//  * kK1Rows: lse2f per row, (B, T_max, U_max+1) float64, and no
 //    labels read (the loss over arc-list lattices, whose arcs select their own
 //    labels).
 //
 // Mapping: a block owns up to `rows_per_block` consecutive units u of one frame
 // t of one utterance, so its rows are consecutive in memory; blocks are numbered
-// so that runs of consecutive frames of an utterance go to the same XCD
-// (dispatch deals blocks to the 8 XCDs round robin), where the lines shared by
-// neighbouring blocks' boundary rows meet in one L2.  A group of
+// so that short runs of consecutive blocks go to the same XCD (dispatch deals
+// blocks to the 8 XCDs round robin).  A group of
 // G lanes reads one row as aligned 16-byte chunks.  The chunks entirely inside
 // the row ("interior") are spread NB per lane (G and NB picked from V so that
 // G*NB just covers them) and need no element masks: a lane with no chunk of its
 // own reloads an interior chunk, which cannot raise the maximum, and drops it
 // from the sum with one select.  The elements of the at most two chunks that
 // straddle the row's ends are spread over the group, one element per lane
-// (two when G is 8), each with its own mask.  Then two passes over the
-// registers: the group maximum (DPP reduction), then the sum of
-// 2^(z*log2 e - max*log2 e) per lane in float32 and across the group by a
-// pairwise float32 tree.
+// (two when G is 8), each with its own mask.  Then the sum of
+// 2^(z*log2 e - shift) per lane in float32 and across the group by a pairwise
+// float32 DPP tree, against a shift taken from the group maximum on the group's
+// first row and kept while the rows' sums stay in range (reduce_row).
 //
 // Fast path (every block whose rows lie in whole chunks): the loads of a
 // group's first row are issued before the block stages its labels in LDS, and
@@ -325,7 +325,7 @@ template <typename T, int G, int NB, int OUT, bool FAST>
 __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
   constexpr int EPC = ElemTraits<T>::kPerChunk;
   constexpr int GROUPS = 256 / G;  // rows in flight per block
-  // per row: the label, then the group results (max, sum of exp, z[blank], z[y])
+  // per row: the label, then the group results (shift, sum of exponentials, z[blank], z[y])
   __shared__ int s_label[kMaxRowsPerBlock];
   __shared__ double s_shift2[kMaxRowsPerBlock];
   __shared__ double s_sum[kMaxRowsPerBlock];

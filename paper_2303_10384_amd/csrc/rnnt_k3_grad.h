@@ -8,7 +8,8 @@
 // located in its row(s) by index arithmetic, chunks of zero rows (padding, bad
 // utterances) are written as 0 without reading the logits, and every other
 // chunk reads the logits once and writes the gradient once.
-// p_v = exp2(z_v * log2(e) - lse2) with lse2 = lse * log2(e) from the row record.
+// p_v = exp2(z_v * kLog2eF - lse2) with lse2 = log2 sum_v 2^(z_v kLog2eF) from the
+// row record (the populate kernel's normaliser of the same exponentials).
 #pragma once
 
 #include "rnnt_device.h"
