@@ -60,7 +60,8 @@ typedef enum {
   RNNT_ERR_ALIGNMENT = 7,    /* logits or grad not 16-byte aligned               */
   RNNT_ERR_HIP = 8,          /* a HIP runtime call failed (launch, allocation)   */
   RNNT_ERR_UNSUPPORTED = 9,  /* shape outside what this build handles (U_max+1 > 2048,
-                                or an arc-list lattice beyond the sweep's limits)   */
+                                T_max * (U_max+1) >= 2^27, or an arc-list lattice
+                                beyond the sweep's limits)                          */
   RNNT_ERR_BAD_LATTICE = 10, /* an arc list that breaks the numbering rules of
                                 rnnt_arc_plan, or a plan that does not match      */
   RNNT_ERR_SCRATCH = 11      /* rnnt_loss_noalloc: the shape needs more workspace
@@ -121,7 +122,9 @@ size_t rnnt_loss_workspace_bytes(rnnt_shape_t shape);
  *               releases one with hipMallocAsync / hipFreeAsync on `stream`.
  *               Its contents need no initialisation and are not preserved.
  *   stream      HIP stream the work is ordered on.
- * Calls that overlap in time must not share a workspace.
+ * Calls that overlap in time must not share a workspace.  Shapes with
+ * U_max + 1 > 2048 or T_max * (U_max + 1) >= 2^27 return RNNT_ERR_UNSUPPORTED
+ * (such lattices go through rnnt_arc_loss).
  */
 rnnt_status_t rnnt_loss(const void* logits, rnnt_shape_t shape, const int32_t* labels,
                         const int32_t* logit_lens, const int32_t* label_lens, int32_t blank,
@@ -238,7 +241,8 @@ rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label
  * blank wins a tie with the jump to the final state.  A bad utterance (as in
  * rnnt_loss) gets score NaN and frames / span -1.  Needs a workspace of
  * rnnt_viterbi_workspace_bytes(shape) bytes (256-byte aligned) or NULL (then
- * allocated stream-ordered).  U_max + 1 <= 2048 (else RNNT_ERR_UNSUPPORTED).
+ * allocated stream-ordered).  U_max + 1 <= 2048 and T_max * (U_max + 1) < 2^27
+ * (else RNNT_ERR_UNSUPPORTED).
  */
 size_t rnnt_viterbi_workspace_bytes(rnnt_shape_t shape);
 rnnt_status_t rnnt_viterbi(const void* logits, rnnt_shape_t shape, const int32_t* labels,

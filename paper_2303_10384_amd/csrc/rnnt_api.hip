@@ -189,6 +189,12 @@ bool plan_consistent(const rnnt_arc_plan_t& pl, const rnnt_shape_t& s) {
   return true;
 }
 
+// The sweeps take U_max + 1 <= kMaxUnits1 and read an utterance's lattice form
+// (T_max x (U_max+1) cells of 16 bytes) through one buffer with 32-bit offsets.
+bool sweep_fits(const rnnt_shape_t& s) {
+  return s.U_max + 1 <= kMaxUnits1 && static_cast<int64_t>(s.T_max) * (s.U_max + 1) * 16 < (int64_t{1} << 31);
+}
+
 // Checks of rnnt_loss's arguments that need no device.
 rnnt_status_t check_loss_args(const void* logits, const rnnt_shape_t& shape, const int32_t* labels,
                               const int32_t* logit_lens, const int32_t* label_lens, int32_t blank, int variant,
@@ -200,7 +206,7 @@ rnnt_status_t check_loss_args(const void* logits, const rnnt_shape_t& shape, con
   if (blank < 0 || blank >= shape.V) return RNNT_ERR_BAD_BLANK;
   if (!variant_known(variant)) return RNNT_ERR_BAD_VARIANT;
   if (!aligned16(logits) || (grad_out && !aligned16(grad_out))) return RNNT_ERR_ALIGNMENT;
-  if (shape.U_max + 1 > kMaxUnits1) return RNNT_ERR_UNSUPPORTED;
+  if (!sweep_fits(shape)) return RNNT_ERR_UNSUPPORTED;
   return RNNT_OK;
 }
 
@@ -255,7 +261,8 @@ const char* rnnt_status_string(rnnt_status_t status) {
     case RNNT_ERR_WORKSPACE: return "workspace smaller than required";
     case RNNT_ERR_ALIGNMENT: return "logits / grad must be 16-byte aligned, workspace 256-byte aligned";
     case RNNT_ERR_HIP: return "HIP runtime error";
-    case RNNT_ERR_UNSUPPORTED: return "unsupported shape (U_max + 1 > 2048, or a lattice past the sweep's limits)";
+    case RNNT_ERR_UNSUPPORTED:
+      return "unsupported shape (U_max + 1 > 2048, T_max * (U_max + 1) >= 2^27, or a lattice past the sweep's limits)";
     case RNNT_ERR_BAD_LATTICE: return "arc list breaks the numbering rules, or the plan does not match the call";
     case RNNT_ERR_SCRATCH:
       return "the shape needs more workspace than the static scratch of rnnt_loss_noalloc (RNNT_NOALLOC_SCRATCH_BYTES)";
@@ -423,7 +430,7 @@ rnnt_status_t rnnt_viterbi_timed(const void* logits, rnnt_shape_t shape, const i
   if (blank < 0 || blank >= shape.V) return RNNT_ERR_BAD_BLANK;
   if (!variant_known(variant)) return RNNT_ERR_BAD_VARIANT;
   if (!aligned16(logits)) return RNNT_ERR_ALIGNMENT;
-  if (shape.U_max + 1 > kMaxUnits1) return RNNT_ERR_UNSUPPORTED;
+  if (!sweep_fits(shape)) return RNNT_ERR_UNSUPPORTED;
   const ViterbiLayout L = make_viterbi_layout(shape);
   OwnedWorkspace owned;
   char* ws = nullptr;

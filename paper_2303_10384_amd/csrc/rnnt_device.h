@@ -334,6 +334,19 @@ __device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, int off
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, NT ? kBufferNT : 0);
 }
 
+// Lattice-form cell (t, u) of one utterance, t = e - u on diagonal e, through a
+// buffer over the utterance's T_max x (U_max+1) cells: its byte offset
+// 16 (e U1 - u (U1 - 1)) is one 24-bit multiply-add per lane on top of the
+// wave-uniform 16 e U1 (u < 2^11 and 16 (U1 - 1) < 2^15; the span is checked on
+// the host to stay under 2^31 bytes).
+__device__ __forceinline__ double2 load_lattice_cell(__amdgpu_buffer_rsrc_t r, int e_row_bytes, int u, int neg_step) {
+  const u32x4 v = buffer_load16<false>(r, __mul24(u, neg_step) + e_row_bytes);
+  double2 w;
+  w.x = __hiloint2double(static_cast<int>(v.y), static_cast<int>(v.x));
+  w.y = __hiloint2double(static_cast<int>(v.w), static_cast<int>(v.z));
+  return w;
+}
+
 // One element of type T (4 or 2 bytes) at byte offset `off`, widened to float.
 template <typename T>
 __device__ __forceinline__ float buffer_load_elem(__amdgpu_buffer_rsrc_t r, int off) {

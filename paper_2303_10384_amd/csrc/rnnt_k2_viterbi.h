@@ -88,10 +88,12 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
   const int D = T - 1 + U;
   const int owner_top = U / K;
   const double2* __restrict__ w_utt = p.lp2 + static_cast<int64_t>(b) * p.T_max * U1;
+  const __amdgpu_buffer_rsrc_t w_rsrc = make_buffer(w_utt, static_cast<int64_t>(p.T_max) * U1 * 16);
+  const int neg_step = -16 * (U1 - 1);
   auto load_w = [&](int e, int k, double& wb, double& wl) {
     const int ec = min(max(e, 0), D);
     const int uc = min(max(lane * K + k, ec - (T - 1)), min(ec, U));
-    const double2 w = w_utt[(ec - uc) * U1 + uc];  // row (t, u) = (ec - uc, uc)
+    const double2 w = load_lattice_cell(w_rsrc, 16 * ec * U1, uc, neg_step);  // row (t, u) = (ec - uc, uc)
     wb = w.x;
     wl = w.y;
   };

@@ -113,6 +113,8 @@ def test_rnnt_loss_host_errors(lib):
     assert call_loss(lib, shape(), logits=FAKE + 4) == 7
     assert call_loss(lib, shape(), grad=FAKE + 8) == 7
     assert call_loss(lib, shape(U=2048)) == 9
+    assert call_loss(lib, shape(B=1, T=65536, U=2047, V=2)) == 9  # the lattice form's 2^31-byte buffer
+    assert call_loss(lib, shape(B=1, T=65535, U=2047, V=2), ws=FAKE, ws_bytes=0) == 6  # fits: on to the workspace
     need = lib.rnnt_loss_workspace_bytes(shape())
     assert call_loss(lib, shape(), ws=FAKE, ws_bytes=need - 1) == 6
     assert call_loss(lib, shape(), ws=FAKE + 16, ws_bytes=need) == 7
@@ -209,6 +211,7 @@ def test_viterbi_host_errors(lib):
     assert call_viterbi(lib, shape(), variant=3) == 5
     assert call_viterbi(lib, shape(), logits=FAKE + 4) == 7
     assert call_viterbi(lib, shape(U=2048)) == 9
+    assert call_viterbi(lib, shape(B=1, T=65536, U=2047, V=2)) == 9
     assert call_viterbi(lib, shape()) == 6  # workspace one byte short
     need = lib.rnnt_viterbi_workspace_bytes(shape())
     assert call_viterbi(lib, shape(), ws=FAKE + 16, ws_bytes=need) == 7
