@@ -323,6 +323,7 @@ struct ElemTraits<f16_t> {
 constexpr int kBufferWord3 = 0x00020000;               // raw buffer, 32-bit data format (gfx9 family)
 constexpr int kOutOfRange = static_cast<int>(0x80000000u);  // past any buffer made here (< 2^31 bytes)
 constexpr int kBufferNT = 2;                           // cache-policy bits: nontemporal
+constexpr int kBufferSC1 = 16;                         // cache-policy bits: device scope (written through the L2)
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_buffer(const void* base, int64_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0), static_cast<int>(bytes),

@@ -476,8 +476,17 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
       double2 w;
       w.x = blank_arc ? clamp_no_arc(lpb * kLog2eD) : kNoArc;
       w.y = (u < Ub) ? clamp_no_arc(lpl * kLog2eD) : kNoArc;
-      p.lp2[row] = w;
-      p.lse2[row] = static_cast<float>(lse2f);
+      // device-scope stores, written through the L2 as they are issued: K1's
+      // stream of reads then slows less than under the L2's later write-backs
+      // (large bf16: K1 0.822 -> 0.812 ms); the block's rows are consecutive
+      const __amdgpu_buffer_rsrc_t r_lp = make_buffer(p.lp2 + row_lo, static_cast<int64_t>(n_rows) * 16);
+      const __amdgpu_buffer_rsrc_t r_lse = make_buffer(p.lse2 + row_lo, static_cast<int64_t>(n_rows) * 4);
+      const uint64_t wx = static_cast<uint64_t>(__double_as_longlong(w.x));
+      const uint64_t wy = static_cast<uint64_t>(__double_as_longlong(w.y));
+      const u32x4 v = {static_cast<uint32_t>(wx), static_cast<uint32_t>(wx >> 32), static_cast<uint32_t>(wy),
+                       static_cast<uint32_t>(wy >> 32)};
+      __builtin_amdgcn_raw_buffer_store_b128(v, r_lp, j * 16, 0, kBufferSC1);
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(static_cast<float>(lse2f)), r_lse, j * 4, 0, kBufferSC1);
     } else if (OUT == kK1Rows) {
       p.lse2_rows[row] = lse2f;
     } else {
