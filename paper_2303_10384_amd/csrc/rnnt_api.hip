@@ -189,10 +189,17 @@ bool plan_consistent(const rnnt_arc_plan_t& pl, const rnnt_shape_t& s) {
   return true;
 }
 
-// The sweeps take U_max + 1 <= kMaxUnits1 and read an utterance's lattice form
-// (T_max x (U_max+1) cells of 16 bytes) through one buffer with 32-bit offsets.
+// The sweeps take U_max + 1 <= kMaxUnits1 and address an utterance's score rows
+// ((T_max + U_max + 1) rows of 64 K float64) through one buffer with 32-bit
+// offsets.
+bool scores_fit(const rnnt_shape_t& s) {
+  return s.U_max + 1 <= kMaxUnits1 &&
+         static_cast<int64_t>(s.T_max + s.U_max + 1) * 64 * units_per_lane(s.U_max + 1) * 8 < (int64_t{1} << 31);
+}
+
+// ... and read its lattice form (T_max x (U_max+1) cells of 16 bytes) the same way.
 bool sweep_fits(const rnnt_shape_t& s) {
-  return s.U_max + 1 <= kMaxUnits1 && static_cast<int64_t>(s.T_max) * (s.U_max + 1) * 16 < (int64_t{1} << 31);
+  return scores_fit(s) && static_cast<int64_t>(s.T_max) * (s.U_max + 1) * 16 < (int64_t{1} << 31);
 }
 
 // Checks of rnnt_loss's arguments that need no device.
@@ -671,7 +678,7 @@ rnnt_status_t rnnt_lattice_scores(const double* lp_blank, const double* lp_label
   if (st != RNNT_OK) return st;
   if (!lp_blank || !lp_label || !logit_lens || !label_lens) return RNNT_ERR_NULL_PTR;
   if (!variant_known(variant)) return RNNT_ERR_BAD_VARIANT;
-  if (s.U_max + 1 > kMaxUnits1) return RNNT_ERR_UNSUPPORTED;
+  if (!scores_fit(s)) return RNNT_ERR_UNSUPPORTED;
   const Layout L = make_layout(s, false);
   OwnedWorkspace owned;
   char* ws = nullptr;

@@ -335,6 +335,28 @@ __device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, int off
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, NT ? kBufferNT : 0);
 }
 
+// A lane's K consecutive float64 scores into a score row, through a buffer:
+// `lane_off` the lane's byte offset in the row (per lane, fixed), `row_off` the
+// row's byte offset (wave-uniform, in a scalar register), 16-byte stores for
+// pairs and an 8-byte store for an odd last score.
+template <int K>
+__device__ __forceinline__ void store_scores(__amdgpu_buffer_rsrc_t r, int lane_off, int row_off, const double (&x)[K]) {
+#pragma unroll
+  for (int k = 0; k + 1 < K; k += 2) {
+    const uint64_t a = static_cast<uint64_t>(__double_as_longlong(x[k]));
+    const uint64_t c = static_cast<uint64_t>(__double_as_longlong(x[k + 1]));
+    const u32x4 v = {static_cast<uint32_t>(a), static_cast<uint32_t>(a >> 32), static_cast<uint32_t>(c),
+                     static_cast<uint32_t>(c >> 32)};
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, lane_off + 8 * k, row_off, 0);
+  }
+  if constexpr (K % 2 == 1) {
+    const uint64_t a = static_cast<uint64_t>(__double_as_longlong(x[K - 1]));
+    typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+    const u32x2 v = {static_cast<uint32_t>(a), static_cast<uint32_t>(a >> 32)};
+    __builtin_amdgcn_raw_buffer_store_b64(v, r, lane_off + 8 * (K - 1), row_off, 0);
+  }
+}
+
 // Lattice-form cell (t, u) of one utterance, t = e - u on diagonal e, through a
 // buffer over the utterance's T_max x (U_max+1) cells: its byte offset
 // 16 (e U1 - u (U1 - 1)) is one 24-bit multiply-add per lane on top of the

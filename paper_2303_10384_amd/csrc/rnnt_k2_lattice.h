@@ -187,6 +187,12 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
   // score rows: diagonals 0..D, then spare rows up to ND
   double* __restrict__ a_utt = p.alpha + static_cast<int64_t>(b) * (ND + 1) * p.u_pad;
   double* __restrict__ b_utt = p.beta + static_cast<int64_t>(b) * (ND + 1) * p.u_pad;
+  // score rows through per-utterance buffers: the row's byte offset is wave-uniform
+  // (the host keeps (T_max + U_max + 1) * u_pad * 8 under 2^31), the lane's fixed
+  const __amdgpu_buffer_rsrc_t a_rsrc = make_buffer(a_utt, static_cast<int64_t>(ND + 1) * p.u_pad * 8);
+  const __amdgpu_buffer_rsrc_t b_rsrc = make_buffer(b_utt, static_cast<int64_t>(ND + 1) * p.u_pad * 8);
+  const int lane_off = lane * K * 8;
+  const int row_bytes = p.u_pad * 8;
 
   // weight of the closing blank, lp_blank(T-1, U)
   double w_close, w_unused;
@@ -247,11 +253,8 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
           a_top = at_unit(a, lane, U, a_top);
         }
         if (VAR != 0 && d >= U && d - U <= T - 2) acc_top = log_add2(acc_top, at_unit(a, lane, U, kNoArc));  // alpha(d-U, U)
-        if (MODE != kLossOnly) {
-          double* __restrict__ row = a_utt + static_cast<int64_t>(min(d, D + 1)) * p.u_pad + lane * K;
-#pragma unroll
-          for (int k = 0; k < K; ++k) row[k] = a[k];
-        }
+        if (MODE != kLossOnly)  // the row offset is uniform; readfirstlane keeps it in a scalar register
+          store_scores<K>(a_rsrc, lane_off, __builtin_amdgcn_readfirstlane(min(d, D + 1) * row_bytes), a);
 #pragma unroll
         for (int k = 0; k < K; ++k) load_w(d - 1 + PF, k, rb[s][k], rl[s][k]);
         __builtin_amdgcn_sched_barrier(0);  // the prefetch stays PF steps ahead of its use
@@ -310,12 +313,9 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
           b00 = nb[0];
         }
         if (VAR != 0 && d >= 1 && d <= T - 1) acc0 = log_add2(acc0, nb[0]);  // beta(d, 0), lane 0
-        double* __restrict__ row = b_utt + static_cast<int64_t>(d >= 0 ? d : ND) * p.u_pad + lane * K;
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-          bv[k] = nb[k];
-          row[k] = nb[k];
-        }
+        for (int k = 0; k < K; ++k) bv[k] = nb[k];
+        store_scores<K>(b_rsrc, lane_off, __builtin_amdgcn_readfirstlane((d >= 0 ? d : ND) * row_bytes), nb);
 #pragma unroll
         for (int k = 0; k < K; ++k) load_w(d - PF, k, rb[s][k], rl[s][k]);
         __builtin_amdgcn_sched_barrier(0);  // the prefetch stays PF steps ahead of its use
