@@ -244,7 +244,7 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
         for (int k = 0; k < K; ++k) a[k] = log_add2(eb[k], k == 0 ? left : el[k > 0 ? k - 1 : 0]);
         // wave-uniform conditions on the diagonal; no memory access inside
         if (VAR != 0 && d <= T - 1 && lane == 0) a[0] = log_add2(a[0], 0.0);  // (0,0)->(d,0)
-        if (d == D) {
+        if (__builtin_expect(d == D, 0)) {  // once per sweep: a branch, not selects in every step
           if (VAR == 1) {
 #pragma unroll
             for (int k = 0; k < K; ++k)
@@ -308,7 +308,7 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
 #pragma unroll
           for (int k = 0; k < K; ++k) nb[k] = (lane * K + k == U) ? x : nb[k];
         }
-        if (d == 0) {  // wave-uniform
+        if (__builtin_expect(d == 0, 0)) {  // wave-uniform, once per sweep: a branch, not selects
           if (VAR != 0 && lane == 0) nb[0] = log_add2(nb[0], acc0);  // (0,0)->(t,0)
           b00 = nb[0];
         }
