@@ -210,6 +210,9 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
     for (int k = 0; k < K; ++k) a[k] = (lane * K + k == 0) ? 0.0 : kNoArc;
     double acc_top = kNoArc;                   // log-sum of alpha(t, U), t <= T-2
     double a_top = (U == 0) ? 0.0 : kNoArc;    // alpha(T-1, U) once the sweep reaches D
+    // the shifted-in neighbour; lane 0 gets none from the shift and keeps kNoArc
+    // from here on, so no fill value is set up in each step
+    double left_carry = kNoArc;
     if (VAR != 0 && U == 0 && T >= 2) acc_top = 0.0;  // alpha(0, U) itself when U = 0
     if (MODE != kLossOnly && lane == 0) a_utt[0] = 0.0;
 
@@ -239,7 +242,8 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
           eb[k] = a[k] + wb;
           el[k] = a[k] + wl;
         }
-        const double left = wave_shift_up(el[K - 1], kNoArc);
+        left_carry = wave_shift_up(el[K - 1], left_carry);
+        const double left = left_carry;
 #pragma unroll
         for (int k = 0; k < K; ++k) a[k] = log_add2(eb[k], k == 0 ? left : el[k > 0 ? k - 1 : 0]);
         // wave-uniform conditions on the diagonal; no memory access inside
@@ -276,6 +280,7 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
     if (VAR != 0 && U == 0 && T >= 2) acc0 = w_close;
     if (lane == owner_top) b_utt[static_cast<int64_t>(D) * p.u_pad + U] = w_close;
     double b00 = (D == 0) ? w_close : kNoArc;  // beta(0,0)
+    double right_carry = kNoArc;  // lane 63 keeps kNoArc (see left_carry)
 
     double rb[PF][K], rl[PF][K];
 #pragma unroll
@@ -289,7 +294,8 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
 #pragma unroll
       for (int s = 0; s < PF; ++s) {
         const int d = d0 - s;  // slot s holds the weights of diagonal d (d < 0: no node)
-        const double right = wave_shift_down(bv[0], kNoArc);
+        right_carry = wave_shift_down(bv[0], right_carry);
+        const double right = right_carry;
         double nb[K];
 #pragma unroll
         for (int k = 0; k < K; ++k) {

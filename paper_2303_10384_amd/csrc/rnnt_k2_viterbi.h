@@ -105,6 +105,7 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
 #pragma unroll
   for (int k = 0; k < K; ++k) a[k] = (lane * K + k == 0) ? 0.0 : kNoArc;
   double a_top = (U == 0) ? 0.0 : kNoArc;  // delta(T-1, U) once the sweep reaches D
+  double left_carry = kNoArc;  // lane 0 gets nothing from the shift and keeps kNoArc
   double acc_top = kNoArc;                 // best delta(t', U), t' <= T-2, and its earliest frame
   int t_star = -1;
   if (VAR != 0 && U == 0 && T >= 2) {
@@ -131,7 +132,8 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
         eb[k] = a[k] + rb[s][k];
         el[k] = a[k] + rl[s][k];
       }
-      const double left = wave_shift_up(el[K - 1], kNoArc);
+      left_carry = wave_shift_up(el[K - 1], left_carry);
+      const double left = left_carry;
       bool dec[K];
 #pragma unroll
       for (int k = 0; k < K; ++k) {
