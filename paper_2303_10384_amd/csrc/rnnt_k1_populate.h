@@ -488,7 +488,11 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
       __builtin_amdgcn_raw_buffer_store_b128(v, r_lp, j * 16, 0, kBufferSC1);
       __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(static_cast<float>(lse2f)), r_lse, j * 4, 0, kBufferSC1);
     } else if (OUT == kK1Rows) {
-      p.lse2_rows[row] = lse2f;
+      const __amdgpu_buffer_rsrc_t r_rows = make_buffer(p.lse2_rows + row_lo, static_cast<int64_t>(n_rows) * 8);
+      const uint64_t lb = static_cast<uint64_t>(__double_as_longlong(lse2f));
+      typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+      const u32x2 v = {static_cast<uint32_t>(lb), static_cast<uint32_t>(lb >> 32)};
+      __builtin_amdgcn_raw_buffer_store_b64(v, r_rows, j * 8, 0, kBufferSC1);  // device scope, as above
     } else {
       if (p.lse_out) p.lse_out[row] = lse;
       p.lp_blank_out[row] = lpb;
