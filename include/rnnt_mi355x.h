@@ -145,7 +145,7 @@ rnnt_status_t rnnt_loss(const void* logits, rnnt_shape_t shape, const int32_t* l
  * array's device address (hipGetSymbolAddress) and keeps it for later calls.
  *   - A shape whose workspace (rnnt_loss_workspace_bytes) exceeds the array
  *     returns RNNT_ERR_SCRATCH, checked on the host before any HIP call; the
- *     bpe-sized batch (B = 32, T_max = 250, U_max = 80) needs about 49 MB.
+ *     bpe-sized batch (B = 32, T_max = 250, U_max = 80) needs about 42 MB.
  *   - Every call on one GPU shares that GPU's array, which keeps the last
  *     call's contents.  Nothing in it needs to start at zero (each call writes
  *     every word it reads before reading it).  Calls that overlap in time on

@@ -44,14 +44,13 @@ rnnt_status_t check_shape(const rnnt_shape_t& s) {
 // cells, one per logits row; S = B * (T_max+U_max+1) * u_pad score cells, u_pad =
 // 64 * units per lane of the lattice sweep):
 //   rowinfo  B*T_max*(U_max+1) RowInfo        (rnnt_loss)
-//   lp2      C double2 {lp_blank, lp_label}    (rnnt_loss)
-//   lse2     C float                           (rnnt_loss)
+//   lp2      C double2 {lp_blank, lp_label}, lse2f in their low bits  (rnnt_loss)
 //   alpha    S double
 //   beta     S double
 //   lnp      2*B double
 //   status   B int32
 struct Layout {
-  size_t rowinfo, lp2, lse2, alpha, beta, lnp, status, total;
+  size_t rowinfo, lp2, alpha, beta, lnp, status, total;
 };
 
 Layout make_layout(const rnnt_shape_t& s, bool with_populate) {
@@ -67,8 +66,6 @@ Layout make_layout(const rnnt_shape_t& s, bool with_populate) {
     o = align256(o + rows * sizeof(RowInfo));
     L.lp2 = o;
     o = align256(o + cells * 2 * sizeof(double));
-    L.lse2 = o;
-    o = align256(o + cells * sizeof(float));
   }
   L.alpha = o;
   o = align256(o + score_cells * sizeof(double));
@@ -82,10 +79,10 @@ Layout make_layout(const rnnt_shape_t& s, bool with_populate) {
   return L;
 }
 
-// Workspace of the forced alignment: the lattice form (lp2, lse2) as in the loss,
+// Workspace of the forced alignment: the lattice form (lp2) as in the loss,
 // the decision words B * (T_max+U_max+1) * K uint64, 256-byte aligned pieces.
 struct ViterbiLayout {
-  size_t lp2, lse2, decisions, total;
+  size_t lp2, decisions, total;
 };
 
 ViterbiLayout make_viterbi_layout(const rnnt_shape_t& s) {
@@ -96,8 +93,6 @@ ViterbiLayout make_viterbi_layout(const rnnt_shape_t& s) {
   size_t o = 0;
   L.lp2 = o;
   o = align256(o + cells * 2 * sizeof(double));
-  L.lse2 = o;
-  o = align256(o + cells * sizeof(float));
   L.decisions = o;
   o = align256(o + words * sizeof(uint64_t));
   L.total = o;
@@ -325,7 +320,7 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
   p1.label_lens = label_lens;
   p1.n_elem = n_elem;
   p1.lp2 = reinterpret_cast<double2*>(ws + L.lp2);
-  p1.lse2 = reinterpret_cast<float*>(ws + L.lse2);
+  p1.pack_lse2f = 1;  // the posterior kernel reads lse2f from the weights
   if (launch_populate_lattice(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(1) != hipSuccess) return RNNT_ERR_HIP;
 
@@ -362,7 +357,6 @@ rnnt_status_t rnnt_loss_timed(const void* logits, rnnt_shape_t shape, const int3
     pb.label_lens = label_lens;
     pb.status = p2.status;
     pb.lp2 = p1.lp2;
-    pb.lse2 = p1.lse2;
     pb.alpha = p2.alpha;
     pb.beta = p2.beta;
     pb.u_pad = p2.u_pad;
@@ -458,7 +452,7 @@ rnnt_status_t rnnt_viterbi_timed(const void* logits, rnnt_shape_t shape, const i
   p1.label_lens = label_lens;
   p1.n_elem = static_cast<int64_t>(shape.B) * shape.T_max * (shape.U_max + 1) * shape.V;
   p1.lp2 = reinterpret_cast<double2*>(ws + L.lp2);
-  p1.lse2 = reinterpret_cast<float*>(ws + L.lse2);
+  p1.pack_lse2f = 0;  // the alignment's ties stay exact in the unmodified weights
   if (launch_populate_lattice(shape.dtype, p1, stream) != hipSuccess) return RNNT_ERR_HIP;
   if (mark(1) != hipSuccess) return RNNT_ERR_HIP;
 

@@ -11,9 +11,10 @@
 //  * kK1Lattice (the fused loss): arc weights in log2 units, stored as
 //    {lp_blank, lp_label} pairs per row, (B, T_max, U_max+1) like the logits'
 //    rows; absent arcs (the label arc of the top row, the blank arcs of the last
-//    frame below the top row) carry kNoArc; plus lse2f (the log2 normaliser of
-//    the kernel's own exponentials, see the results loop) as float32 at the same
-//    index.
+//    frame below the top row) carry kNoArc; lse2f (the log2 normaliser of the
+//    kernel's own exponentials, see the results loop) rides as float32 in the
+//    low 16 bits of the two weights' mantissas (pack_lse2f) when the loss asks
+//    for it.
 //  * kK1Dense: natural-log lse / lp_blank / lp_label, (B, T_max, U_max+1)
 //    float64 (the populate step on its own);
 //  * kK1Rows: lse2f per row, (B, T_max, U_max+1) float64, and no
@@ -73,7 +74,8 @@ struct PopulateParams {
   int32_t rows_per_block;  // consecutive units u per block (<= kMaxRowsPerBlock)
   // lattice form
   double2* lp2;            // (B, T_max, U_max+1) {lp_blank, lp_label} * log2(e)
-  float* lse2;             // same index: lse2f = log2 sum_v 2^(z_v kLog2eF)
+  int32_t pack_lse2f;      // nonzero: lse2f rides in the low bits of each row's two weights (the loss);
+                           // zero: the weights as they are (forced alignment, whose ties stay exact)
   // dense form
   double* lse_out;         // (B, T_max, U_max+1) or null
   double* lp_blank_out;
@@ -479,14 +481,13 @@ __global__ __launch_bounds__(256) void k1_populate(PopulateParams p) {
       // device-scope stores, written through the L2 as they are issued: K1's
       // stream of reads then slows less than under the L2's later write-backs
       // (large bf16: K1 0.822 -> 0.812 ms); the block's rows are consecutive
+      if (p.pack_lse2f) w = pack_lse2f(w, static_cast<float>(lse2f));  // lse2f rides in the weights' low bits
       const __amdgpu_buffer_rsrc_t r_lp = make_buffer(p.lp2 + row_lo, static_cast<int64_t>(n_rows) * 16);
-      const __amdgpu_buffer_rsrc_t r_lse = make_buffer(p.lse2 + row_lo, static_cast<int64_t>(n_rows) * 4);
       const uint64_t wx = static_cast<uint64_t>(__double_as_longlong(w.x));
       const uint64_t wy = static_cast<uint64_t>(__double_as_longlong(w.y));
       const u32x4 v = {static_cast<uint32_t>(wx), static_cast<uint32_t>(wx >> 32), static_cast<uint32_t>(wy),
                        static_cast<uint32_t>(wy >> 32)};
       __builtin_amdgcn_raw_buffer_store_b128(v, r_lp, j * 16, 0, kBufferSC1);
-      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(static_cast<float>(lse2f)), r_lse, j * 4, 0, kBufferSC1);
     } else if (OUT == kK1Rows) {
       const __amdgpu_buffer_rsrc_t r_rows = make_buffer(p.lse2_rows + row_lo, static_cast<int64_t>(n_rows) * 8);
       const uint64_t lb = static_cast<uint64_t>(__double_as_longlong(lse2f));

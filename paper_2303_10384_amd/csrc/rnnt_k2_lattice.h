@@ -340,8 +340,7 @@ struct PostParams {
   const int32_t* logit_lens;
   const int32_t* label_lens;
   const int32_t* status;
-  const double2* lp2;  // kernel 1's lattice form, or
-  const float* lse2;
+  const double2* lp2;  // kernel 1's lattice form (lse2f in the weights' low bits), or
   const double* lp_blank;  // dense natural-log weights
   const double* lp_label;
   const double* alpha;
@@ -395,7 +394,7 @@ __global__ __launch_bounds__(kPostThreads) void k2b_posteriors(PostParams p) {
   const double lnP2 = p.lnp2_fwd[b];
   const int64_t ab0 = static_cast<int64_t>(b) * (p.T_max + p.U_max + 1) * p.u_pad;
   const LatticeRecordSrc src{p.T_max, p.U_max, p.u_pad, p.labels, p.logit_lens, p.label_lens, p.status,
-                             p.lp2,   p.lse2,  p.alpha, p.beta,   p.lnp2_fwd};
+                             p.lp2,   p.alpha, p.beta,  p.lnp2_fwd};
 
   const int n_items = kPostTileT * (kPostTileT - 1 + U1);
   for (int i = threadIdx.x; i < n_items; i += kPostThreads) {

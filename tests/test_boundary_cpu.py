@@ -64,8 +64,7 @@ def expected_workspace(B, T, U, V):
     K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16, 24, 32) if U + 1 <= 64 * k or k == 32)  # units per lane of the sweep
     score_cells = B * (T + U + 1) * 64 * K  # rows 64*K wide, plus one spare diagonal per utterance
     o = a(rows * 16)               # row records
-    o = a(o + cells * 16)          # {lp_blank, lp_label}
-    o = a(o + cells * 4)           # lse2f
+    o = a(o + cells * 16)          # {lp_blank, lp_label}, lse2f in their low bits
     o = a(o + score_cells * 8)     # alpha
     o = a(o + score_cells * 8)     # beta
     o = a(o + 2 * B * 8)           # log P forward / backward
@@ -178,8 +177,7 @@ def expected_viterbi_workspace(B, T, U, V):
     a = lambda x: (x + 255) // 256 * 256  # noqa: E731
     cells = B * T * (U + 1)
     K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16, 24, 32) if U + 1 <= 64 * k or k == 32)
-    o = a(cells * 16)                    # {lp_blank, lp_label}
-    o = a(o + cells * 4)                 # lse * log2 e
+    o = a(cells * 16)                    # {lp_blank, lp_label}, lse2f in their low bits
     return a(o + B * (T + U + 1) * K * 8)  # decision words
 
 
