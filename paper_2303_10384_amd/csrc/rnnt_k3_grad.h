@@ -199,13 +199,16 @@ __global__ __launch_bounds__(kGradThreads<Tin>) void k3_grad(GradParams p) {
 // most two rows, a and a+1, so everything that depends on the row is the same
 // across the wave: the two row records (scalar loads), whether a row is a zero
 // row, and where the corrected elements -- the blank and the label y_{u+1} of
-// each row -- fall.  Each lane picks (lse2, g_b + g_l) by the row its chunk
-// lies in, and an element costs exp2(z log2 e - lse2) * (g_b + g_l) alone.
-// The one lane whose chunk straddles the row end (if any) redoes its chunk
-// element by element under a wave-uniform branch, where an element of a zero
-// row is set to 0 whatever its logits hold (padding logits may be NaN).  The at
-// most four corrections -g_b at v = blank and -g_l at v = y_{u+1} are applied
-// by the lane owning the element, at a position known to the whole wave.
+// each row -- fall.  An element costs one exponential, 2^(z log2 e - s), with
+// the row's occupancy g_b + g_l folded into the shift s (one_exp_shift).  In a
+// group that reaches into row b, each lane holds two shifts, for the elements
+// of its chunk before and after the wave-uniform column where row b starts
+// (they differ only in the one lane whose chunk straddles the row end), and an
+// element picks one of them by its constant index; where one of the two rows
+// is a zero row, that lane's elements of it are set to 0 whatever its logits
+// hold (padding logits may be NaN).  The at most four corrections -g_b at
+// v = blank and -g_l at v = y_{u+1} are applied by the lane owning the element,
+// at a position known to the whole wave.
 template <typename Tin>
 constexpr int kWideMinV = kWave * ElemTraits<Tin>::kPerChunk - 1;
 
@@ -223,6 +226,27 @@ __device__ __forceinline__ void fix_element(float (&out)[EPC], int lane, int own
 template <int EPC>
 __device__ __forceinline__ void fix_column(float (&out)[EPC], int lane, int pos, float corr) {
   if (pos >= 0 && pos < kWave * EPC) fix_element<EPC>(out, lane, pos / EPC, pos % EPC, corr);
+}
+
+// The shift s and factor m of a row record such that p_v (g_b + g_l) =
+// 2^(z_v log2 e - s) * m.  While |lse2| < kOneExpMaxLse2 the occupancy moves into
+// the exponent (s = lse2 - log2(g_b + g_l), m = 1: one exponential and no
+// multiply per element); the rounding of s then costs at most 2^-24 |s| ln 2 of
+// the element, under 3e-6 of the largest (|s| <= 64 where g_b + g_l is near 1)
+// and decaying with the occupancy.  Rows with larger normalisers keep s = lse2
+// and m = g_b + g_l, and so do rows whose occupancy lies in (0, 2^-60): the
+// exponential unit returns 0 for results below 2^-126, where the product with
+// m keeps the subnormal result of the multiply.  A row with no occupancy (zero
+// rows included) gets s = +inf: every finite logit then gives exactly 0.
+// Returns whether m == 1.
+constexpr float kOneExpMaxLse2 = 64.f;
+constexpr float kOneExpMinOcc = 0x1p-60f;
+__device__ __forceinline__ bool one_exp_shift(const RowInfo& r, float& s, float& m) {
+  const float occ = r.occ_blank + r.occ_label;
+  const bool one = __builtin_fabsf(r.lse2) < kOneExpMaxLse2 && (occ >= kOneExpMinOcc || occ == 0.f);
+  s = one ? r.lse2 - fast_log2(occ) : r.lse2;
+  m = one ? 1.f : occ;
+  return one;
 }
 
 template <typename Tin, typename Tout>
@@ -275,7 +299,6 @@ __global__ __launch_bounds__(kGradThreads<Tin>) void k3_grad_wide(GradParams p) 
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
     const int cl = q * kThreads + static_cast<int>(threadIdx.x);
-    const int v = va[q] + lane * EPC;
     const int to_b = p.V - va[q];  // the group's first element of row b (>= 64*EPC: none)
     const bool za = Ra[q].label == kZeroRow, zb = Rb[q].label == kZeroRow;
     float out[EPC];
@@ -285,21 +308,36 @@ __global__ __launch_bounds__(kGradThreads<Tin>) void k3_grad_wide(GradParams p) 
     } else {
       float f[EPC];
       ElemTraits<T>::unpack(make_uint4(raw[q].x, raw[q].y, raw[q].z, raw[q].w), f);
-      const bool in_b = v >= p.V;
-      const float lse2 = in_b ? Rb[q].lse2 : Ra[q].lse2;
-      const float occ = in_b ? Rb[q].occ_blank + Rb[q].occ_label : Ra[q].occ_blank + Ra[q].occ_label;
+      // p_v (g_b + g_l) = 2^(z_v log2 e - s) * m per row: s = lse2 - log2(g_b + g_l) and m = 1
+      // while |lse2| < kOneExpMaxLse2, else s = lse2 and m = g_b + g_l (see one_exp_shift)
+      float sa, ma, sb, mb;
+      const bool one_a = one_exp_shift(Ra[q], sa, ma), one_b = one_exp_shift(Rb[q], sb, mb);
+      if (to_b >= kWave * EPC) {  // the group lies in row a
+        if (one_a) {
 #pragma unroll
-      for (int j = 0; j < EPC; ++j) out[j] = fast_exp2(fmaf(f[j], kLog2eF, -lse2)) * occ;
-      if (to_b % EPC != 0 && to_b < kWave * EPC) {  // one lane's chunk straddles the row end
-        if (v < p.V && v + EPC > p.V) {
+          for (int j = 0; j < EPC; ++j) out[j] = fast_exp2(fmaf(f[j], kLog2eF, -sa));
+        } else {
 #pragma unroll
-          for (int j = 0; j < EPC; ++j) {
-            const bool bj = v + j >= p.V;
-            const float l2 = bj ? Rb[q].lse2 : Ra[q].lse2;
-            const float oc = bj ? Rb[q].occ_blank + Rb[q].occ_label : Ra[q].occ_blank + Ra[q].occ_label;
-            const float g = fast_exp2(fmaf(f[j], kLog2eF, -l2)) * oc;
-            out[j] = (bj ? zb : za) ? 0.f : g;
-          }
+          for (int j = 0; j < EPC; ++j) out[j] = fast_exp2(fmaf(f[j], kLog2eF, -sa)) * ma;
+        }
+      } else {
+        // row b starts at element ks of lane L's chunk: element j of a lane lies in
+        // row b from lane L + 1 on (j < ks) or from lane L on (j >= ks)
+        const int L = to_b / EPC, ks = to_b % EPC;
+        const float s_lo = lane > L ? sb : sa, s_hi = lane >= L ? sb : sa;
+        if (one_a && one_b) {
+#pragma unroll
+          for (int j = 0; j < EPC; ++j) out[j] = fast_exp2(fmaf(f[j], kLog2eF, -(j < ks ? s_lo : s_hi)));
+        } else {
+          const float m_lo = lane > L ? mb : ma, m_hi = lane >= L ? mb : ma;
+#pragma unroll
+          for (int j = 0; j < EPC; ++j)
+            out[j] = fast_exp2(fmaf(f[j], kLog2eF, -(j < ks ? s_lo : s_hi))) * (j < ks ? m_lo : m_hi);
+        }
+        if (za != zb) {  // the straddling chunk's elements of a zero row are 0 whatever its logits hold
+          const bool z_lo = lane > L ? zb : za, z_hi = lane >= L ? zb : za;
+#pragma unroll
+          for (int j = 0; j < EPC; ++j) out[j] = (j < ks ? z_lo : z_hi) ? 0.f : out[j];
         }
       }
       if (!za) {
