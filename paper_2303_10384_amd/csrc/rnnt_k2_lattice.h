@@ -134,8 +134,18 @@ __device__ __forceinline__ double at_unit(const double (&x)[K], int lane, int u,
 
 // VAR: 0 RNN-T, 1 W-Transducer force-final, 2 allow-ignore.
 // DENSE_IN: weights from the dense natural-log arrays instead of kernel 1.
-template <int K, int PF, int VAR, int MODE, bool DENSE_IN>
-__global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
+// NW: wavefronts per sweep.  Wave w owns units w*64*K .. (w+1)*64*K - 1 (unit u
+// still sits in column u of the score rows) and runs the diagonals a whole
+// segment of PF steps behind the wave it depends on: the forward wave w after
+// wave w-1 (its lane 0 needs the label-arc term of the unit below it), the
+// backward wave w after wave w+1 (its lane 63 needs beta of the unit above).
+// The neighbouring wave's values of a segment go through LDS, one per step,
+// and every wave passes one barrier per segment, active or not, so every wave
+// reaches the same barriers.  One unit per lane shortens a step's dependent
+// chain to one log-add; the stagger costs NW-1 segments per sweep.
+template <int K, int PF, int VAR, int MODE, bool DENSE_IN, int NW = 1>
+__global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
+  static_assert(NW >= 1 && NW <= 4, "one to four waves per sweep");
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   const int T = p.logit_lens[b];
@@ -143,6 +153,8 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
   const int U1 = p.U_max + 1;
   const int ND = p.T_max + p.U_max;  // diagonals of the lattice form
   const double kNaN = __builtin_nan("");
+  // the neighbouring wave's value of each step of a segment, two segments in turn
+  __shared__ double s_xch[NW > 1 ? NW - 1 : 1][2][PF];
 
   bool ok = (T >= 1 && T <= p.T_max && U >= 0 && U <= p.U_max);
   int bad = 0;
@@ -155,7 +167,7 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
   bad = __syncthreads_or(bad);
   // both sweeps of an utterance reach the same verdict and store the same values
   if (tid == 0) p.status[b] = (ok && !bad) ? 0 : 1;
-  if (!ok || bad) {
+  if (!ok || bad) {  // the whole block leaves together
     if (tid == 0) {
       p.lnp2_fwd[b] = kNaN;
       p.lnp2_bwd[b] = kNaN;
@@ -164,10 +176,13 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
     return;
   }
 
-  const int wave = blockIdx.y;  // 0: forward, 1: backward (a block of its own, one wavefront)
-  const int lane = tid;
-  const int D = T - 1 + U;  // last diagonal
-  const int owner_top = U / K;  // lane owning u = U
+  const int sweep = blockIdx.y;  // 0: forward, 1: backward (a block of its own)
+  const int lane = tid % kWave;
+  const int wv = (NW == 1) ? 0 : __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int ub = wv * kWave * K;  // this wave's first unit
+  const int D = T - 1 + U;        // last diagonal
+  // the lane owning u = U, in the wave owning it
+  const bool owns_top = (U / (kWave * K) == wv) && lane == (U - ub) / K;
   // weights of cell (e, u) clamped into the utterance: diagonal into [0, D], then the
   // unit into [e - (T-1), min(e, U)] (t = e - u in [0, T-1]); the row pointer is wave-uniform
   const double2* __restrict__ w_utt = p.lp2 + static_cast<int64_t>(b) * p.T_max * U1;
@@ -176,12 +191,12 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
   auto load_w = [&](int e, int k, double& wb, double& wl) {
     if (!DENSE_IN) {
       const int ec = min(max(e, 0), D);
-      const int uc = min(max(lane * K + k, ec - (T - 1)), min(ec, U));
+      const int uc = min(max(ub + lane * K + k, ec - (T - 1)), min(ec, U));
       const double2 w = load_lattice_cell(w_rsrc, 16 * ec * U1, uc, neg_step);  // row (t, u) = (ec - uc, uc)
       wb = w.x;
       wl = w.y;
     } else {
-      load_cell<true>(p, b, e, lane * K + k, T, U, D, wb, wl);
+      load_cell<true>(p, b, e, ub + lane * K + k, T, U, D, wb, wl);
     }
   };
   // score rows: diagonals 0..D, then spare rows up to ND
@@ -191,8 +206,11 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
   // (the host keeps (T_max + U_max + 1) * u_pad * 8 under 2^31), the lane's fixed
   const __amdgpu_buffer_rsrc_t a_rsrc = make_buffer(a_utt, static_cast<int64_t>(ND + 1) * p.u_pad * 8);
   const __amdgpu_buffer_rsrc_t b_rsrc = make_buffer(b_utt, static_cast<int64_t>(ND + 1) * p.u_pad * 8);
-  const int lane_off = lane * K * 8;
+  const int lane_off = (ub + lane * K) * 8;
   const int row_bytes = p.u_pad * 8;
+  // segments of PF steps in a sweep of D steps, and the barriers every wave passes
+  const int n_seg = (D + PF - 1) / PF;
+  const int n_rounds = n_seg + NW - 1;
 
   // weight of the closing blank, lp_blank(T-1, U)
   double w_close, w_unused;
@@ -203,18 +221,18 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
     w_close = to_lattice(w_close, true);
   }
 
-  if (wave == 0) {
+  if (sweep == 0) {
     // ---------------- forward sweep ----------------
     double a[K];
 #pragma unroll
-    for (int k = 0; k < K; ++k) a[k] = (lane * K + k == 0) ? 0.0 : kNoArc;
+    for (int k = 0; k < K; ++k) a[k] = (ub + lane * K + k == 0) ? 0.0 : kNoArc;
     double acc_top = kNoArc;                   // log-sum of alpha(t, U), t <= T-2
     double a_top = (U == 0) ? 0.0 : kNoArc;    // alpha(T-1, U) once the sweep reaches D
-    // the shifted-in neighbour; lane 0 gets none from the shift and keeps kNoArc
-    // from here on, so no fill value is set up in each step
+    // the shifted-in neighbour; lane 0 of wave 0 gets none from the shift and keeps
+    // kNoArc from here on, so no fill value is set up in each step
     double left_carry = kNoArc;
     if (VAR != 0 && U == 0 && T >= 2) acc_top = 0.0;  // alpha(0, U) itself when U = 0
-    if (MODE != kLossOnly && lane == 0) a_utt[0] = 0.0;
+    if (MODE != kLossOnly && wv == 0 && lane == 0) a_utt[0] = 0.0;
 
     double rb[PF][K], rl[PF][K];
 #pragma unroll
@@ -224,63 +242,80 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
       __builtin_amdgcn_sched_barrier(0);  // issue order = use order (oldest first)
     }
 
-    // whole blocks of PF steps, no branch around loads or stores; the up to PF-1
+    // whole segments of PF steps, no branch around loads or stores; the up to PF-1
     // steps past D touch only nodes outside the utterance and store into spare rows
-    for (int d0 = 1; d0 <= D; d0 += PF) {
+    for (int r = 0; r < n_rounds; ++r) {
+      const int g = r - wv;  // this wave's segment in round r
+      if (g >= 0 && g < n_seg) {
+        const int d0 = 1 + g * PF;
+        // the wave before wrote this segment's values in the previous round: all of them
+        // are read at once, so no step waits on the LDS
+        double x_in[PF];
+        if (NW > 1 && wv > 0) {
 #pragma unroll
-      for (int s = 0; s < PF; ++s) {
-        const int d = d0 + s;  // slot s holds the weights of diagonal d-1
-        double eb[K], el[K];
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-          double wb = rb[s][k], wl = rl[s][k];
-          if (DENSE_IN) {
-            const int u = lane * K + k, t = d - 1 - u;
-            wb = to_lattice(wb, t < T - 1 || u == U);
-            wl = to_lattice(wl, u < U);
-          }
-          eb[k] = a[k] + wb;
-          el[k] = a[k] + wl;
+          for (int s = 0; s < PF; ++s) x_in[s] = s_xch[max(wv - 1, 0)][(r - 1) & 1][s];
         }
-        left_carry = wave_shift_up(el[K - 1], left_carry);
-        const double left = left_carry;
 #pragma unroll
-        for (int k = 0; k < K; ++k) a[k] = log_add2(eb[k], k == 0 ? left : el[k > 0 ? k - 1 : 0]);
-        // wave-uniform conditions on the diagonal; no memory access inside
-        if (VAR != 0 && d <= T - 1 && lane == 0) a[0] = log_add2(a[0], 0.0);  // (0,0)->(d,0)
-        if (__builtin_expect(d == D, 0)) {  // once per sweep: a branch, not selects in every step
-          if (VAR == 1) {
+        for (int s = 0; s < PF; ++s) {
+          const int d = d0 + s;  // slot s holds the weights of diagonal d-1
+          double eb[K], el[K];
 #pragma unroll
-            for (int k = 0; k < K; ++k)
-              if (lane * K + k == U) a[k] = log_add2(a[k], acc_top);  // (t,U)->(T-1,U)
+          for (int k = 0; k < K; ++k) {
+            double wb = rb[s][k], wl = rl[s][k];
+            if (DENSE_IN) {
+              const int u = ub + lane * K + k, t = d - 1 - u;
+              wb = to_lattice(wb, t < T - 1 || u == U);
+              wl = to_lattice(wl, u < U);
+            }
+            eb[k] = a[k] + wb;
+            el[k] = a[k] + wl;
           }
-          a_top = at_unit(a, lane, U, a_top);
-        }
-        if (VAR != 0 && d >= U && d - U <= T - 2) acc_top = log_add2(acc_top, at_unit(a, lane, U, kNoArc));  // alpha(d-U, U)
-        if (MODE != kLossOnly)  // the row offset is uniform; readfirstlane keeps it in a scalar register
-          store_scores<K>(a_rsrc, lane_off, __builtin_amdgcn_readfirstlane(min(d, D + 1) * row_bytes), a);
+          if (NW > 1 && wv < NW - 1 && lane == kWave - 1) s_xch[wv][r & 1][s] = el[K - 1];  // for wave wv+1
+          // lane 0 of a later wave takes the unit below it from the wave before, one segment old
+          const double fill = (NW > 1 && wv > 0) ? x_in[s] : left_carry;
+          left_carry = wave_shift_up(el[K - 1], fill);
+          const double left = left_carry;
 #pragma unroll
-        for (int k = 0; k < K; ++k) load_w(d - 1 + PF, k, rb[s][k], rl[s][k]);
-        __builtin_amdgcn_sched_barrier(0);  // the prefetch stays PF steps ahead of its use
+          for (int k = 0; k < K; ++k) a[k] = log_add2(eb[k], k == 0 ? left : el[k > 0 ? k - 1 : 0]);
+          // wave-uniform conditions on the diagonal; no memory access inside
+          if (VAR != 0 && d <= T - 1 && wv == 0 && lane == 0) a[0] = log_add2(a[0], 0.0);  // (0,0)->(d,0)
+          if (__builtin_expect(d == D, 0)) {  // once per sweep: a branch, not selects in every step
+            if (VAR == 1) {
+#pragma unroll
+              for (int k = 0; k < K; ++k)
+                if (ub + lane * K + k == U) a[k] = log_add2(a[k], acc_top);  // (t,U)->(T-1,U)
+            }
+            a_top = at_unit(a, lane, U - ub, a_top);
+          }
+          if (VAR != 0 && d >= U && d - U <= T - 2)
+            acc_top = log_add2(acc_top, at_unit(a, lane, U - ub, kNoArc));  // alpha(d-U, U)
+          if (MODE != kLossOnly)  // the row offset is uniform; readfirstlane keeps it in a scalar register
+            store_scores<K>(a_rsrc, lane_off, __builtin_amdgcn_readfirstlane(min(d, D + 1) * row_bytes), a);
+#pragma unroll
+          for (int k = 0; k < K; ++k) load_w(d - 1 + PF, k, rb[s][k], rl[s][k]);
+          __builtin_amdgcn_sched_barrier(0);  // the prefetch stays PF steps ahead of its use
+        }
       }
+      if (NW > 1) __syncthreads();  // the segment's values reach the next wave
     }
-    if (lane == owner_top) {
+    if (owns_top) {
       double lnP2 = a_top + w_close;
       if (VAR == 2) lnP2 = log_add2(lnP2, acc_top);  // (t,U)->final
       p.lnp2_fwd[b] = lnP2;
       if (p.loss_f32) p.loss_f32[b] = static_cast<float>(-lnP2 / kLog2eD);
     }
-  } else if (MODE != kLossOnly && wave == 1) {
+  } else if (MODE != kLossOnly && sweep == 1) {
     // ---------------- backward sweep ----------------
     double bv[K];
 #pragma unroll
-    for (int k = 0; k < K; ++k) bv[k] = (lane * K + k == U) ? w_close : kNoArc;
+    for (int k = 0; k < K; ++k) bv[k] = (ub + lane * K + k == U) ? w_close : kNoArc;
     const double b_top = w_close;  // beta(T-1, U)
     double acc0 = kNoArc;          // log-sum of beta(t, 0), t >= 1
     if (VAR != 0 && U == 0 && T >= 2) acc0 = w_close;
-    if (lane == owner_top) b_utt[static_cast<int64_t>(D) * p.u_pad + U] = w_close;
+    if (owns_top) b_utt[static_cast<int64_t>(D) * p.u_pad + U] = w_close;
     double b00 = (D == 0) ? w_close : kNoArc;  // beta(0,0)
-    double right_carry = kNoArc;  // lane 63 keeps kNoArc (see left_carry)
+    double right_carry = kNoArc;  // lane 63 of the last wave keeps kNoArc (see left_carry)
+    const int lag = NW - 1 - wv;  // the last wave goes first
 
     double rb[PF][K], rl[PF][K];
 #pragma unroll
@@ -290,44 +325,57 @@ __global__ __launch_bounds__(64) void k2_lattice(LatticeParams p) {
       __builtin_amdgcn_sched_barrier(0);  // issue order = use order (oldest first)
     }
 
-    for (int d0 = D - 1; d0 >= 0; d0 -= PF) {
+    for (int r = 0; r < n_rounds; ++r) {
+      const int g = r - lag;
+      if (g >= 0 && g < n_seg) {
+        const int d0 = D - 1 - g * PF;
+        double x_in[PF];  // the wave after wrote them in the previous round (see the forward sweep)
+        if (NW > 1 && wv < NW - 1) {
 #pragma unroll
-      for (int s = 0; s < PF; ++s) {
-        const int d = d0 - s;  // slot s holds the weights of diagonal d (d < 0: no node)
-        right_carry = wave_shift_down(bv[0], right_carry);
-        const double right = right_carry;
-        double nb[K];
+          for (int s = 0; s < PF; ++s) x_in[s] = s_xch[wv][(r - 1) & 1][s];
+        }
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-          double wb = rb[s][k], wl = rl[s][k];
-          if (DENSE_IN) {
-            const int u = lane * K + k, t = d - u;
-            wb = to_lattice(wb, t < T - 1 || u == U);
-            wl = to_lattice(wl, u < U);
+        for (int s = 0; s < PF; ++s) {
+          const int d = d0 - s;  // slot s holds the weights of diagonal d (d < 0: no node)
+          if (NW > 1 && wv > 0 && lane == 0) s_xch[max(wv - 1, 0)][r & 1][s] = bv[0];  // for wave wv-1
+          // lane 63 of an earlier wave takes the unit above it from the wave after, one segment old
+          const double fill = (NW > 1 && wv < NW - 1) ? x_in[s] : right_carry;
+          right_carry = wave_shift_down(bv[0], fill);
+          const double right = right_carry;
+          double nb[K];
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            double wb = rb[s][k], wl = rl[s][k];
+            if (DENSE_IN) {
+              const int u = ub + lane * K + k, t = d - u;
+              wb = to_lattice(wb, t < T - 1 || u == U);
+              wl = to_lattice(wl, u < U);
+            }
+            const double xb = wb + bv[k];
+            const double xl = wl + (k == K - 1 ? right : bv[k + 1 < K ? k + 1 : k]);
+            nb[k] = log_add2(xb, xl);
           }
-          const double xb = wb + bv[k];
-          const double xl = wl + (k == K - 1 ? right : bv[k + 1 < K ? k + 1 : k]);
-          nb[k] = log_add2(xb, xl);
-        }
-        if (VAR != 0 && d >= U && d - U <= T - 2) {  // wave-uniform: (d-U, U)->(T-1, U) or ->final
-          const double x = log_add2(at_unit(nb, lane, U, kNoArc), VAR == 1 ? b_top : 0.0);
+          if (VAR != 0 && d >= U && d - U <= T - 2) {  // wave-uniform: (d-U, U)->(T-1, U) or ->final
+            const double x = log_add2(at_unit(nb, lane, U - ub, kNoArc), VAR == 1 ? b_top : 0.0);
 #pragma unroll
-          for (int k = 0; k < K; ++k) nb[k] = (lane * K + k == U) ? x : nb[k];
-        }
-        if (__builtin_expect(d == 0, 0)) {  // wave-uniform, once per sweep: a branch, not selects
-          if (VAR != 0 && lane == 0) nb[0] = log_add2(nb[0], acc0);  // (0,0)->(t,0)
-          b00 = nb[0];
-        }
-        if (VAR != 0 && d >= 1 && d <= T - 1) acc0 = log_add2(acc0, nb[0]);  // beta(d, 0), lane 0
+            for (int k = 0; k < K; ++k) nb[k] = (ub + lane * K + k == U) ? x : nb[k];
+          }
+          if (__builtin_expect(d == 0, 0)) {  // wave-uniform, once per sweep: a branch, not selects
+            if (VAR != 0 && wv == 0 && lane == 0) nb[0] = log_add2(nb[0], acc0);  // (0,0)->(t,0)
+            b00 = nb[0];
+          }
+          if (VAR != 0 && d >= 1 && d <= T - 1) acc0 = log_add2(acc0, nb[0]);  // beta(d, 0), lane 0 of wave 0
 #pragma unroll
-        for (int k = 0; k < K; ++k) bv[k] = nb[k];
-        store_scores<K>(b_rsrc, lane_off, __builtin_amdgcn_readfirstlane((d >= 0 ? d : ND) * row_bytes), nb);
+          for (int k = 0; k < K; ++k) bv[k] = nb[k];
+          store_scores<K>(b_rsrc, lane_off, __builtin_amdgcn_readfirstlane((d >= 0 ? d : ND) * row_bytes), nb);
 #pragma unroll
-        for (int k = 0; k < K; ++k) load_w(d - PF, k, rb[s][k], rl[s][k]);
-        __builtin_amdgcn_sched_barrier(0);  // the prefetch stays PF steps ahead of its use
+          for (int k = 0; k < K; ++k) load_w(d - PF, k, rb[s][k], rl[s][k]);
+          __builtin_amdgcn_sched_barrier(0);  // the prefetch stays PF steps ahead of its use
+        }
       }
+      if (NW > 1) __syncthreads();  // the segment's values reach the previous wave
     }
-    if (lane == 0) p.lnp2_bwd[b] = b00;
+    if (wv == 0 && lane == 0) p.lnp2_bwd[b] = b00;
   }
 }
 

@@ -16,21 +16,33 @@ namespace {  // each including unit keeps its own copy
 
 // ---- kernel 2 ---------------------------------------------------------------
 
-template <int K, int VAR, int MODE, bool DENSE_IN>
+template <int K, int VAR, int MODE, bool DENSE_IN, int NW = 1>
 hipError_t launch_k2_k(const LatticeParams& p, hipStream_t stream) {
   constexpr int PF = (K >= 24) ? 1 : (K >= 16) ? 2 : (48 / K > 24 ? 24 : 48 / K);  // diagonals of weights in flight
   const int sweeps = (MODE == kLossOnly) ? 1 : 2;  // forward only, or forward and backward
-  hipLaunchKernelGGL((k2_lattice<K, PF, VAR, MODE, DENSE_IN>), dim3(p.B, sweeps), dim3(64), 0, stream, p);
+  hipLaunchKernelGGL((k2_lattice<K, PF, VAR, MODE, DENSE_IN, NW>), dim3(p.B, sweeps), dim3(64 * NW), 0, stream, p);
   return hipGetLastError();
 }
 
+// Up to 256 units a sweep takes one unit per lane over as many wavefronts as it
+// needs (the score rows keep the same 64 * units_per_lane columns); wider
+// lattices take one wavefront with several units per lane.
+#ifndef RNNT_K2_MULTI_WAVE
+#define RNNT_K2_MULTI_WAVE 1
+#endif
 template <int VAR, int MODE, bool DENSE_IN>
 hipError_t launch_k2_v(const LatticeParams& p, hipStream_t stream) {
   switch (units_per_lane(p.U_max + 1)) {
     case 1: return launch_k2_k<1, VAR, MODE, DENSE_IN>(p, stream);
+#if RNNT_K2_MULTI_WAVE
+    case 2: return launch_k2_k<1, VAR, MODE, DENSE_IN, 2>(p, stream);
+    case 3: return launch_k2_k<1, VAR, MODE, DENSE_IN, 3>(p, stream);
+    case 4: return launch_k2_k<1, VAR, MODE, DENSE_IN, 4>(p, stream);
+#else
     case 2: return launch_k2_k<2, VAR, MODE, DENSE_IN>(p, stream);
     case 3: return launch_k2_k<3, VAR, MODE, DENSE_IN>(p, stream);
     case 4: return launch_k2_k<4, VAR, MODE, DENSE_IN>(p, stream);
+#endif
     case 6: return launch_k2_k<6, VAR, MODE, DENSE_IN>(p, stream);
     case 8: return launch_k2_k<8, VAR, MODE, DENSE_IN>(p, stream);
     case 12: return launch_k2_k<12, VAR, MODE, DENSE_IN>(p, stream);

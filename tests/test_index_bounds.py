@@ -14,10 +14,23 @@ import pytest
 
 from paper_2303_10384_amd.workloads import WORKLOADS
 
-_K1_SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
-                       "paper_2303_10384_amd", "csrc", "rnnt_k1_populate.h")
+_CSRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2303_10384_amd", "csrc")
+_K1_SRC = os.path.join(_CSRC, "rnnt_k1_populate.h")
 # consecutive populate blocks per XCD turn, as the kernel source defines it
 K1_XCD_RUN = int(re.search(r"#define RNNT_K1_XCD_RUN (\d+)", open(_K1_SRC).read()).group(1))
+# whether sweeps of 65..256 units run one unit per lane over several wavefronts
+K2_MULTI_WAVE = int(re.search(r"#define RNNT_K2_MULTI_WAVE (\d+)",
+                              open(os.path.join(_CSRC, "rnnt_launch_k2.h")).read()).group(1))
+
+
+def units_per_lane(U1):
+    return next(k for k in (1, 2, 3, 4, 6, 8, 12, 16, 24, 32) if U1 <= 64 * k)
+
+
+def sweep_shape(U1):
+    """(wavefronts per sweep, units per lane) of the lattice sweeps."""
+    K = units_per_lane(U1)
+    return (K, 1) if K2_MULTI_WAVE and K in (2, 3, 4) else (1, K)
 
 EPC = {"f32": 4, "bf16": 8, "f16": 8}
 SHAPES = [(w.B, w.T_max, w.U_max, w.V, w.dtype) for w in WORKLOADS.values()] + [
@@ -147,11 +160,12 @@ def test_lattice_kernel_addresses(B, T, U, V, dt):
     u_pad = 64*K wide; the posterior kernel reads alpha, beta only at diagonals <= D."""
     U1 = U + 1
     ND = T + U
-    K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16, 24, 32) if U1 <= 64 * k)
-    u_pad = 64 * K
+    NW, K = sweep_shape(U1)
+    u_pad = 64 * units_per_lane(U1)
+    assert NW * 64 * K == u_pad  # unit u in column u whatever the waves
     n_cells = B * T * U1  # kernel 1's lattice form: one cell per logits row
     n_scores = B * (ND + 1) * u_pad
-    lanes = np.arange(64)
+    lanes = np.concatenate([w * 64 * K + np.arange(64) * K for w in range(NW)])  # each lane's first unit
     for Tb, Ub in [(T, U), (1, 0), (max(1, T // 2), U // 2), (1, U), (T, 0)]:
         D = Tb - 1 + Ub
         PF = 1 if K >= 24 else 2 if K >= 16 else min(24, 48 // K)
@@ -159,7 +173,7 @@ def test_lattice_kernel_addresses(B, T, U, V, dt):
             for e in range(-PF - 2, D + PF + 2):  # every diagonal a load or store step can name
                 ec = min(max(e, 0), D)
                 for k in range(K):
-                    uc = np.minimum(np.maximum(lanes * K + k, ec - (Tb - 1)), min(ec, Ub))
+                    uc = np.minimum(np.maximum(lanes + k, ec - (Tb - 1)), min(ec, Ub))
                     tc = ec - uc
                     assert np.all((tc >= 0) & (tc < Tb) & (uc >= 0) & (uc <= Ub))  # a cell kernel 1 wrote
                     w = (bb * T + tc) * U1 + uc  # row (t, u) of utterance bb
@@ -170,10 +184,53 @@ def test_lattice_kernel_addresses(B, T, U, V, dt):
                     if -PF + 1 <= e <= D - 1:  # backward steps d = D-1 .. (last block's end)
                         rows.append(e if e >= 0 else ND)
                     for row in rows:
-                        a = (bb * (ND + 1) + row) * u_pad + lanes * K + k
+                        a = (bb * (ND + 1) + row) * u_pad + lanes + k
                         assert np.all(a >= 0) and np.all(a < n_scores)
         # spare rows never overlap the rows the posterior kernel reads (d <= D)
         assert D + 1 <= ND
+
+
+@pytest.mark.parametrize("NW", [2, 3, 4])
+@pytest.mark.parametrize("D", [0, 1, 23, 24, 25, 47, 48, 330, 649])
+def test_lattice_multi_wave_schedule(NW, D):
+    """Several wavefronts per sweep: wave w runs segment g = r - lag(w) of PF steps in round r
+    (lag w forward, NW-1-w backward) and every wave passes one barrier per round.  Each value a
+    wave takes from its neighbour (slot [pair][r-1 & 1][s] in round r) was written by that
+    neighbour in round r-1 for the same diagonal, and is not overwritten before it is read; the
+    LDS slots stay inside [NW-1][2][PF]."""
+    PF = 24  # one unit per lane
+    n_seg = (D + PF - 1) // PF
+    n_rounds = n_seg + NW - 1
+    for sweep in ("forward", "backward"):
+        writes = {}  # (pair, half, s) -> list of (round, diagonal)
+        reads = []   # (round, pair, half, s, diagonal)
+        active = {w: 0 for w in range(NW)}
+        for r in range(n_rounds):  # the same trip count for every wave: equal barrier counts
+            for w in range(NW):
+                lag = w if sweep == "forward" else NW - 1 - w
+                g = r - lag
+                if not (0 <= g < n_seg):
+                    continue
+                active[w] += 1
+                for s in range(PF):
+                    d = 1 + g * PF + s if sweep == "forward" else D - 1 - g * PF - s
+                    producer = w < NW - 1 if sweep == "forward" else w > 0
+                    consumer = w > 0 if sweep == "forward" else w < NW - 1
+                    if producer:
+                        pair = w if sweep == "forward" else w - 1
+                        assert 0 <= pair < NW - 1
+                        writes.setdefault((pair, r & 1, s), []).append((r, d))
+                    if consumer:
+                        pair = w - 1 if sweep == "forward" else w
+                        assert 0 <= pair < NW - 1
+                        reads.append((r, pair, (r - 1) & 1, s, d))
+        assert all(n == n_seg for n in active.values())  # every wave runs every segment once
+        for r, pair, half, s, d in reads:
+            # the latest write to the slot before round r: made in round r-1, for diagonal d
+            before = [(rw, dw) for rw, dw in writes.get((pair, half, s), []) if rw < r]
+            assert before and before[-1] == (r - 1, d)
+            # and the next write to that slot comes after round r's barrier
+            assert all(rw > r for rw, _ in writes[(pair, half, s)] if rw >= r)
 
 
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
