@@ -15,7 +15,10 @@
 // Schedule: the nodes of an anti-diagonal d = t + u depend only on diagonal
 // d-1 (forward) or d+1 (backward).  One wavefront sweeps the diagonals, lane j
 // owning the K consecutive units u = K*j .. K*j+K-1, so a step exchanges one
-// value with the neighbouring lane (a DPP whole-wave shift).  The forward and
+// value with the neighbouring lane (a DPP whole-wave shift); from 65 to 256
+// units, two to four wavefronts with one unit per lane do, staggered by a
+// segment of steps and exchanging their boundary values through LDS (see the
+// kernel's NW parameter).  The forward and
 // backward waves of an utterance run concurrently, each a one-wavefront block of
 // its own (blockIdx.y), so that the two chains do not share a compute unit.  The weights of
 // the next PF diagonals stay in flight in registers (one load per unit and
