@@ -156,8 +156,11 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
   const int U1 = p.U_max + 1;
   const int ND = p.T_max + p.U_max;  // diagonals of the lattice form
   const double kNaN = __builtin_nan("");
-  // the neighbouring wave's value of each step of a segment, two segments in turn
+  // the neighbouring wave's value of each step of a segment, two segments in turn;
+  // every lane writes each step (no exec mask), the lanes without a value to pass
+  // into a scratch run of their own (lane + step: no two lanes of a write collide)
   __shared__ double s_xch[NW > 1 ? NW - 1 : 1][2][PF];
+  __shared__ double s_sink[NW > 1 ? kWave + PF : 1];
 
   bool ok = (T >= 1 && T <= p.T_max && U >= 0 && U <= p.U_max);
   int bad = 0;
@@ -190,11 +193,16 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
   // unit into [e - (T-1), min(e, U)] (t = e - u in [0, T-1]); the row pointer is wave-uniform
   const double2* __restrict__ w_utt = p.lp2 + static_cast<int64_t>(b) * p.T_max * U1;
   const __amdgpu_buffer_rsrc_t w_rsrc = make_buffer(w_utt, static_cast<int64_t>(p.T_max) * U1 * 16);
-  const int neg_step = -16 * (U1 - 1);
+  // the per-unit factor in a vector register, so the offset's multiply-add takes the
+  // row term as its one scalar operand
+  int neg_step;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(neg_step) : "s"(-16 * (U1 - 1)));
   auto load_w = [&](int e, int k, double& wb, double& wl) {
     if (!DENSE_IN) {
       const int ec = min(max(e, 0), D);
-      const int uc = min(max(ub + lane * K + k, ec - (T - 1)), min(ec, U));
+      // the unit's upper clamp as one scalar (a min against two scalars costs a vector move)
+      const int hi = __builtin_amdgcn_readfirstlane(min(ec, U));
+      const int uc = min(max(ub + lane * K + k, ec - (T - 1)), hi);
       const double2 w = load_lattice_cell(w_rsrc, 16 * ec * U1, uc, neg_step);  // row (t, u) = (ec - uc, uc)
       wb = w.x;
       wl = w.y;
@@ -244,6 +252,9 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
       for (int k = 0; k < K; ++k) load_w(s, k, rb[s][k], rl[s][k]);
       __builtin_amdgcn_sched_barrier(0);  // issue order = use order (oldest first)
     }
+    double x_in[PF];  // the fill of lane 0 in each step of a segment (several waves)
+#pragma unroll
+    for (int s = 0; s < PF; ++s) x_in[s] = kNoArc;
 
     // whole segments of PF steps, no branch around loads or stores; the up to PF-1
     // steps past D touch only nodes outside the utterance and store into spare rows
@@ -252,12 +263,14 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
       if (g >= 0 && g < n_seg) {
         const int d0 = 1 + g * PF;
         // the wave before wrote this segment's values in the previous round: all of them
-        // are read at once, so no step waits on the LDS
-        double x_in[PF];
+        // are read at once, so no step waits on the LDS (wave 0's lane 0 takes kNoArc)
         if (NW > 1 && wv > 0) {
 #pragma unroll
           for (int s = 0; s < PF; ++s) x_in[s] = s_xch[max(wv - 1, 0)][(r - 1) & 1][s];
         }
+        // lane 63 writes into this round's slots for the next wave, the others into the sink
+        double* const x_out = (lane == kWave - 1 && wv < NW - 1) ? &s_xch[min(wv, NW > 1 ? NW - 2 : 0)][r & 1][0]
+                                                                  : &s_sink[NW > 1 ? lane : 0];
 #pragma unroll
         for (int s = 0; s < PF; ++s) {
           const int d = d0 + s;  // slot s holds the weights of diagonal d-1
@@ -273,9 +286,9 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
             eb[k] = a[k] + wb;
             el[k] = a[k] + wl;
           }
-          if (NW > 1 && wv < NW - 1 && lane == kWave - 1) s_xch[wv][r & 1][s] = el[K - 1];  // for wave wv+1
+          if (NW > 1) x_out[s] = el[K - 1];  // lane 63's for wave wv+1
           // lane 0 of a later wave takes the unit below it from the wave before, one segment old
-          const double fill = (NW > 1 && wv > 0) ? x_in[s] : left_carry;
+          const double fill = (NW > 1) ? x_in[s] : left_carry;
           left_carry = wave_shift_up(el[K - 1], fill);
           const double left = left_carry;
 #pragma unroll
@@ -327,22 +340,26 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
       for (int k = 0; k < K; ++k) load_w(D - 1 - s, k, rb[s][k], rl[s][k]);
       __builtin_amdgcn_sched_barrier(0);  // issue order = use order (oldest first)
     }
+    double x_in[PF];  // the fill of lane 63 in each step of a segment (several waves)
+#pragma unroll
+    for (int s = 0; s < PF; ++s) x_in[s] = kNoArc;
 
     for (int r = 0; r < n_rounds; ++r) {
       const int g = r - lag;
       if (g >= 0 && g < n_seg) {
         const int d0 = D - 1 - g * PF;
-        double x_in[PF];  // the wave after wrote them in the previous round (see the forward sweep)
+        // the wave after wrote them in the previous round (see the forward sweep)
         if (NW > 1 && wv < NW - 1) {
 #pragma unroll
-          for (int s = 0; s < PF; ++s) x_in[s] = s_xch[wv][(r - 1) & 1][s];
+          for (int s = 0; s < PF; ++s) x_in[s] = s_xch[min(wv, NW > 1 ? NW - 2 : 0)][(r - 1) & 1][s];
         }
+        double* const x_out = (lane == 0 && wv > 0) ? &s_xch[max(wv - 1, 0)][r & 1][0] : &s_sink[NW > 1 ? lane : 0];
 #pragma unroll
         for (int s = 0; s < PF; ++s) {
           const int d = d0 - s;  // slot s holds the weights of diagonal d (d < 0: no node)
-          if (NW > 1 && wv > 0 && lane == 0) s_xch[max(wv - 1, 0)][r & 1][s] = bv[0];  // for wave wv-1
+          if (NW > 1) x_out[s] = bv[0];  // lane 0's for wave wv-1
           // lane 63 of an earlier wave takes the unit above it from the wave after, one segment old
-          const double fill = (NW > 1 && wv < NW - 1) ? x_in[s] : right_carry;
+          const double fill = (NW > 1) ? x_in[s] : right_carry;
           right_carry = wave_shift_down(bv[0], fill);
           const double right = right_carry;
           double nb[K];
