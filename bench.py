@@ -396,8 +396,8 @@ def main():
                          "known-size copy that calibrates the HBM byte counters), then exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the loss has no multi-GPU path in this build "
-              "(utterances are independent; see the design notes on batch sharding). Use --gpus 1.",
+        print("bench.py measures one GPU: the library has no multi-GPU path (utterances are "
+              "independent, so a batch shards by utterance across processes). Use --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
 

@@ -59,7 +59,7 @@ typedef enum {
   RNNT_ERR_WORKSPACE = 6,    /* workspace given but smaller than required        */
   RNNT_ERR_ALIGNMENT = 7,    /* logits or grad not 16-byte aligned               */
   RNNT_ERR_HIP = 8,          /* a HIP runtime call failed (launch, allocation)   */
-  RNNT_ERR_UNSUPPORTED = 9,  /* shape outside what this build handles (U_max+1 > 2048,
+  RNNT_ERR_UNSUPPORTED = 9,  /* shape outside what the library handles (U_max+1 > 2048,
                                 T_max * (U_max+1) >= 2^27, or an arc-list lattice
                                 beyond the sweep's limits)                          */
   RNNT_ERR_BAD_LATTICE = 10, /* an arc list that breaks the numbering rules of

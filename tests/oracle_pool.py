@@ -33,7 +33,7 @@ def utterance_ref(job):
 
 
 def workers():
-    """Pool size: the process's CPUs, at most 16 (a GPU machine's CPU share)."""
+    """Pool size: the process's CPUs, at most 16 (the CPU share that goes with one GPU)."""
     return max(1, min(16, len(os.sched_getaffinity(0))))
 
 

@@ -40,7 +40,7 @@ FIGS = [
 ]
 
 
-def test_golden_values_are_the_survey_pins():
+def test_golden_values_are_the_hand_computed_pins():
     """Stored losses equal the values computed from the printed weights."""
     e = expected()
     assert e["rnnt_fig1"]["loss"] == pytest.approx(4.2574511041, abs=1e-10)
