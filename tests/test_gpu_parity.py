@@ -327,12 +327,17 @@ def test_large_vocabulary(torch, pkg, dtype, V, blank):
     tol_check(loss, grad, loss_ref, grad_ref, dtype, tl, ul)
 
 
-def test_loss_only_matches_fused(torch, pkg):
-    logits, tl, ul, labels = W.small_case(4, 12, 9, 40, seed=11)
-    a, _, _ = run_case(torch, pkg, logits, tl, ul, labels, need_grad=False)
-    b, g, _ = run_case(torch, pkg, logits, tl, ul, labels, need_grad=True)
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("B,T,U,seed", [(4, 12, 9, 11), (3, 9, 100, 13), (2, 7, 150, 14), (2, 5, 230, 15)])
+def test_loss_only_matches_fused(torch, pkg, variant, B, T, U, seed):
+    # one sweep wave, and two, three and four waves per sweep (65 to 256 units)
+    logits, tl, ul, labels = W.small_case(B, T, U, 40, seed=seed)
+    a, _, seen = run_case(torch, pkg, logits, tl, ul, labels, variant=variant, need_grad=False)
+    b, g, _ = run_case(torch, pkg, logits, tl, ul, labels, variant=variant, need_grad=True)
     assert g is not None
     np.testing.assert_array_equal(a, b)
+    loss_ref, _ = R.rnnt_loss_grad(seen, labels, tl, ul, 0, variant, need_grad=False)
+    tol_check(a, None, loss_ref, None, "f32")
 
 
 def test_bad_data_is_isolated(torch, pkg):
