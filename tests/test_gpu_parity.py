@@ -318,6 +318,20 @@ def test_wide_label_axis(torch, pkg, dtype, variant, B, T, U, V, seed):
     tol_check(loss, grad, loss_ref, grad_ref, dtype, tl, ul, grad_dtype="f32")
 
 
+@pytest.mark.parametrize("variant", VARIANTS)
+def test_sweep_wave_boundaries(torch, pkg, variant):
+    # U_max + 1 = 151: three sweep waves of 64 units.  The utterances put u = U at and around
+    # the waves' edges (63, 64, 65, 127, 128) and at the ends (0, 1, 150), with one, two and
+    # several frames, so the last unit and the closing blank sit in every wave and lane 0 / 63
+    # of each wave exchange across the boundary.
+    logits, _, _, labels = W.small_case(12, 7, 150, 9, seed=31, sigma=2.0)
+    ul = np.array([0, 1, 63, 64, 65, 127, 128, 150, 64, 127, 0, 150], np.int32)
+    tl = np.array([7, 1, 2, 7, 3, 1, 7, 2, 1, 7, 1, 7], np.int32)
+    loss, grad, seen = run_case(torch, pkg, logits, tl, ul, labels, variant=variant)
+    loss_ref, grad_ref = R.rnnt_loss_grad(seen, labels, tl, ul, 0, variant)
+    tol_check(loss, grad, loss_ref, grad_ref, "f32", tl, ul)
+
+
 @pytest.mark.parametrize("dtype,V,blank", [("f32", 4100, 17), ("bf16", 8200, 8199), ("f16", 2600, 0)])
 def test_large_vocabulary(torch, pkg, dtype, V, blank):
     # rows longer than the populate kernel's register path (64 lanes x 5 chunks) take its batched path
