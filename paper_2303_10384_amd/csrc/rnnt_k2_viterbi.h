@@ -17,9 +17,10 @@
 // 1 when it is entered by its label arc, or at u = 0 by the initial wild-card
 // arc.  Each step stores, per lane slot k, the wave's ballot of those bits: one
 // 64-bit word per (diagonal, k), bit j for unit K*j + k.  The same wave then
-// walks back from the path's end, one diagonal per step, reading the words
-// through a window of 64 words held one per lane, with the next 64 words loaded
-// ahead (so no step waits on memory), and records each unit's frame in LDS.
+// walks back from the path's end one label move at a time, finding each unit's
+// entry diagonal among 64 at once (a ballot of that unit's bits over a block of
+// diagonals staged in LDS, the next block loaded ahead), and records each unit's
+// frame in LDS.
 #pragma once
 
 #include "rnnt_device.h"
@@ -40,12 +41,6 @@ struct ViterbiParams {
 };
 
 constexpr int kViterbiMaxUnits1 = 2048;
-
-__device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int lane) {
-  const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(x), lane);
-  const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(x >> 32), lane);
-  return (static_cast<uint64_t>(hi) << 32) | lo;
-}
 
 template <typename V>
 __device__ __forceinline__ V from_lane(V x, int lane) {
@@ -193,45 +188,66 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
 
   // ---------------- backtrace ----------------
   __syncthreads();  // the decision words stored above are read back below
-  int u = U, start_frame = 0;
-  // Two windows of 64 words, one per lane, in turn: the walk reads one while the next
-  // 64 words below load into the other (a copy between them would wait for that load).
-  // A step moves the word index down by at most 2K-1 < 64, so the walk leaves a window
-  // only into the next one.
-  auto load_window = [&](int lo) { return lo + lane >= 0 ? dec_utt[lo + lane] : uint64_t{0}; };
-  // walks while its word lies in [lo, lo + 64); true once (0,0) is reached or the path jumped
-  auto walk = [&](const uint64_t& win, int lo) {
-    while (t + u > 0) {
-      const unsigned uu = static_cast<unsigned>(u);  // u >= 0: unsigned division by K is a shift or a multiply
-      const int widx = (t + u) * K + static_cast<int>(uu % K);
-      if (widx < lo) return false;
-      const uint64_t wd = readlane_u64(win, widx - lo);
-      // the move, without branches and in integer 0/1 flags (scalar arithmetic; boolean
-      // flags went through a vector select and back): the label arc (t,u-1)->(t,u) (the
-      // only way into (0,u)) emits unit u at frame t; at u = 0 a set bit is the initial
-      // wild-card arc from (0,0).  t, u >= 0 here.
-      const unsigned bit = static_cast<unsigned>(wd >> (uu / K)) & 1u;
-      const unsigned u_pos = static_cast<unsigned>(-u) >> 31;      // u > 0
-      const unsigned t_zero = static_cast<unsigned>(t - 1) >> 31;  // t == 0
-      const int label = static_cast<int>(u_pos & (bit | t_zero));
-      const bool jumped = VAR != 0 && (bit & (u_pos ^ 1u)) != 0;
-      s_frames[label ? u - 1 : kViterbiMaxUnits1] = t;  // every lane the same value; a spare slot otherwise
-      start_frame = jumped ? t : start_frame;
-      u -= label;
-      t = jumped ? 0 : t - 1 + label;  // a jump ends the walk: (t,u) becomes (0,0)
+  // One step per label move: from node (d - u, u) the path runs down blank arcs (d
+  // falls, u stays) to the highest diagonal d' <= d whose node of unit u was entered by
+  // its label arc -- at t = 0 it always is -- emits unit u at frame d' - u and goes on
+  // from (d' - u, u - 1) on diagonal d' - 1.  Unit u's decision bits over a block of 64
+  // diagonals are one ballot: lane l reads the word of diagonal 64 w + l in column u % K
+  // (the block staged in LDS, one column per 64 words) and tests bit u / K.  At u = 0
+  // (W-Transducer) a set bit is the initial wild-card arc: the path starts there.  Each
+  // step lowers d, so the walk ends after at most U + D/64 + 1 steps.
+  __shared__ uint64_t s_blk[K][kWave];
+  const __amdgpu_buffer_rsrc_t dec_rsrc = make_buffer(dec_utt, static_cast<int64_t>(ND + 1) * K * 8);
+  // the words of diagonal 64 w + lane, all columns (0 past the stored rows)
+  auto load_block = [&](int w, uint64_t (&x)[K]) {
+    typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(dec_rsrc, ((kWave * w + lane) * K + k) * 8, 0, 0);
+      x[k] = (static_cast<uint64_t>(v.y) << 32) | v.x;
     }
-    return true;
   };
-  int lo = (t + u) * K + K - 64;
-  uint64_t win_a = load_window(lo);
-  uint64_t win_b = load_window(lo - 64);
-  while (true) {
-    if (walk(win_a, lo)) break;
-    lo -= 64;
-    win_a = load_window(lo - 64);
-    if (walk(win_b, lo)) break;
-    lo -= 64;
-    win_b = load_window(lo - 64);
+  int u = U, d = t + u, start_frame = 0;
+  int w = d / kWave;
+  uint64_t nxt[K];
+  load_block(w, nxt);
+#pragma unroll
+  for (int k = 0; k < K; ++k) s_blk[k][lane] = nxt[k];
+  if (w > 0) load_block(w - 1, nxt);  // the block below, in flight while this one is walked
+  while (d > 0 && (VAR != 0 || u > 0)) {
+    if (d < kWave * w) {  // one block down (a step lowers the block by at most one)
+      w -= 1;
+#pragma unroll
+      for (int k = 0; k < K; ++k) s_blk[k][lane] = nxt[k];
+      if (w > 0) load_block(w - 1, nxt);
+    }
+    const unsigned uu = static_cast<unsigned>(u);
+    const uint64_t col = s_blk[uu % K][lane];
+    const uint64_t bits = __ballot(static_cast<int>((col >> (uu / K)) & 1u));  // bit l: diagonal 64 w + l
+    const int base = kWave * w;
+    const int lo = max(u, 1) - base;  // t >= 0, and never diagonal 0 (node (0,0) has no decision)
+    const int hi = d - base;          // lo <= hi <= 63
+    const uint64_t m = bits & (~uint64_t{0} >> (63 - hi)) & (~uint64_t{0} << max(lo, 0));
+    if (u > 0) {
+      int dl;
+      if (m != 0) {
+        dl = base + 63 - __builtin_clzll(m);
+      } else if (u >= base) {
+        dl = u;  // t = 0: entered by its label arc
+      } else {
+        d = base - 1;  // no label move in this block
+        continue;
+      }
+      s_frames[u - 1] = dl - u;  // every lane the same value
+      u -= 1;
+      d = dl - 1;
+    } else {  // u = 0, W-Transducer: the initial wild-card arc into (t, 0), or (0, 0) itself
+      if (m != 0) {
+        start_frame = base + 63 - __builtin_clzll(m);
+        break;
+      }
+      d = base - 1;
+    }
   }
   __syncthreads();
   for (int i = lane; i < p.U_max; i += 64)
