@@ -289,13 +289,14 @@ def test_posterior_kernel_tiles_cover_every_row_once(B, T, U, V, dt):
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
 def test_viterbi_kernel_addresses(B, T, U, V, dt):
     """Forced-alignment kernel: decision words stored at row min(d, D+1), K words a row; the
-    backtrace's windows of 64 words start at w_lo = D_end*K + K - 64 and step down by 64, each load
-    (index w_lo + lane, skipped below 0) inside the utterance's (T_max+U_max+1)*K words, and every
-    word the walk reads lies in the current window."""
+    backtrace stages blocks of 64 diagonals, lane l loading the K words of diagonal 64 w + l at
+    byte offset ((64 w + l) K + k) * 8: never negative, and past the utterance's (T_max+U_max+1)*K
+    words only beyond the last row (a buffer load there reads 0), under 2^31 bytes."""
     U1 = U + 1
     ND = T + U
     K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16, 24, 32) if U1 <= 64 * k)
     words = (ND + 1) * K
+    lanes = np.arange(64)
     for Tb, Ub in [(T, U), (1, 0), (max(1, T // 2), U // 2), (1, U), (T, 0)]:
         D = Tb - 1 + Ub
         PF = 1 if K >= 24 else 2 if K >= 16 else min(24, 48 // K)
@@ -303,25 +304,82 @@ def test_viterbi_kernel_addresses(B, T, U, V, dt):
             row = min(d, D + 1)
             for lane in range(64):
                 assert 0 <= row * K + min(lane, K - 1) < words
-        # a walk that takes every label move first, then every blank move (and the reverse)
-        for labels_first in (True, False):
-            t, u = Tb - 1, Ub
-            w_lo = (t + u) * K + K - 64
+        for w in range(D // 64 + 1):
+            for k in range(K):
+                idx = (64 * w + lanes) * K + k
+                assert np.all(idx >= 0) and np.all(idx * 8 < 2 ** 31)
+                # a word past the stored rows is a diagonal past ND: masked off by the walk (d <= D)
+                assert np.all((idx < words) | (64 * w + lanes > ND))
 
-            def window_ok(lo):
-                idx = lo + np.arange(64)
-                idx = idx[idx >= 0]
-                return np.all(idx < words)
-            assert window_ok(w_lo) and window_ok(w_lo - 64)
-            while t + u > 0:
-                dd = t + u
-                widx = dd * K + u % K
-                if widx < w_lo:
-                    w_lo -= 64
-                    assert window_ok(w_lo - 64)
-                assert w_lo <= widx <= w_lo + 63
-                assert 0 <= u // K < 64
-                if (labels_first and u > 0) or t == 0:
-                    u -= 1
-                else:
-                    t -= 1
+
+def _walk_by_diagonal(dec, t, U, var):
+    """The backtrace one diagonal per step (the plain definition): at node (t, u) a set bit
+    means entered by the label arc (or, at u = 0, by the initial wild-card arc)."""
+    u, start, frames = U, 0, {}
+    while t + u > 0:
+        bit = dec[t + u][u]
+        label = u > 0 and (bit or t == 0)
+        jumped = var != 0 and bit and u == 0
+        if label:
+            frames[u - 1] = t
+            u -= 1
+        elif jumped:
+            start = t
+            break
+        else:
+            t -= 1
+    return frames, start
+
+
+def _walk_by_label_moves(dec, t, U, var, ND):
+    """The kernel's backtrace: one step per label move, unit u's bits over a block of 64
+    diagonals taken as one 64-bit mask (the ballot), the highest set bit in [max(u, 1), d]."""
+    u, start, frames = U, 0, {}
+    d = t + u
+    w = d // 64
+    steps = 0
+    while d > 0 and (var != 0 or u > 0):
+        steps += 1
+        if d < 64 * w:
+            w -= 1
+            assert d >= 64 * w  # at most one block down per step
+        base = 64 * w
+        bits = 0
+        for lane in range(64):
+            if base + lane <= ND and dec[base + lane][u]:
+                bits |= 1 << lane
+        lo, hi = max(u, 1) - base, d - base
+        assert lo <= hi <= 63
+        m = bits & ((1 << (hi + 1)) - 1) & ~((1 << max(lo, 0)) - 1)
+        if u > 0:
+            if m:
+                dl = base + m.bit_length() - 1
+            elif u >= base:
+                dl = u
+            else:
+                d = base - 1
+                continue
+            frames[u - 1] = dl - u
+            u -= 1
+            d = dl - 1
+        else:
+            if m:
+                start = base + m.bit_length() - 1
+                break
+            d = base - 1
+    assert steps <= U + (t + U) // 64 + 1
+    return frames, start
+
+
+@pytest.mark.parametrize("var", [0, 1, 2])
+@pytest.mark.parametrize("T,U,density", [(1, 0, 0.5), (3, 1, 0.5), (7, 5, 0.2), (70, 3, 0.05), (5, 130, 0.9),
+                                         (200, 80, 0.3), (150, 150, 0.5), (64, 64, 0.0), (65, 63, 1.0)])
+def test_viterbi_walk_by_label_moves(var, T, U, density):
+    """The block-ballot backtrace reaches the same frames and start frame as the walk one
+    diagonal at a time, on random decision bits (any bits define a valid walk)."""
+    rng = np.random.default_rng(T * 1000 + U + var)
+    ND = T - 1 + U
+    for _ in range(5):
+        dec = rng.random((ND + 65, U + 1)) < density
+        for t_end in {T - 1, max(0, T // 2)}:
+            assert _walk_by_label_moves(dec, t_end, U, var, ND) == _walk_by_diagonal(dec, t_end, U, var)
