@@ -54,11 +54,25 @@ __device__ __forceinline__ V from_lane(V x, int lane) {
 }
 
 // VAR: 0 RNN-T, 1 W-Transducer force-final, 2 allow-ignore.
-template <int K, int PF, int VAR>
-__global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
+// NW: wavefronts in the sweep, as in kernel 2: wave w owns units 64w .. 64w+63 (one
+// per lane), runs a segment of PF steps behind wave w-1 and takes the label-arc term
+// of unit 64w-1 from it through LDS.  Its decision word of a diagonal is then word w,
+// bit u - 64w (one word per wave and diagonal instead of one per lane slot).  The
+// backtrace is wave 0's.
+template <int K, int PF, int VAR, int NW = 1>
+__global__ __launch_bounds__(64 * NW) void k2_viterbi(ViterbiParams p) {
+  static_assert(NW == 1 || K == 1, "several waves take one unit per lane");
+  constexpr int kCols = NW > 1 ? NW : K;  // decision words per diagonal
   __shared__ int s_frames[kViterbiMaxUnits1 + 1];  // the last slot takes the stores of blank moves
+  __shared__ double s_xch[NW > 1 ? NW - 1 : 1][2][PF];
+  __shared__ double s_sink[NW > 1 ? kWave + PF : 1];
+  __shared__ double s_end[2];  // the path's end, from the lane owning u = U: delta(T-1, U), acc_top
+  __shared__ int s_end_i[2];   // t_star, final_skip
   const int b = blockIdx.x;
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid % kWave;
+  const int wv = (NW == 1) ? 0 : __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int ub = wv * kWave * K;  // this wave's first unit
   const int T = p.logit_lens[b];
   const int U = p.label_lens[b];
   const int U1 = p.U_max + 1;
@@ -67,40 +81,41 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
   bool ok = (T >= 1 && T <= p.T_max && U >= 0 && U <= p.U_max);
   int bad = 0;
   if (ok) {
-    for (int u = lane; u < U; u += 64) {
+    for (int u = tid; u < U; u += blockDim.x) {
       const int y = p.labels[static_cast<int64_t>(b) * p.U_max + u];
       if (y < 0 || y >= p.V || y == p.blank) bad = 1;
     }
   }
   bad = __syncthreads_or(bad);
-  if (!ok || bad) {
-    if (lane == 0) p.score_out[b] = __builtin_nanf("");
-    for (int i = lane; i < p.U_max; i += 64) p.label_frames[static_cast<int64_t>(b) * p.U_max + i] = -1;
-    if (p.span && lane < 2) p.span[2 * b + lane] = -1;
+  if (!ok || bad) {  // the whole block leaves together
+    if (tid == 0) p.score_out[b] = __builtin_nanf("");
+    for (int i = tid; i < p.U_max; i += blockDim.x) p.label_frames[static_cast<int64_t>(b) * p.U_max + i] = -1;
+    if (p.span && tid < 2) p.span[2 * b + tid] = -1;
     return;
   }
 
   const int D = T - 1 + U;
-  const int owner_top = U / K;
+  const int owner_top = (U - ub) / K;  // in the wave owning u = U
+  const bool owns_top = (U / (kWave * K) == wv) && lane == owner_top;
   const double2* __restrict__ w_utt = p.lp2 + static_cast<int64_t>(b) * p.T_max * U1;
   const __amdgpu_buffer_rsrc_t w_rsrc = make_buffer(w_utt, static_cast<int64_t>(p.T_max) * U1 * 16);
   const int neg_step = -16 * (U1 - 1);
   auto load_w = [&](int e, int k, double& wb, double& wl) {
     const int ec = min(max(e, 0), D);
-    const int uc = min(max(lane * K + k, ec - (T - 1)), min(ec, U));
+    const int uc = min(max(ub + lane * K + k, ec - (T - 1)), min(ec, U));
     const double2 w = load_lattice_cell(w_rsrc, 16 * ec * U1, uc, neg_step);  // row (t, u) = (ec - uc, uc)
     wb = w.x;
     wl = w.y;
   };
-  uint64_t* __restrict__ dec_utt = p.decisions + static_cast<int64_t>(b) * (ND + 1) * K;
+  uint64_t* __restrict__ dec_utt = p.decisions + static_cast<int64_t>(b) * (ND + 1) * kCols;
   const double w_close = w_utt[(T - 1) * U1 + U].x;
 
   // ---------------- forward max-plus sweep ----------------
   double a[K];
 #pragma unroll
-  for (int k = 0; k < K; ++k) a[k] = (lane * K + k == 0) ? 0.0 : kNoArc;
+  for (int k = 0; k < K; ++k) a[k] = (ub + lane * K + k == 0) ? 0.0 : kNoArc;
   double a_top = (U == 0) ? 0.0 : kNoArc;  // delta(T-1, U) once the sweep reaches D
-  double left_carry = kNoArc;  // lane 0 gets nothing from the shift and keeps kNoArc
+  double left_carry = kNoArc;  // lane 0 of wave 0 gets nothing from the shift and keeps kNoArc
   double acc_top = kNoArc;                 // best delta(t', U), t' <= T-2, and its earliest frame
   int t_star = -1;
   if (VAR != 0 && U == 0 && T >= 2) {
@@ -117,7 +132,21 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
     __builtin_amdgcn_sched_barrier(0);  // issue order = use order (oldest first)
   }
 
-  for (int d0 = 1; d0 <= D; d0 += PF) {
+  double x_in[PF];  // the fill of lane 0 in each step of a segment (several waves; kNoArc for wave 0)
+#pragma unroll
+  for (int s = 0; s < PF; ++s) x_in[s] = kNoArc;
+  const int n_seg = (D + PF - 1) / PF;
+  for (int r = 0; r < n_seg + NW - 1; ++r) {  // every wave passes one barrier per round (several waves)
+    const int g = r - wv;  // this wave's segment in round r
+    if (g >= 0 && g < n_seg) {
+    const int d0 = 1 + g * PF;
+    if (NW > 1 && wv > 0) {  // the wave before wrote this segment's values in the previous round
+#pragma unroll
+      for (int s = 0; s < PF; ++s) x_in[s] = s_xch[max(wv - 1, 0)][(r - 1) & 1][s];
+    }
+    // lane 63 writes into this round's slots for the next wave, the others into the sink
+    double* const x_out = (lane == kWave - 1 && wv < NW - 1) ? &s_xch[min(wv, NW > 1 ? NW - 2 : 0)][r & 1][0]
+                                                              : &s_sink[NW > 1 ? lane : 0];
 #pragma unroll
     for (int s = 0; s < PF; ++s) {
       const int d = d0 + s;  // slot s holds the weights of diagonal d-1
@@ -127,7 +156,8 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
         eb[k] = a[k] + rb[s][k];
         el[k] = a[k] + rl[s][k];
       }
-      left_carry = wave_shift_up(el[K - 1], left_carry);
+      if (NW > 1) x_out[s] = el[K - 1];  // lane 63's for wave wv+1
+      left_carry = wave_shift_up(el[K - 1], NW > 1 ? x_in[s] : left_carry);
       const double left = left_carry;
       bool dec[K];
 #pragma unroll
@@ -137,7 +167,7 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
         a[k] = dec[k] ? cl : eb[k];
       }
       // wave-uniform conditions on the diagonal; no memory access inside
-      if (VAR != 0 && d <= T - 1 && lane == 0 && 0.0 > a[0]) {  // (0,0)->(d,0), delta(0,0) = 0
+      if (VAR != 0 && d <= T - 1 && wv == 0 && lane == 0 && 0.0 > a[0]) {  // (0,0)->(d,0), delta(0,0) = 0
         a[0] = 0.0;
         dec[0] = true;
       }
@@ -145,39 +175,57 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
         if (VAR == 1) {
 #pragma unroll
           for (int k = 0; k < K; ++k)
-            if (lane * K + k == U && acc_top > a[k]) {  // (t*,U)->(T-1,U)
+            if (ub + lane * K + k == U && acc_top > a[k]) {  // (t*,U)->(T-1,U)
               a[k] = acc_top;
               final_skip = true;
             }
         }
-        a_top = at_unit(a, lane, U, a_top);
+        a_top = at_unit(a, lane, U - ub, a_top);
       }
       if (VAR != 0 && d >= U && d - U <= T - 2) {  // delta(d-U, U), earliest frame on ties
-        const double x = at_unit(a, lane, U, kNoArc);
+        const double x = at_unit(a, lane, U - ub, kNoArc);
         if (x > acc_top) {
           acc_top = x;
           t_star = d - U;
         }
       }
-      // the diagonal's decisions: word k = ballot of slot k; lane l stores word min(l, K-1)
+      // the diagonal's decisions: word k = ballot of slot k, lane l storing word min(l, K-1);
+      // several waves: wave w's ballot is word w
       uint64_t word = 0;
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         const uint64_t m = __ballot(dec[k]);
         word = (lane == k || (k == K - 1 && lane > k)) ? m : word;
       }
-      dec_utt[static_cast<int64_t>(min(d, D + 1)) * K + min(lane, K - 1)] = word;
+      dec_utt[static_cast<int64_t>(min(d, D + 1)) * kCols + (NW > 1 ? wv : min(lane, K - 1))] = word;
 #pragma unroll
       for (int k = 0; k < K; ++k) load_w(d - 1 + PF, k, rb[s][k], rl[s][k]);
       __builtin_amdgcn_sched_barrier(0);  // the prefetch stays PF steps ahead of its use
     }
+    }
+    if (NW > 1) __syncthreads();  // the segment's values reach the next wave
   }
 
-  // the path's end (values of the lane owning u = U)
-  a_top = from_lane(a_top, owner_top);
-  acc_top = from_lane(acc_top, owner_top);
-  t_star = from_lane(t_star, owner_top);
-  const bool skip_in = from_lane(static_cast<int>(final_skip), owner_top) != 0;
+  // the path's end (values of the lane owning u = U; through LDS from another wave)
+  bool skip_in;
+  if (NW == 1) {
+    a_top = from_lane(a_top, owner_top);
+    acc_top = from_lane(acc_top, owner_top);
+    t_star = from_lane(t_star, owner_top);
+    skip_in = from_lane(static_cast<int>(final_skip), owner_top) != 0;
+  } else {
+    if (owns_top) {
+      s_end[0] = a_top;
+      s_end[1] = acc_top;
+      s_end_i[0] = t_star;
+      s_end_i[1] = static_cast<int>(final_skip);
+    }
+    __syncthreads();
+    a_top = s_end[0];
+    acc_top = s_end[1];
+    t_star = s_end_i[0];
+    skip_in = s_end_i[1] != 0;
+  }
   double best2 = a_top + w_close;  // closing blank
   int t = T - 1, end_frame = T - 1;
   if (VAR == 1 && skip_in) t = end_frame = t_star;
@@ -192,38 +240,41 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
   // falls, u stays) to the highest diagonal d' <= d whose node of unit u was entered by
   // its label arc -- at t = 0 it always is -- emits unit u at frame d' - u and goes on
   // from (d' - u, u - 1) on diagonal d' - 1.  Unit u's decision bits over a block of 64
-  // diagonals are one ballot: lane l reads the word of diagonal 64 w + l in column u % K
-  // (the block staged in LDS, one column per 64 words) and tests bit u / K.  At u = 0
-  // (W-Transducer) a set bit is the initial wild-card arc: the path starts there.  Each
-  // step lowers d, so the walk ends after at most U + D/64 + 1 steps.
-  __shared__ uint64_t s_blk[K][kWave];
-  const __amdgpu_buffer_rsrc_t dec_rsrc = make_buffer(dec_utt, static_cast<int64_t>(ND + 1) * K * 8);
+  // diagonals are one ballot: lane l reads the word of diagonal 64 w + l in unit u's
+  // column (u % K, or u / 64 with several waves; the block staged in LDS, one column
+  // per 64 words) and tests unit u's bit (u / K, or u % 64).  At u = 0 (W-Transducer) a
+  // set bit is the initial wild-card arc: the path starts there.  Each step lowers d,
+  // so the walk ends after at most U + D/64 + 1 steps.  Wave 0 walks.
+  __shared__ uint64_t s_blk[kCols][kWave];
+  const __amdgpu_buffer_rsrc_t dec_rsrc = make_buffer(dec_utt, static_cast<int64_t>(ND + 1) * kCols * 8);
   // the words of diagonal 64 w + lane, all columns (0 past the stored rows)
-  auto load_block = [&](int w, uint64_t (&x)[K]) {
+  auto load_block = [&](int w, uint64_t (&x)[kCols]) {
     typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 #pragma unroll
-    for (int k = 0; k < K; ++k) {
-      const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(dec_rsrc, ((kWave * w + lane) * K + k) * 8, 0, 0);
-      x[k] = (static_cast<uint64_t>(v.y) << 32) | v.x;
+    for (int c = 0; c < kCols; ++c) {
+      const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(dec_rsrc, ((kWave * w + lane) * kCols + c) * 8, 0, 0);
+      x[c] = (static_cast<uint64_t>(v.y) << 32) | v.x;
     }
   };
   int u = U, d = t + u, start_frame = 0;
+  if (wv == 0) {
   int w = d / kWave;
-  uint64_t nxt[K];
+  uint64_t nxt[kCols];
   load_block(w, nxt);
 #pragma unroll
-  for (int k = 0; k < K; ++k) s_blk[k][lane] = nxt[k];
+  for (int c = 0; c < kCols; ++c) s_blk[c][lane] = nxt[c];
   if (w > 0) load_block(w - 1, nxt);  // the block below, in flight while this one is walked
   while (d > 0 && (VAR != 0 || u > 0)) {
     if (d < kWave * w) {  // one block down (a step lowers the block by at most one)
       w -= 1;
 #pragma unroll
-      for (int k = 0; k < K; ++k) s_blk[k][lane] = nxt[k];
+      for (int c = 0; c < kCols; ++c) s_blk[c][lane] = nxt[c];
       if (w > 0) load_block(w - 1, nxt);
     }
     const unsigned uu = static_cast<unsigned>(u);
-    const uint64_t col = s_blk[uu % K][lane];
-    const uint64_t bits = __ballot(static_cast<int>((col >> (uu / K)) & 1u));  // bit l: diagonal 64 w + l
+    const uint64_t col = s_blk[NW > 1 ? uu / kWave : uu % K][lane];
+    const unsigned bit_of_u = NW > 1 ? uu % kWave : uu / K;
+    const uint64_t bits = __ballot(static_cast<int>((col >> bit_of_u) & 1u));  // bit l: diagonal 64 w + l
     const int base = kWave * w;
     const int lo = max(u, 1) - base;  // t >= 0, and never diagonal 0 (node (0,0) has no decision)
     const int hi = d - base;          // lo <= hi <= 63
@@ -249,10 +300,11 @@ __global__ __launch_bounds__(64) void k2_viterbi(ViterbiParams p) {
       d = base - 1;
     }
   }
+  }
   __syncthreads();
-  for (int i = lane; i < p.U_max; i += 64)
+  for (int i = tid; i < p.U_max; i += blockDim.x)
     p.label_frames[static_cast<int64_t>(b) * p.U_max + i] = (i < U) ? s_frames[i] : -1;
-  if (lane == 0) {
+  if (tid == 0) {
     p.score_out[b] = static_cast<float>(best2 / kLog2eD);
     if (p.span) {
       p.span[2 * b] = start_frame;

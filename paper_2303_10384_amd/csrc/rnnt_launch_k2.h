@@ -61,20 +61,27 @@ hipError_t launch_k2(int variant, const LatticeParams& p, hipStream_t stream) {
   }
 }
 
-template <int K, int VAR>
+template <int K, int VAR, int NW = 1>
 hipError_t launch_k2v_k(const ViterbiParams& p, hipStream_t stream) {
   constexpr int PF = (K >= 24) ? 1 : (K >= 16) ? 2 : (48 / K > 24 ? 24 : 48 / K);
-  hipLaunchKernelGGL((k2_viterbi<K, PF, VAR>), dim3(p.B), dim3(64), 0, stream, p);
+  hipLaunchKernelGGL((k2_viterbi<K, PF, VAR, NW>), dim3(p.B), dim3(64 * NW), 0, stream, p);
   return hipGetLastError();
 }
 
+// the forced-alignment sweep splits over wavefronts as kernel 2 does (65 to 256 units)
 template <int VAR>
 hipError_t launch_k2v_v(const ViterbiParams& p, hipStream_t stream) {
   switch (units_per_lane(p.U_max + 1)) {
     case 1: return launch_k2v_k<1, VAR>(p, stream);
+#if RNNT_K2_MULTI_WAVE
+    case 2: return launch_k2v_k<1, VAR, 2>(p, stream);
+    case 3: return launch_k2v_k<1, VAR, 3>(p, stream);
+    case 4: return launch_k2v_k<1, VAR, 4>(p, stream);
+#else
     case 2: return launch_k2v_k<2, VAR>(p, stream);
     case 3: return launch_k2v_k<3, VAR>(p, stream);
     case 4: return launch_k2v_k<4, VAR>(p, stream);
+#endif
     case 6: return launch_k2v_k<6, VAR>(p, stream);
     case 8: return launch_k2v_k<8, VAR>(p, stream);
     case 12: return launch_k2v_k<12, VAR>(p, stream);

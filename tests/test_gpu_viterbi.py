@@ -72,7 +72,8 @@ def check_utterance(seen_b, labels_b, blank, variant, score, frames, span, T_b, 
 @pytest.mark.parametrize("B,T,U,V,blank,seed", [
     (4, 9, 6, 7, 0, 1), (3, 17, 70, 33, 5, 2), (2, 5, 130, 11, 10, 3), (5, 13, 3, 1030, 1029, 4),
     (2, 4, 2, 3, 1, 5), (3, 6, 4, 2, 0, 6), (1, 1, 5, 9, 0, 7), (2, 11, 0, 6, 2, 8), (2, 4, 300, 6, 0, 9),
-    (1, 3, 700, 5, 0, 10), (1, 3, 1535, 5, 0, 11), (1, 2, 2047, 4, 0, 12)])
+    (1, 3, 700, 5, 0, 10), (1, 3, 1535, 5, 0, 11), (1, 2, 2047, 4, 0, 12),
+    (2, 6, 200, 9, 0, 13), (3, 5, 127, 8, 2, 14)])  # four sweep waves; U at the second wave's edge
 def test_viterbi_matches_oracle(torch, pkg, dtype, variant, B, T, U, V, blank, seed):
     logits, tl, ul, labels = W.small_case(B, T, U, V, seed=seed, sigma=2.0, blank=blank)
     score, frames, span, seen = run_viterbi(torch, pkg, logits, tl, ul, labels, blank, variant, dtype)
@@ -84,7 +85,7 @@ def test_viterbi_matches_oracle(torch, pkg, dtype, variant, B, T, U, V, blank, s
 
 
 @pytest.mark.parametrize("variant", VARIANTS)
-@pytest.mark.parametrize("T,U", [(1, 0), (3, 0), (1, 3), (4, 2), (9, 5), (40, 70)])
+@pytest.mark.parametrize("T,U", [(1, 0), (3, 0), (1, 3), (4, 2), (9, 5), (40, 70), (3, 128), (6, 200)])
 def test_viterbi_ties_follow_the_fixed_order(torch, pkg, variant, T, U):
     # all-equal logits: every arc weighs -ln V on both sides, every path of the same length
     # ties exactly, and the fixed order decides

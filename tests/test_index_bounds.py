@@ -288,25 +288,33 @@ def test_posterior_kernel_tiles_cover_every_row_once(B, T, U, V, dt):
 
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
 def test_viterbi_kernel_addresses(B, T, U, V, dt):
-    """Forced-alignment kernel: decision words stored at row min(d, D+1), K words a row; the
-    backtrace stages blocks of 64 diagonals, lane l loading the K words of diagonal 64 w + l at
-    byte offset ((64 w + l) K + k) * 8: never negative, and past the utterance's (T_max+U_max+1)*K
-    words only beyond the last row (a buffer load there reads 0), under 2^31 bytes."""
+    """Forced-alignment kernel: decision words stored at row min(d, D+1), one per lane slot (K a
+    row) or one per wave (NW a row); the backtrace stages blocks of 64 diagonals, lane l loading
+    the words of diagonal 64 w + l at byte offset ((64 w + l) cols + c) * 8: never negative, and past
+    the utterance's (T_max+U_max+1)*cols words only beyond the last row (a buffer load there reads
+    0), under 2^31 bytes."""
     U1 = U + 1
     ND = T + U
-    K = next(k for k in (1, 2, 3, 4, 6, 8, 12, 16, 24, 32) if U1 <= 64 * k)
-    words = (ND + 1) * K
+    NW, K = sweep_shape(U1)
+    cols = units_per_lane(U1)  # decision words per diagonal: one per lane slot, or one per wave
+    assert cols == (NW if NW > 1 else K)
+    words = (ND + 1) * cols
     lanes = np.arange(64)
     for Tb, Ub in [(T, U), (1, 0), (max(1, T // 2), U // 2), (1, U), (T, 0)]:
         D = Tb - 1 + Ub
         PF = 1 if K >= 24 else 2 if K >= 16 else min(24, 48 // K)
         for d in range(1, D + PF):
             row = min(d, D + 1)
-            for lane in range(64):
-                assert 0 <= row * K + min(lane, K - 1) < words
+            for wv in range(NW):
+                for lane in range(64):
+                    assert 0 <= row * cols + (wv if NW > 1 else min(lane, K - 1)) < words
+        # unit u's word column and bit: (u % K, u // K) in one wave, (u // 64, u % 64) over several
+        for u in range(Ub + 1):
+            c, bit = (u // 64, u % 64) if NW > 1 else (u % K, u // K)
+            assert 0 <= c < cols and 0 <= bit < 64
         for w in range(D // 64 + 1):
-            for k in range(K):
-                idx = (64 * w + lanes) * K + k
+            for k in range(cols):
+                idx = (64 * w + lanes) * cols + k
                 assert np.all(idx >= 0) and np.all(idx * 8 < 2 ** 31)
                 # a word past the stored rows is a diagonal past ND: masked off by the walk (d <= D)
                 assert np.all((idx < words) | (64 * w + lanes > ND))
