@@ -18,7 +18,7 @@ static __device__ __align__(256) unsigned char scratch[RNNT_NOALLOC_SCRATCH_BYTE
 namespace rnnt {
 namespace {
 
-constexpr int kMaxUnits1 = 2048;  // U_max + 1 handled by one wavefront (32 units per lane)
+constexpr int kMaxUnits1 = 2048;  // widest U_max + 1 of the grid sweeps (one wavefront, 32 units per lane)
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
