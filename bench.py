@@ -109,26 +109,41 @@ def plain_step_times(torch, ev, call, steps):
     return float(np.median(spans)), mean
 
 
-def algorithmic_bytes(w, tl, ul, s_in, s_out):
+def algorithmic_bytes(w, tl, ul, s_in, s_out, r_grad=None):
     """Bytes each streaming kernel must move at the least, per launch.
 
     Kernel 1 reads the logits of the valid rows (t < T_b, u <= U_b) once.
-    Kernel 3 reads the valid rows' logits and the per-row record of every padded
-    row, and writes the whole gradient (zeros in the padding rows).  The lattice
-    arrays of kernels 2 / 2b (a few MB) are left out.  The step as a whole must
-    read the valid logits twice (the arc posteriors that kernel 3 needs depend on
-    every row's normaliser) and write the whole gradient once."""
+    Kernel 3 reads the logits of the valid rows whose gradient is not identically
+    zero (r_grad of them; a row whose arc posteriors both underflow float32 has an
+    exactly zero gradient and needs no logits) and the per-row record of every
+    padded row, and writes the whole gradient (zeros in the padding rows).  The
+    lattice arrays of kernels 2 / 2b (a few MB) are left out.  The step as a whole
+    must read the valid logits once for the normalisers and those r_grad rows a
+    second time (the arc posteriors depend on every row's normaliser), and write
+    the whole gradient once.  r_grad defaults to every valid row."""
     import numpy as np
     r_valid = int(np.sum(tl.astype(np.int64) * (ul.astype(np.int64) + 1)))
     r_total = w.B * w.T_max * (w.U_max + 1)
+    r_grad = r_valid if r_grad is None else int(r_grad)
     V = w.V
     return {
         "valid_rows": r_valid,
         "padded_rows": r_total,
+        "gradient_rows": r_grad,
         "k1_populate": r_valid * V * s_in,
-        "k3_grad": r_valid * V * s_in + r_total * V * s_out + r_total * ROWREC_BYTES,
-        "step": 2 * r_valid * V * s_in + r_total * V * s_out,
+        "k3_grad": r_grad * V * s_in + r_total * V * s_out + r_total * ROWREC_BYTES,
+        "step": (r_valid + r_grad) * V * s_in + r_total * V * s_out,
     }
+
+
+def gradient_rows(torch, grad, tl, ul):
+    """Valid rows whose gradient holds a nonzero element (the rows whose logits the
+    gradient needs), counted on the device one utterance at a time."""
+    n = 0
+    for b in range(grad.shape[0]):
+        g = grad[b, :int(tl[b]), :int(ul[b]) + 1]
+        n += int((g != 0).any(dim=-1).sum().item())
+    return n
 
 
 def cpu_oracle_worker(args):
@@ -330,7 +345,7 @@ def arc_bench(args, w, tl, ul, labels, logits, tl_d, ul_d, cpu):
     log("[bench] per step %.4f ms median, %.4f mean (instrumented %.4f, wall %.4f ms): k1 %.4f  populate %.4f  "
         "sweep %.4f  rows %.4f  k3 %.4f ms" % (ms_per_step, ms_mean, ms_inst, wall * 1e3 / args.steps, k1_ms, kp_ms,
                                                ks_ms, kr_ms, k3_ms))
-    ab = algorithmic_bytes(w, tl, ul, logits.element_size(), grad.element_size())
+    ab = algorithmic_bytes(w, tl, ul, logits.element_size(), grad.element_size(), gradient_rows(torch, grad, tl, ul))
     elems = ab["padded_rows"] * w.V
     k3_gbs = ab["k3_grad"] / (k3_ms * 1e-3) / 1e9
     result = {
@@ -352,7 +367,7 @@ def arc_bench(args, w, tl, ul, labels, logits, tl_d, ul_d, cpu):
         "config": {
             "workload": w.describe() + " as arc lists",
             "B": w.B, "T_max": w.T_max, "U_max": w.U_max, "V": w.V, "variant": w.variant,
-            "valid_rows": ab["valid_rows"], "padded_rows": ab["padded_rows"],
+            "valid_rows": ab["valid_rows"], "padded_rows": ab["padded_rows"], "gradient_rows": ab["gradient_rows"],
             "states": plan.num_states, "arcs": plan.num_arcs, "levels": plan.num_levels,
             "plan": "built once on the host before timing (%.2f s), image %d bytes on the device"
                     % (plan_s, plan.image_bytes),
@@ -461,7 +476,7 @@ def main():
     log("[bench] per step %.4f ms median, %.4f mean (instrumented %.4f, wall %.4f ms): k1 %.4f  k2 %.4f  k2b %.4f  "
         "k3 %.4f ms" % (ms_per_step, ms_mean, ms_inst, wall * 1e3 / args.steps, k1_ms, k2_ms, k2b_ms, k3_ms))
 
-    ab = algorithmic_bytes(w, tl, ul, logits.element_size(), grad.element_size())
+    ab = algorithmic_bytes(w, tl, ul, logits.element_size(), grad.element_size(), gradient_rows(torch, grad, tl, ul))
     r_valid, r_total, V = ab["valid_rows"], ab["padded_rows"], w.V
     elems = r_total * V
     k1_bytes, k3_bytes, step_bytes = ab["k1_populate"], ab["k3_grad"], ab["step"]
@@ -497,7 +512,7 @@ def main():
         "config": {
             "workload": w.describe(),
             "B": w.B, "T_max": w.T_max, "U_max": w.U_max, "V": V, "variant": w.variant,
-            "valid_rows": r_valid, "padded_rows": r_total,
+            "valid_rows": r_valid, "padded_rows": r_total, "gradient_rows": ab["gradient_rows"],
             "lattice_scores": "f64", "softmax": "f32",
         },
         "hbm_gbs_step": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),

@@ -507,8 +507,11 @@ __global__ __launch_bounds__(NT) void k_arc_rows(ArcRowParams p) {
         extra = true;  // a second non-blank label: the extra-rows kernel writes this row
       }
     }
-    if (!extra) {
-      ri.lse2 = static_cast<float>(p.lse2_rows[r]);
+    const float lse2 = static_cast<float>(p.lse2_rows[r]);
+    // no posterior left in float32 and finite logits: the row's gradient is exactly +0 at
+    // every v, written as a zero row without reading its logits (as for the grid lattice)
+    if (!extra && !(ob == 0.f && ol == 0.f && __builtin_isfinite(lse2))) {
+      ri.lse2 = lse2;
       ri.occ_blank = ob;
       ri.occ_label = ol;
       ri.label = primary;

@@ -110,6 +110,12 @@ __device__ __forceinline__ RowInfo lattice_row_record(const LatticeRecordSrc& s,
   o.occ_blank = fast_exp2(static_cast<float>(xb));
   o.occ_label = fast_exp2(static_cast<float>(xl));
   o.label = (u < U) ? y : kNoLabel;
+  // Both posteriors underflow float32 (the node lies far from every likely path) and the
+  // row's normaliser is finite, so every logit of the row is finite: its gradient
+  // p_v (g_b + g_l) - g_b [v = blank] - g_l [v = y] is exactly +0 at every v.  The row
+  // goes to the gradient kernel as a zero row, which writes those zeros without reading
+  // its logits.
+  if (o.occ_blank == 0.f && o.occ_label == 0.f && __builtin_isfinite(lse2)) o = RowInfo{0.f, 0.f, 0.f, kZeroRow};
   return o;
 }
 

@@ -33,6 +33,23 @@ def test_algorithmic_bytes_of_the_bpe_workload():
     # bf16 logits with a float32 gradient
     ab2 = bench.algorithmic_bytes(w, tl, ul, 2, 4)
     assert ab2["k3_grad"] == r_valid * 1025 * 2 + 648000 * 1025 * 4 + 648000 * 16
+    # only the rows whose gradient is not identically zero are read a second time
+    r_grad = r_valid * 3 // 5
+    ab3 = bench.algorithmic_bytes(w, tl, ul, 4, 4, r_grad)
+    assert ab3["gradient_rows"] == r_grad and ab3["k1_populate"] == ab["k1_populate"]
+    assert ab3["k3_grad"] == r_grad * 1025 * 4 + 648000 * 1025 * 4 + 648000 * 16
+    assert ab3["step"] == (r_valid + r_grad) * 1025 * 4 + 648000 * 1025 * 4
+
+
+def test_gradient_rows_counts_valid_rows_with_a_nonzero_element():
+    import torch
+    g = torch.zeros(2, 4, 3, 5)
+    g[0, 1, 2, 4] = 1e-30   # a valid row (t < 3, u <= 2)
+    g[0, 3, 0, 0] = 1.0     # a padding frame: not counted
+    g[1, 0, 1, 2] = -2.0    # valid (t < 2, u <= 1)
+    g[1, 0, 2, 0] = 5.0     # u > 1: padding, not counted
+    tl = np.array([3, 2]); ul = np.array([2, 1])
+    assert bench.gradient_rows(torch, g, tl, ul) == 2
 
 
 def test_step_times_median_and_mean():
