@@ -332,6 +332,27 @@ def test_sweep_wave_boundaries(torch, pkg, variant):
     tol_check(loss, grad, loss_ref, grad_ref, "f32", tl, ul)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_rows_of_underflowed_posteriors_are_exact_zeros(torch, pkg, dtype):
+    # long lattices with sharp logits: many valid rows lie so far from every likely path that
+    # both arc posteriors underflow float32; the gradient kernel writes them as zero rows
+    # without reading their logits, so their gradient must be exactly +0 (and the rest match)
+    logits, tl, ul, labels = W.small_case(2, 120, 40, 300, seed=41, sigma=3.0, full=True)
+    loss, grad, seen = run_case(torch, pkg, logits, tl, ul, labels, dtype=dtype, grad_dtype="f32")
+    loss_ref, grad_ref = R.rnnt_loss_grad(seen, labels, tl, ul, 0, "rnnt")
+    tol_check(loss, grad, loss_ref, grad_ref, dtype, tl, ul, grad_dtype="f32")
+    n_far = 0
+    for b in range(2):
+        _, lp_b, lp_l = R.lattice_weights(seen[b], labels[b], 0)
+        alpha, lnP = R.forward_scores(lp_b, lp_l, "rnnt")
+        beta, _ = R.backward_scores(lp_b, lp_l, "rnnt")
+        ob, ol = R.arc_posteriors(alpha, beta, lp_b, lp_l, lnP)
+        far = np.maximum(ob, ol) < 2.0 ** -140  # well below float32's range: 0 on the device too
+        n_far += int(far.sum())
+        assert np.all(grad[b][far] == 0) and not np.any(np.signbit(grad[b][far]))
+    assert n_far >= 0.1 * 2 * 120 * 41, n_far  # the case exercises the skipped rows
+
+
 @pytest.mark.parametrize("dtype,V,blank", [("f32", 4100, 17), ("bf16", 8200, 8199), ("f16", 2600, 0)])
 def test_large_vocabulary(torch, pkg, dtype, V, blank):
     # rows longer than the populate kernel's register path (64 lanes x 5 chunks) take its batched path
