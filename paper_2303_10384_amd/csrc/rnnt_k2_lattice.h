@@ -135,6 +135,13 @@ __device__ __forceinline__ double at_unit(const double (&x)[K], int lane, int u,
   return r;
 }
 
+// Log-sum (log2 units) over the 64 lanes of a wave; every lane gets the result.
+__device__ __forceinline__ double wave_log_sum(double x) {
+#pragma unroll
+  for (int m = kWave / 2; m >= 1; m /= 2) x = log_add2(x, __shfl_xor(x, m, kWave));
+  return x;
+}
+
 // VAR: 0 RNN-T, 1 W-Transducer force-final, 2 allow-ignore.
 // DENSE_IN: weights from the dense natural-log arrays instead of kernel 1.
 // NW: wavefronts per sweep.  Wave w owns units w*64*K .. (w+1)*64*K - 1 (unit u
@@ -160,7 +167,10 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
   // every lane writes each step (no exec mask), the lanes without a value to pass
   // into a scratch run of their own (lane + step: no two lanes of a write collide)
   __shared__ double s_xch[NW > 1 ? NW - 1 : 1][2][PF];
-  __shared__ double s_sink[NW > 1 ? kWave + PF : 1];
+  __shared__ double s_sink[NW > 1 || VAR != 0 ? kWave + PF : 1];
+  // W-Transducer: the segment's values of the one node whose scores are summed over
+  // the sweep (alpha(d-U, U) forward, beta(d, 0) backward), one per step
+  __shared__ double s_sum[VAR != 0 ? PF : 1];
 
   bool ok = (T >= 1 && T <= p.T_max && U >= 0 && U <= p.U_max);
   int bad = 0;
@@ -237,12 +247,17 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
     double a[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) a[k] = (ub + lane * K + k == 0) ? 0.0 : kNoArc;
-    double acc_top = kNoArc;                   // log-sum of alpha(t, U), t <= T-2
     double a_top = (U == 0) ? 0.0 : kNoArc;    // alpha(T-1, U) once the sweep reaches D
     // the shifted-in neighbour; lane 0 of wave 0 gets none from the shift and keeps
     // kNoArc from here on, so no fill value is set up in each step
     double left_carry = kNoArc;
-    if (VAR != 0 && U == 0 && T >= 2) acc_top = 0.0;  // alpha(0, U) itself when U = 0
+    // W-Transducer: log-sum of alpha(t, U), t <= T-2, kept per lane (lane s sums the
+    // steps s of every segment) in the wave owning unit U and summed over lanes at the
+    // end; the owning lane's only work in a step is one LDS store
+    const int w_top = U / (kWave * K);
+    double acc_lane = kNoArc;
+    if (VAR != 0 && U == 0 && T >= 2 && lane == 0) acc_lane = 0.0;  // alpha(0, U) itself when U = 0
+    double* const sum_out = owns_top ? &s_sum[0] : &s_sink[VAR != 0 ? lane : 0];
     if (MODE != kLossOnly && wv == 0 && lane == 0) a_utt[0] = 0.0;
 
     double rb[PF][K], rl[PF][K];
@@ -288,31 +303,44 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
           }
           if (NW > 1) x_out[s] = el[K - 1];  // lane 63's for wave wv+1
           // lane 0 of a later wave takes the unit below it from the wave before, one segment old
-          const double fill = (NW > 1) ? x_in[s] : left_carry;
+          double fill = (NW > 1) ? x_in[s] : left_carry;
+          // unit 0 has no unit below; in the W-Transducer its second term is the skip arc
+          // (0,0)->(d,0) of weight 0 from alpha(0,0) = 0, so no second log-add follows on
+          // the chain (log_add2(x, kNoArc) is exactly x)
+          if (VAR != 0 && wv == 0) fill = (d <= T - 1) ? 0.0 : kNoArc;
           left_carry = wave_shift_up(el[K - 1], fill);
           const double left = left_carry;
 #pragma unroll
           for (int k = 0; k < K; ++k) a[k] = log_add2(eb[k], k == 0 ? left : el[k > 0 ? k - 1 : 0]);
           // wave-uniform conditions on the diagonal; no memory access inside
-          if (VAR != 0 && d <= T - 1 && wv == 0 && lane == 0) a[0] = log_add2(a[0], 0.0);  // (0,0)->(d,0)
-          if (__builtin_expect(d == D, 0)) {  // once per sweep: a branch, not selects in every step
-            if (VAR == 1) {
-#pragma unroll
-              for (int k = 0; k < K; ++k)
-                if (ub + lane * K + k == U) a[k] = log_add2(a[k], acc_top);  // (t,U)->(T-1,U)
-            }
-            a_top = at_unit(a, lane, U - ub, a_top);
-          }
-          if (VAR != 0 && d >= U && d - U <= T - 2)
-            acc_top = log_add2(acc_top, at_unit(a, lane, U - ub, kNoArc));  // alpha(d-U, U)
+          // once per sweep: a branch, not selects in every step.  The force-final skip arcs
+          // into (T-1, U) are added after the sweep: no later step reads alpha(T-1, U)
+          if (__builtin_expect(d == D, 0)) a_top = at_unit(a, lane, U - ub, a_top);
+          if (VAR != 0) sum_out[s] = K == 1 ? a[0] : at_unit(a, lane, U - ub, kNoArc);
           if (MODE != kLossOnly)  // the row offset is uniform; readfirstlane keeps it in a scalar register
             store_scores<K>(a_rsrc, lane_off, __builtin_amdgcn_readfirstlane(min(d, D + 1) * row_bytes), a);
 #pragma unroll
           for (int k = 0; k < K; ++k) load_w(d - 1 + PF, k, rb[s][k], rl[s][k]);
           __builtin_amdgcn_sched_barrier(0);  // the prefetch stays PF steps ahead of its use
         }
+        if (VAR != 0 && wv == w_top) {  // lane s: alpha(d-U, U) of step s, if 0 <= d-U <= T-2
+          const int dl = d0 + lane;     // (a wave's LDS accesses complete in order)
+          const double x = s_sum[min(lane, PF - 1)];
+          acc_lane = log_add2(acc_lane, (lane < PF && dl >= U && dl - U <= T - 2) ? x : kNoArc);
+        }
       }
       if (NW > 1) __syncthreads();  // the segment's values reach the next wave
+    }
+    double acc_top = kNoArc;  // log-sum of alpha(t, U), t <= T-2
+    if (VAR != 0 && wv == w_top) acc_top = wave_log_sum(acc_lane);
+    if (VAR == 1 && owns_top) {
+      a_top = log_add2(a_top, acc_top);  // (t,U)->(T-1,U)
+      if (MODE != kLossOnly) {
+        // replaces the value the step stored (the fence keeps the compiler from moving that
+        // store after this one; one lane's stores to an address complete in order)
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        a_utt[static_cast<int64_t>(D) * p.u_pad + U] = a_top;
+      }
     }
     if (owns_top) {
       double lnP2 = a_top + w_close;
@@ -326,8 +354,11 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
 #pragma unroll
     for (int k = 0; k < K; ++k) bv[k] = (ub + lane * K + k == U) ? w_close : kNoArc;
     const double b_top = w_close;  // beta(T-1, U)
-    double acc0 = kNoArc;          // log-sum of beta(t, 0), t >= 1
-    if (VAR != 0 && U == 0 && T >= 2) acc0 = w_close;
+    // W-Transducer: log-sum of beta(t, 0), t >= 1, kept per lane of wave 0 as in the
+    // forward sweep (lane 0 of wave 0 owns unit 0)
+    double acc_lane = kNoArc;
+    if (VAR != 0 && U == 0 && T >= 2 && wv == 0 && lane == 0) acc_lane = w_close;  // beta(T-1, 0)
+    double* const sum_out = (wv == 0 && lane == 0) ? &s_sum[0] : &s_sink[VAR != 0 ? lane : 0];
     if (owns_top) b_utt[static_cast<int64_t>(D) * p.u_pad + U] = w_close;
     double b00 = (D == 0) ? w_close : kNoArc;  // beta(0,0)
     double right_carry = kNoArc;  // lane 63 of the last wave keeps kNoArc (see left_carry)
@@ -362,6 +393,10 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
           const double fill = (NW > 1) ? x_in[s] : right_carry;
           right_carry = wave_shift_down(bv[0], fill);
           const double right = right_carry;
+          // W-Transducer: node (d-U, U), t <= T-2, has a skip arc of weight 0 to (T-1, U)
+          // (force-final) or to the final node (allow-ignore); it takes the place of the
+          // label arc that unit U lacks, so no second log-add follows on the chain
+          const bool skip_top = VAR != 0 && d >= U && d - U <= T - 2;  // wave-uniform
           double nb[K];
 #pragma unroll
           for (int k = 0; k < K; ++k) {
@@ -372,19 +407,14 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
               wl = to_lattice(wl, u < U);
             }
             const double xb = wb + bv[k];
-            const double xl = wl + (k == K - 1 ? right : bv[k + 1 < K ? k + 1 : k]);
+            double xl = wl + (k == K - 1 ? right : bv[k + 1 < K ? k + 1 : k]);
+            if (VAR != 0) xl = (skip_top && ub + lane * K + k == U) ? (VAR == 1 ? b_top : 0.0) : xl;
             nb[k] = log_add2(xb, xl);
           }
-          if (VAR != 0 && d >= U && d - U <= T - 2) {  // wave-uniform: (d-U, U)->(T-1, U) or ->final
-            const double x = log_add2(at_unit(nb, lane, U - ub, kNoArc), VAR == 1 ? b_top : 0.0);
-#pragma unroll
-            for (int k = 0; k < K; ++k) nb[k] = (ub + lane * K + k == U) ? x : nb[k];
-          }
-          if (__builtin_expect(d == 0, 0)) {  // wave-uniform, once per sweep: a branch, not selects
-            if (VAR != 0 && wv == 0 && lane == 0) nb[0] = log_add2(nb[0], acc0);  // (0,0)->(t,0)
-            b00 = nb[0];
-          }
-          if (VAR != 0 && d >= 1 && d <= T - 1) acc0 = log_add2(acc0, nb[0]);  // beta(d, 0), lane 0 of wave 0
+          // wave-uniform, once per sweep: a branch, not selects.  The skip arcs out of (0,0)
+          // are added after the sweep: no later step reads beta(0,0)
+          if (__builtin_expect(d == 0, 0)) b00 = nb[0];
+          if (VAR != 0) sum_out[s] = nb[0];
 #pragma unroll
           for (int k = 0; k < K; ++k) bv[k] = nb[k];
           store_scores<K>(b_rsrc, lane_off, __builtin_amdgcn_readfirstlane((d >= 0 ? d : ND) * row_bytes), nb);
@@ -392,8 +422,21 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
           for (int k = 0; k < K; ++k) load_w(d - PF, k, rb[s][k], rl[s][k]);
           __builtin_amdgcn_sched_barrier(0);  // the prefetch stays PF steps ahead of its use
         }
+        if (VAR != 0 && wv == 0) {  // lane s: beta(d, 0) of step s, if 1 <= d <= T-1
+          const int dl = d0 - lane;
+          const double x = s_sum[min(lane, PF - 1)];
+          acc_lane = log_add2(acc_lane, (lane < PF && dl >= 1 && dl <= T - 1) ? x : kNoArc);
+        }
       }
       if (NW > 1) __syncthreads();  // the segment's values reach the previous wave
+    }
+    if (VAR != 0 && wv == 0) {
+      const double acc0 = wave_log_sum(acc_lane);  // log-sum of beta(t, 0), t >= 1
+      if (lane == 0) {
+        b00 = log_add2(b00, acc0);  // (0,0)->(t,0)
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");  // after the step's store of row 0
+        b_utt[0] = b00;
+      }
     }
     if (wv == 0 && lane == 0) p.lnp2_bwd[b] = b00;
   }
