@@ -267,7 +267,7 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
       for (int k = 0; k < K; ++k) load_w(s, k, rb[s][k], rl[s][k]);
       __builtin_amdgcn_sched_barrier(0);  // issue order = use order (oldest first)
     }
-    double x_in[PF];  // the fill of lane 0 in each step of a segment (several waves)
+    double x_in[PF];  // lane 0: the fill of each step of a segment (several waves)
 #pragma unroll
     for (int s = 0; s < PF; ++s) x_in[s] = kNoArc;
 
@@ -302,14 +302,16 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
             el[k] = a[k] + wl;
           }
           if (NW > 1) x_out[s] = el[K - 1];  // lane 63's for wave wv+1
-          // lane 0 of a later wave takes the unit below it from the wave before, one segment old
-          double fill = (NW > 1) ? x_in[s] : left_carry;
-          // unit 0 has no unit below; in the W-Transducer its second term is the skip arc
-          // (0,0)->(d,0) of weight 0 from alpha(0,0) = 0, so no second log-add follows on
-          // the chain (log_add2(x, kNoArc) is exactly x)
+          // lane 0 of a later wave takes the unit below it from the wave before, one segment
+          // old.  The shift writes over its own fill register, whose lane 0 keeps the fill
+          // (the only lane of it ever read), so no copy of the fill precedes it.  Unit 0 has
+          // no unit below; in the W-Transducer its second term is the skip arc (0,0)->(d,0)
+          // of weight 0 from alpha(0,0) = 0, so no second log-add follows on the chain
+          // (log_add2(x, kNoArc) is exactly x)
+          double& fill = (NW > 1) ? x_in[s] : left_carry;
           if (VAR != 0 && wv == 0) fill = (d <= T - 1) ? 0.0 : kNoArc;
-          left_carry = wave_shift_up(el[K - 1], fill);
-          const double left = left_carry;
+          fill = wave_shift_up(el[K - 1], fill);
+          const double left = fill;
 #pragma unroll
           for (int k = 0; k < K; ++k) a[k] = log_add2(eb[k], k == 0 ? left : el[k > 0 ? k - 1 : 0]);
           // wave-uniform conditions on the diagonal; no memory access inside
@@ -371,7 +373,7 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
       for (int k = 0; k < K; ++k) load_w(D - 1 - s, k, rb[s][k], rl[s][k]);
       __builtin_amdgcn_sched_barrier(0);  // issue order = use order (oldest first)
     }
-    double x_in[PF];  // the fill of lane 63 in each step of a segment (several waves)
+    double x_in[PF];  // lane 63: the fill of each step of a segment (several waves)
 #pragma unroll
     for (int s = 0; s < PF; ++s) x_in[s] = kNoArc;
 
@@ -389,10 +391,11 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
         for (int s = 0; s < PF; ++s) {
           const int d = d0 - s;  // slot s holds the weights of diagonal d (d < 0: no node)
           if (NW > 1) x_out[s] = bv[0];  // lane 0's for wave wv-1
-          // lane 63 of an earlier wave takes the unit above it from the wave after, one segment old
-          const double fill = (NW > 1) ? x_in[s] : right_carry;
-          right_carry = wave_shift_down(bv[0], fill);
-          const double right = right_carry;
+          // lane 63 of an earlier wave takes the unit above it from the wave after, one segment
+          // old (in place, as in the forward sweep)
+          double& fill = (NW > 1) ? x_in[s] : right_carry;
+          fill = wave_shift_down(bv[0], fill);
+          const double right = fill;
           // W-Transducer: node (d-U, U), t <= T-2, has a skip arc of weight 0 to (T-1, U)
           // (force-final) or to the final node (allow-ignore); it takes the place of the
           // label arc that unit U lacks, so no second log-add follows on the chain

@@ -132,7 +132,7 @@ __global__ __launch_bounds__(64 * NW) void k2_viterbi(ViterbiParams p) {
     __builtin_amdgcn_sched_barrier(0);  // issue order = use order (oldest first)
   }
 
-  double x_in[PF];  // the fill of lane 0 in each step of a segment (several waves; kNoArc for wave 0)
+  double x_in[PF];  // lane 0: the fill of each step of a segment (several waves; kNoArc for wave 0)
 #pragma unroll
   for (int s = 0; s < PF; ++s) x_in[s] = kNoArc;
   const int n_seg = (D + PF - 1) / PF;
@@ -157,8 +157,9 @@ __global__ __launch_bounds__(64 * NW) void k2_viterbi(ViterbiParams p) {
         el[k] = a[k] + rl[s][k];
       }
       if (NW > 1) x_out[s] = el[K - 1];  // lane 63's for wave wv+1
-      left_carry = wave_shift_up(el[K - 1], NW > 1 ? x_in[s] : left_carry);
-      const double left = left_carry;
+      double& fill = (NW > 1) ? x_in[s] : left_carry;  // in place: lane 0 keeps the fill
+      fill = wave_shift_up(el[K - 1], fill);
+      const double left = fill;
       bool dec[K];
 #pragma unroll
       for (int k = 0; k < K; ++k) {
