@@ -248,8 +248,8 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
 #pragma unroll
     for (int k = 0; k < K; ++k) a[k] = (ub + lane * K + k == 0) ? 0.0 : kNoArc;
     double a_top = (U == 0) ? 0.0 : kNoArc;    // alpha(T-1, U) once the sweep reaches D
-    // the shifted-in neighbour; lane 0 of wave 0 gets none from the shift and keeps
-    // kNoArc from here on, so no fill value is set up in each step
+    // the shifted-in neighbour; in RNN-T lane 0 of wave 0 gets none from the shift and
+    // keeps kNoArc from here on, so no fill value is set up in each step
     double left_carry = kNoArc;
     // W-Transducer: log-sum of alpha(t, U), t <= T-2, kept per lane (lane s sums the
     // steps s of every segment) in the wave owning unit U and summed over lanes at the
@@ -278,7 +278,7 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
       if (g >= 0 && g < n_seg) {
         const int d0 = 1 + g * PF;
         // the wave before wrote this segment's values in the previous round: all of them
-        // are read at once, so no step waits on the LDS (wave 0's lane 0 takes kNoArc)
+        // are read at once, so no step waits on the LDS (wave 0 has no wave before it)
         if (NW > 1 && wv > 0) {
 #pragma unroll
           for (int s = 0; s < PF; ++s) x_in[s] = s_xch[max(wv - 1, 0)][(r - 1) & 1][s];
@@ -314,9 +314,8 @@ __global__ __launch_bounds__(64 * NW) void k2_lattice(LatticeParams p) {
           const double left = fill;
 #pragma unroll
           for (int k = 0; k < K; ++k) a[k] = log_add2(eb[k], k == 0 ? left : el[k > 0 ? k - 1 : 0]);
-          // wave-uniform conditions on the diagonal; no memory access inside
-          // once per sweep: a branch, not selects in every step.  The force-final skip arcs
-          // into (T-1, U) are added after the sweep: no later step reads alpha(T-1, U)
+          // once per sweep, wave-uniform: a branch, not selects in every step.  The force-final
+          // skip arcs into (T-1, U) are added after the sweep: no later step reads alpha(T-1, U)
           if (__builtin_expect(d == D, 0)) a_top = at_unit(a, lane, U - ub, a_top);
           if (VAR != 0) sum_out[s] = K == 1 ? a[0] : at_unit(a, lane, U - ub, kNoArc);
           if (MODE != kLossOnly)  // the row offset is uniform; readfirstlane keeps it in a scalar register
