@@ -19,8 +19,8 @@
 // units, two to four wavefronts with one unit per lane do, staggered by a
 // segment of steps and exchanging their boundary values through LDS (see the
 // kernel's NW parameter).  The forward and
-// backward waves of an utterance run concurrently, each a one-wavefront block of
-// its own (blockIdx.y), so that the two chains do not share a compute unit.  The weights of
+// backward sweeps of an utterance run concurrently, each in a block of its own
+// (blockIdx.y), so that the two chains do not share a compute unit.  The weights of
 // the next PF diagonals stay in flight in registers (one load per unit and
 // diagonal).  No node is masked:
 // absent arcs carry kNoArc, so a node outside the utterance accumulates only
@@ -32,9 +32,12 @@
 // beta rows are 64*K wide, one column per lane slot, and the
 // steps past the utterance's last diagonal (or before the first) store into
 // spare rows, so every load and store goes through a wave-uniform row pointer
-// plus a constant lane offset and none sits under a branch.  The wild-card
-// arcs cost two running log-sums held by the lanes owning u = 0 and u = U,
-// updated under wave-uniform conditions on the diagonal.
+// plus a constant lane offset and none sits under a branch.  No wild-card arc
+// lengthens a step's chain: the arc into (t,0) is unit 0's second log-add term
+// (it has no unit below), the arc out of (t,U) takes the place of unit U's
+// absent label arc, and the two log-sums over frames they need (of alpha(t,U)
+// and of beta(t,0)) go through LDS to per-lane sums once per segment; the one
+// cell each changes is stored again after the sweep.
 //
 // Kernel 2b, for every padded row (t, u):
 //   occ_blank(t,u) = 2^(alpha(t,u) + lp_blank(t,u) + beta(t+1,u) - log2 P)   (t < T-1)
