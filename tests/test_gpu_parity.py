@@ -353,6 +353,66 @@ def test_rows_of_underflowed_posteriors_are_exact_zeros(torch, pkg, dtype):
     assert n_far >= 0.1 * 2 * 120 * 41, n_far  # the case exercises the skipped rows
 
 
+def random_case(rng):
+    """Shape, variant, dtypes, blank and logit scale of one seeded random case (up to 2e7 logits)."""
+    B = int(rng.integers(1, 5))
+    T = int(rng.choice([1, 2, 3, int(rng.integers(1, 40)), int(rng.integers(40, 260))]))
+    U = int(rng.choice([0, 1, int(rng.integers(0, 70)), int(rng.integers(60, 260)), int(rng.integers(250, 700))]))
+    V = int(rng.choice([2, 3, int(rng.integers(2, 64)), int(rng.integers(64, 700))]))
+    while B * T * (U + 1) * V > 20_000_000:
+        if U > 0 and rng.random() < 0.5:
+            U //= 2
+        elif T > 1:
+            T = max(1, T // 2)
+        else:
+            V = max(2, V // 2)
+    variant = str(rng.choice(VARIANTS))
+    dtype = str(rng.choice(["f32", "f32", "bf16", "f16"]))
+    gdt = dtype if dtype == "f32" else str(rng.choice([dtype, "f32"]))
+    return dict(B=B, T=T, U=U, V=V, variant=variant, dtype=dtype, gdt=gdt, blank=int(rng.integers(0, V)),
+                sigma=float(rng.choice([1.0, 2.0, 3.0, 4.0])), full=bool(rng.random() < 0.3),
+                seed=int(rng.integers(0, 1 << 30)))
+
+
+@pytest.mark.parametrize("chunk", range(8))
+def test_seeded_random_sweep(torch, pkg, chunk):
+    # 50 seeded random cases per chunk: any blank index, U from 0 to ~700 (one to four
+    # waves, or 6-12 units per lane), T from 1, V from 2, every variant and dtype.
+    # The loss is held to the relative bound against max(1, |L_ref|): a W-Transducer
+    # loss with U = 0 can sit near 0 (P may exceed 1), where each log-add's float32
+    # correction term leaves ~1e-8 of absolute error.  The share of bf16-stored
+    # elements off the correctly rounded value is checked for V >= 32 only: with two
+    # or three classes most elements are cancelling differences p*occ - occ, whose
+    # float32 value need not round like the exact one (each is still within the bound).
+    rng = np.random.default_rng(9100 + chunk)
+    for i in range(50):
+        c = random_case(rng)
+        sys.__stderr__.write("[random-case %d.%d] %s\n" % (chunk, i, c))
+        sys.__stderr__.flush()
+        logits, tl, ul, labels = W.small_case(c["B"], c["T"], c["U"], c["V"], seed=c["seed"], sigma=c["sigma"],
+                                              full=c["full"], blank=c["blank"])
+        loss, grad, seen = run_case(torch, pkg, logits, tl, ul, labels, blank=c["blank"], variant=c["variant"],
+                                    dtype=c["dtype"], grad_dtype=c["gdt"])
+        loss_ref, grad_ref = R.rnnt_loss_grad(seen, labels, tl, ul, c["blank"], c["variant"])
+        good = np.isfinite(loss_ref)
+        assert np.array_equal(np.isnan(loss), ~good), (c, loss, loss_ref)
+        lrel = np.abs(loss[good] - loss_ref[good]) / np.maximum(np.abs(loss_ref[good]), 1.0)
+        assert np.all(lrel <= (1e-5 if c["dtype"] == "f32" else 2e-3)), (c, lrel.max())
+        err = np.abs(grad - grad_ref)
+        assert np.all(err <= grad_bound(grad_ref, c["dtype"], c["gdt"])), (c, float(np.nanmax(err)))
+        if c["gdt"] == "bf16":
+            rn = bf16_round(grad_ref)
+            differ = grad != rn
+            assert np.all(np.abs(grad - rn)[differ] <= 2.0 ** -7 * np.abs(rn[differ]) + 1e-5), c
+            if differ.size >= 10000 and c["V"] >= 32:
+                assert differ.mean() <= 1e-2, (c, differ.mean())
+        for b in range(c["B"]):
+            if not good[b]:
+                assert np.all(grad[b] == 0), c
+                continue
+            assert np.all(grad[b, tl[b]:] == 0) and np.all(grad[b, :, ul[b] + 1:] == 0), c
+
+
 @pytest.mark.parametrize("dtype,V,blank", [("f32", 4100, 17), ("bf16", 8200, 8199), ("f16", 2600, 0)])
 def test_large_vocabulary(torch, pkg, dtype, V, blank):
     # rows longer than the populate kernel's register path (64 lanes x 5 chunks) take its batched path
