@@ -4,7 +4,10 @@ through the C-ABI) against the float64 arc-list oracle (oracle/arc_lattice.py).
 Tolerances as for the grid path, with the loss's relative error taken against
 max(1, |L_ref|): fp32 logits, |L - L_ref| <= 1e-5 max(1, |L_ref|) and every
 gradient element within 1e-5; half-precision logits, 2e-3 max(1, |L_ref|) and
-the gradient bounds of test_gpu_parity.grad_bound.  An utterance whose final state
+the gradient bounds of test_gpu_parity.grad_bound.  The absolute 1e-5 term of a
+gradient bound grows to 1e-5 max(1, S) on a row whose arcs' posteriors sum to S:
+a general lattice may read one row many times over on a path, which a grid never
+does (S <= 1 there, so the grid's bounds are unchanged).  An utterance whose final state
 no path reaches has loss +inf and a zero gradient; one with bad data, loss NaN
 and a zero gradient.  On the lattices of Fig. 1 / Fig. 4 the arc-list path also
 agrees with the grid kernels (rnnt_loss) on the same logits.
@@ -67,9 +70,30 @@ def run_arc(torch, pkg, logits_np, tl, ul, lattices, blank=0, dtype="f32", need_
     return loss.cpu().numpy().astype(np.float64), g, seen
 
 
+def reference(seen, tl, ul, lattices, need_grad):
+    """Oracle losses and gradient of the batch (as AL.batch_loss_grad), plus each row's
+    occupancy: the summed posteriors of the arcs that read it."""
+    B, T_max, U1, V = seen.shape
+    ref_loss = np.full(B, np.nan)
+    ref_grad = np.zeros(seen.shape) if need_grad else None
+    occ = np.zeros(seen.shape[:3])
+    for b, (n, a) in enumerate(lattices):
+        arcs = as_tuples(a)
+        T_b, U_b = int(tl[b]), int(ul[b])
+        if not AL.utterance_is_valid(T_b, U_b, arcs, T_max, U1 - 1, V):
+            continue
+        r = AL.arc_lattice_loss_grad(seen[b, :T_b, :U_b + 1], arcs, n, need_grad)
+        ref_loss[b] = r["loss"]
+        if need_grad:
+            ref_grad[b, :T_b, :U_b + 1] = r["grad"]
+        for g, (_s, _d, t, u, label, _w) in zip(r["posteriors"], arcs):
+            if label >= 0:
+                occ[b, t, u] += g
+    return ref_loss, ref_grad, occ
+
+
 def check(loss, grad, seen, tl, ul, lattices, dtype="f32"):
-    ref_loss, ref_grad = AL.batch_loss_grad(seen, tl, ul, [(n, as_tuples(a)) for n, a in lattices],
-                                            need_grad=grad is not None)
+    ref_loss, ref_grad, occ = reference(seen, tl, ul, lattices, grad is not None)
     assert np.array_equal(np.isnan(loss), np.isnan(ref_loss)), (loss, ref_loss)
     assert np.array_equal(np.isinf(loss), np.isinf(ref_loss)), (loss, ref_loss)
     good = np.isfinite(ref_loss)
@@ -80,7 +104,10 @@ def check(loss, grad, seen, tl, ul, lattices, dtype="f32"):
     assert np.all(rel <= lim), (rel.max(), loss, ref_loss)
     if grad is not None:
         err = np.abs(grad - ref_grad)
-        bad = ~(err <= grad_bound(ref_grad, dtype, dtype))
+        # a row read by arcs of total posterior S has elements p_v S - occ_v, formed in float32:
+        # the absolute term of the bound scales with max(1, S) (S <= 1 on every grid lattice)
+        bound = grad_bound(ref_grad, dtype, dtype) + 1e-5 * (np.maximum(occ, 1.0) - 1.0)[..., None]
+        bad = ~(err <= bound)
         assert not bad.any(), (err.max(), np.argwhere(bad)[:5])
         for b in range(len(tl)):
             assert np.all(grad[b, int(tl[b]):] == 0) and np.all(grad[b, :, int(ul[b]) + 1:] == 0)
@@ -123,6 +150,39 @@ def test_random_lattices(torch, pkg, dtype, seed):
                 for b in range(B)]
     loss, grad, seen = run_arc(torch, pkg, logits, tl, ul, lattices, 0, dtype)
     check(loss, grad, seen, tl, ul, lattices, dtype)
+
+
+@pytest.mark.parametrize("chunk", range(4))
+def test_arc_seeded_random_sweep(torch, pkg, chunk):
+    # 12 seeded random batches per chunk: random padded shape and lengths, random acyclic
+    # lattices (up to ~4000 states, dense or sparse, arcs without logits, long arcs),
+    # any blank index, every logits dtype
+    rng = np.random.default_rng(9500 + chunk)
+    for i in range(12):
+        B = int(rng.integers(1, 5))
+        T_max = int(rng.choice([1, 2, int(rng.integers(1, 20)), int(rng.integers(20, 80))]))
+        U_max = int(rng.choice([0, 1, int(rng.integers(0, 12)), int(rng.integers(12, 50))]))
+        V = int(rng.choice([2, int(rng.integers(2, 40)), int(rng.integers(40, 400))]))
+        blank = int(rng.integers(0, V))
+        dtype = str(rng.choice(["f32", "bf16", "f16"]))
+        tl = rng.integers(1, T_max, endpoint=True, size=B).astype(np.int32)
+        ul = rng.integers(0, U_max, endpoint=True, size=B).astype(np.int32)
+        sizes = [int(rng.choice([2, int(rng.integers(2, 60)), int(rng.integers(60, 800)), int(rng.integers(800, 4000))]))
+                 for _ in range(B)]
+        # within the planner's limits: no more than ~700 arcs reading one row on average
+        # (a row carrying several labels takes at most 1024)
+        sizes = [max(2, min(n, 700 * int(tl[b]) * (int(ul[b]) + 1))) for b, n in enumerate(sizes)]
+        dens = [float(rng.choice([1.0, 2.0, 4.0])) for _ in range(B)]
+        long_frac = float(rng.choice([0.0, 0.05, 0.3]))
+        eps_frac = float(rng.choice([0.0, 0.2, 0.6]))
+        print("[arc-random %d.%d] B=%d T_max=%d U_max=%d V=%d blank=%d %s states=%s density=%s long=%g eps=%g"
+              % (chunk, i, B, T_max, U_max, V, blank, dtype, sizes, dens, long_frac, eps_frac), flush=True)
+        logits = (rng.standard_normal((B, T_max, U_max + 1, V)) * float(rng.choice([1.0, 2.0, 3.0]))).astype(np.float32)
+        arcs = [min(int(dens[b] * sizes[b]), 700 * int(tl[b]) * (int(ul[b]) + 1)) for b in range(B)]
+        lattices = [W.random_arc_lattice(rng, int(tl[b]), int(ul[b]), V, sizes[b], arcs[b], eps_frac=eps_frac,
+                                         long_frac=long_frac) for b in range(B)]
+        loss, grad, seen = run_arc(torch, pkg, logits, tl, ul, lattices, blank, dtype)
+        check(loss, grad, seen, tl, ul, lattices, dtype)
 
 
 def test_long_arcs_and_many_levels(torch, pkg):

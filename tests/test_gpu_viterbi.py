@@ -84,6 +84,39 @@ def test_viterbi_matches_oracle(torch, pkg, dtype, variant, B, T, U, V, blank, s
         assert sum(same) >= B - 1  # random fp32 weights: the oracle's path, bar a rare near-tie
 
 
+@pytest.mark.parametrize("chunk", range(4))
+def test_viterbi_seeded_random_sweep(torch, pkg, chunk):
+    # 40 seeded random cases per chunk: any blank index, T from 1, U from 0 to ~700,
+    # V from 2, every variant, fp32 / bf16 / fp16 logits; each utterance checked as above
+    rng = np.random.default_rng(9300 + chunk)
+    for i in range(40):
+        B = int(rng.integers(1, 5))
+        T = int(rng.choice([1, 2, 3, int(rng.integers(1, 40)), int(rng.integers(40, 260))]))
+        U = int(rng.choice([0, 1, int(rng.integers(0, 70)), int(rng.integers(60, 260)),
+                            int(rng.integers(250, 700))]))
+        V = int(rng.choice([2, 3, int(rng.integers(2, 64)), int(rng.integers(64, 700))]))
+        while B * T * (U + 1) * V > 20_000_000:
+            if U > 0 and rng.random() < 0.5:
+                U //= 2
+            elif T > 1:
+                T = max(1, T // 2)
+            else:
+                V = max(2, V // 2)
+        variant = str(rng.choice(VARIANTS))
+        dtype = str(rng.choice(["f32", "bf16", "f16"]))
+        blank = int(rng.integers(0, V))
+        sigma = float(rng.choice([1.0, 2.0, 3.0]))
+        seed = int(rng.integers(0, 1 << 30))
+        print("[viterbi-random %d.%d] B=%d T=%d U=%d V=%d %s %s blank=%d sigma=%g seed=%d"
+              % (chunk, i, B, T, U, V, variant, dtype, blank, sigma, seed), flush=True)
+        logits, tl, ul, labels = W.small_case(B, T, U, V, seed=seed, sigma=sigma, blank=blank)
+        score, frames, span, seen = run_viterbi(torch, pkg, logits, tl, ul, labels, blank, variant, dtype)
+        rel = 1e-5 if dtype == "f32" else 2e-3
+        for b in range(B):
+            check_utterance(seen[b], labels[b], blank, variant, score[b], frames[b], span[b], int(tl[b]), int(ul[b]),
+                            rel)
+
+
 @pytest.mark.parametrize("variant", VARIANTS)
 @pytest.mark.parametrize("T,U", [(1, 0), (3, 0), (1, 3), (4, 2), (9, 5), (40, 70), (3, 128), (6, 200)])
 def test_viterbi_ties_follow_the_fixed_order(torch, pkg, variant, T, U):
