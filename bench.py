@@ -182,33 +182,35 @@ def cpu_baseline(w, tl, ul, labels, budget_s, mode="loss"):
              mode) for b in range(w.B)]
     ctx = mp.get_context("fork")
     with ctx.Pool(cores) as pool:
-        t0 = time.perf_counter()
-        pool.map(cpu_oracle_worker, jobs[:cores])  # one round, to size the sample
-        t_round = time.perf_counter() - t0
-        # cycle through the batch's utterances until about budget_s of work is queued
-        rounds = max(1, int(budget_s / max(t_round, 1e-3)))
-        sample = [jobs[i % len(jobs)] for i in range(rounds * min(cores, len(jobs)))]
-        log("[bench] cpu oracle: one round of %d utterances took %.1f s; timing %d utterance evaluations"
-            % (min(cores, len(jobs)), t_round, len(sample)))
+        pool.map(cpu_oracle_worker, jobs[:cores])  # warm-up round (worker start-up, first imports)
+        # one pass over the batch sizes the sample: the mean of the evaluations' own times
+        t_eval = sum(pool.map(cpu_oracle_worker, jobs)) / len(jobs)
+        # cycle through the batch's utterances until about budget_s of work per worker is queued
+        n_eval = max(min(cores, len(jobs)), int(budget_s * min(cores, len(jobs)) / max(t_eval, 1e-4)))
+        sample = [jobs[i % len(jobs)] for i in range(n_eval)]
+        log("[bench] cpu oracle: %.3f s per utterance evaluation; timing %d evaluations" % (t_eval, len(sample)))
         t0 = time.perf_counter()
         per_eval = pool.map(cpu_oracle_worker, sample)  # each evaluation's own time, in its worker
-        dt = time.perf_counter() - t0
+        wall = time.perf_counter() - t0
     n = len(sample)
+    used = min(cores, n)
+    busy = sum(per_eval) / used  # oracle time per worker, the logits' drawing excluded
     return {
-        "value": n * per_utt_elems / dt,
+        "value": n * per_utt_elems / busy,
         "unit": "joint-logit elements/s",
-        "cores": min(cores, n),
+        "cores": used,
         "cores_available": available,
         "kind": "oracle",
         "single_core_value": n * per_utt_elems / sum(per_eval),
         "sample": "%d utterance evaluations cycling through the %d utterances of the batch (their lengths and "
                   "labels; logits freshly drawn on the host from N(0,%g), the workload's distribution, not copied "
-                  "from the GPU's tensor), float64 %s, %d worker processes, %.1f s; elements counted as padded "
-                  "rows x V like the GPU value" % (n, w.B, w.sigma,
-                                                   {"viterbi": "forced alignment",
-                                                    "arc": "arc-list loss + gradient (oracle/arc_lattice.py)"}.get(
-                                                       mode, "loss + gradient"),
-                                                   min(cores, n), dt),
+                  "from the GPU's tensor), float64 %s, %d worker processes running at once, %.1f s of oracle "
+                  "time per worker (%.1f s wall, which also draws the logits); elements counted as padded rows x V "
+                  "like the GPU value" % (n, w.B, w.sigma,
+                                          {"viterbi": "forced alignment",
+                                           "arc": "arc-list loss + gradient (oracle/arc_lattice.py)"}.get(
+                                              mode, "loss + gradient"),
+                                          used, busy, wall),
     }
 
 
@@ -402,7 +404,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="bpe", choices=["tiny", "char", "bpe", "wrnnt", "large"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=30.0, help="seconds of oracle work to time")
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work per worker to time")
     ap.add_argument("--mode", default="loss", choices=["loss", "viterbi", "arc"],
                     help="loss: the fused loss + gradient (the headline metric); viterbi: forced alignment; "
                          "arc: the loss + gradient over the workload's lattices given as arc lists")
