@@ -9,6 +9,7 @@ correctly rounded g_ref except next to ties.  g_ref is computed from the same
 half-precision values upcast exactly.  Padding rows must be exactly 0 and NaN
 logits in the padding must not leak.
 """
+import dataclasses
 import os
 import sys
 
@@ -512,9 +513,11 @@ def utterance_bits(torch, lg, b, T_b, U_b):
     return x.view(torch.int16).cpu().numpy().view(np.uint16)
 
 
-def full_size_case(torch, pkg, pool, name, grad_utts, grad_dtype=None, logits_dtype=None):
+def full_size_case(torch, pkg, pool, name, grad_utts, grad_dtype=None, logits_dtype=None, variant=None):
     import oracle_pool as OP
     w = W.WORKLOADS[name]
+    if variant is not None:
+        w = dataclasses.replace(w, variant=variant)  # same seed: the same lengths, labels and logits
     ldt = logits_dtype or w.dtype
     gdt = grad_dtype or ldt
     tl, ul, labels = W.make_lengths_labels(w)
@@ -547,9 +550,9 @@ def full_size_case(torch, pkg, pool, name, grad_utts, grad_dtype=None, logits_dt
                             grad_dtype=gdt)
         gmax = max(gmax, gerr)
         gratio = max(gratio, float(np.max(np.abs(g - gref) / grad_bound(gref, ldt, gdt))))
-    sys.__stderr__.write("[full-size] %s logits %s grad %s: loss max rel err %.2e over %d utterances; grad max abs "
-                         "err %.2e, max err / bound %.3f over utterances %s\n"
-                         % (name, ldt, gdt, lrel, w.B, gmax, gratio, sorted(grad_set)))
+    sys.__stderr__.write("[full-size] %s (%s) logits %s grad %s: loss max rel err %.2e over %d utterances; grad max "
+                         "abs err %.2e, max err / bound %.3f over utterances %s\n"
+                         % (name, w.variant, ldt, gdt, lrel, w.B, gmax, gratio, sorted(grad_set)))
     sys.__stderr__.flush()
     # properties that hold at any size, on every utterance
     for b in range(w.B):
@@ -584,6 +587,11 @@ def test_large_bf16_workload_full_size(torch, pkg, oracle_pool):
 
 def test_large_bf16_workload_float32_gradient(torch, pkg, oracle_pool):
     full_size_case(torch, pkg, oracle_pool, "large", grad_utts=[5, 33, 50], grad_dtype="f32")
+
+
+def test_wrnnt_workload_allow_ignore_full_size(torch, pkg, oracle_pool):
+    # the wrnnt batch's shape, lengths and logits under the allow-ignore arcs (Section 4.3)
+    full_size_case(torch, pkg, oracle_pool, "wrnnt", grad_utts=[0, 14, 27], variant="wrnnt_allow_ignore")
 
 
 def test_large_shape_float16_logits(torch, pkg, oracle_pool):
