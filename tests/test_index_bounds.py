@@ -233,6 +233,38 @@ def test_lattice_multi_wave_schedule(NW, D):
             assert all(rw > r for rw, _ in writes[(pair, half, s)] if rw >= r)
 
 
+@pytest.mark.parametrize("T,U", [(1, 0), (2, 0), (5, 0), (1, 7), (2, 1), (30, 17), (250, 80), (24, 0), (25, 23),
+                                 (500, 150), (3, 255), (40, 300), (7, 700), (3, 1000), (2, 1535), (9, 2047)])
+def test_wildcard_sums_take_each_frame_once(T, U):
+    """W-Transducer sweeps: the owning lane stores the value of step s of a segment in LDS
+    slot s, and after the segment lane s adds it to its own sum when the step's diagonal is
+    in range.  Every frame's term enters exactly once: alpha(t, U) for t <= T-2 (forward;
+    t = 0 from the start when U = 0) and beta(t, 0) for 1 <= t <= T-1 (backward; t = T-1
+    from the start when U = 0), and the stash and sink indices stay inside their arrays."""
+    nw, K = sweep_shape(U + 1)
+    PF = 1 if K >= 24 else 2 if K >= 16 else min(24, 48 // K)
+    D = T - 1 + U
+    n_seg = (D + PF - 1) // PF
+    fwd, bwd = [], []
+    if U == 0 and T >= 2:
+        fwd.append(0)
+        bwd.append(T - 1)
+    for g in range(n_seg):
+        d0f, d0b = 1 + g * PF, D - 1 - g * PF
+        for lane in range(64):
+            for s_ in range(PF):
+                assert 0 <= lane + s_ < 64 + PF  # the sink of the lanes without a value
+            if lane < PF:  # min(lane, PF - 1) is the slot read; lanes >= PF add nothing
+                d = d0f + lane
+                if U <= d <= U + T - 2:
+                    fwd.append(d - U)
+                d = d0b - lane
+                if 1 <= d <= T - 1:
+                    bwd.append(d)
+    assert sorted(fwd) == list(range(0, T - 1))
+    assert sorted(bwd) == list(range(1, T))
+
+
 @pytest.mark.parametrize("B,T,U,V,dt", SHAPES)
 def test_gradient_kernel_fast_path_buffer(B, T, U, V, dt):
     """Blocks on the buffer-load path: no partial chunk inside, a per-block buffer of at
