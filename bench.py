@@ -146,6 +146,22 @@ def gradient_rows(torch, grad, tl, ul):
     return n
 
 
+def gradient_rows_f32(torch, grad, tl, ul, call_f32):
+    """gradient_rows, counted on a float32 gradient: a 16-bit store can round all of a
+    row's tiny but nonzero elements to 0 (fp16's range ends at 6e-8), though the row's
+    logits were read to form them.  call_f32(g32) runs the step once more (untimed)
+    with a float32 gradient into g32."""
+    if grad.dtype == torch.float32:
+        return gradient_rows(torch, grad, tl, ul)
+    g32 = torch.empty(grad.shape, dtype=torch.float32, device=grad.device)
+    call_f32(g32)
+    if g32.is_cuda:
+        torch.cuda.synchronize()
+    n = gradient_rows(torch, g32, tl, ul)
+    del g32
+    return n
+
+
 def cpu_oracle_worker(args):
     import numpy as np
 
@@ -298,7 +314,7 @@ def viterbi_bench(args, w, tl, ul, logits, labels_d, tl_d, ul_d, cpu):
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
             "frac": round(k1_gbs / PEAK_HBM_GBS, 4),
-            "traffic": profiled_traffic(args.workload, "k1_populate"),
+            "traffic": profiled_traffic(args.workload, "k1_populate") if args.traffic_ok else None,
             "bytes_per_launch": ab["k1_populate"],
             "launch_ms": round(k1_ms, 5),
         },
@@ -347,7 +363,9 @@ def arc_bench(args, w, tl, ul, labels, logits, tl_d, ul_d, cpu):
     log("[bench] per step %.4f ms median, %.4f mean (instrumented %.4f, wall %.4f ms): k1 %.4f  populate %.4f  "
         "sweep %.4f  rows %.4f  k3 %.4f ms" % (ms_per_step, ms_mean, ms_inst, wall * 1e3 / args.steps, k1_ms, kp_ms,
                                                ks_ms, kr_ms, k3_ms))
-    ab = algorithmic_bytes(w, tl, ul, logits.element_size(), grad.element_size(), gradient_rows(torch, grad, tl, ul))
+    r_grad = gradient_rows_f32(torch, grad, tl, ul,
+                               lambda g32: binding.arc_loss(logits, tl_d, ul_d, plan, True, ws, g32, loss))
+    ab = algorithmic_bytes(w, tl, ul, logits.element_size(), grad.element_size(), r_grad)
     elems = ab["padded_rows"] * w.V
     k3_gbs = ab["k3_grad"] / (k3_ms * 1e-3) / 1e9
     result = {
@@ -388,7 +406,7 @@ def arc_bench(args, w, tl, ul, labels, logits, tl_d, ul_d, cpu):
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
             "frac": round(k3_gbs / PEAK_HBM_GBS, 4),
-            "traffic": profiled_traffic(args.workload + "_arc", "k3_grad", "arc"),
+            "traffic": profiled_traffic(args.workload + "_arc", "k3_grad", "arc") if args.traffic_ok else None,
             "bytes_per_launch": ab["k3_grad"],
             "launch_ms": round(k3_ms, 5),
         },
@@ -405,6 +423,8 @@ def main():
     ap.add_argument("--workload", default="bpe", choices=["tiny", "char", "bpe", "wrnnt", "large"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work per worker to time")
+    ap.add_argument("--dtype", default=None, choices=["f32", "bf16", "f16"],
+                    help="logits dtype in place of the workload's own (same draws, rounded)")
     ap.add_argument("--mode", default="loss", choices=["loss", "viterbi", "arc"],
                     help="loss: the fused loss + gradient (the headline metric); viterbi: forced alignment; "
                          "arc: the loss + gradient over the workload's lattices given as arc lists")
@@ -412,6 +432,7 @@ def main():
                     help="only run --steps device-to-device copies of the workload's gradient size (the "
                          "known-size copy that calibrates the HBM byte counters), then exit")
     args = ap.parse_args()
+    args.traffic_ok = True  # cleared when --dtype changes the workload's logits dtype
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the library has no multi-GPU path (utterances are "
               "independent, so a batch shards by utterance across processes). Use --gpus 1.",
@@ -425,6 +446,12 @@ def main():
     from paper_2303_10384_amd import workloads as W
 
     w = W.WORKLOADS[args.workload]
+    if args.dtype is not None and args.dtype != w.dtype:
+        # the same shapes, lengths, labels and normal draws, rounded to another logits dtype;
+        # the committed counter records are of the workload's own dtype, so no traffic is reported
+        import dataclasses
+        w = dataclasses.replace(w, dtype=args.dtype)
+        args.traffic_ok = False
     if args.copy_probe:
         copy_probe(torch, w, args.steps)
         return
@@ -478,12 +505,14 @@ def main():
     log("[bench] per step %.4f ms median, %.4f mean (instrumented %.4f, wall %.4f ms): k1 %.4f  k2 %.4f  k2b %.4f  "
         "k3 %.4f ms" % (ms_per_step, ms_mean, ms_inst, wall * 1e3 / args.steps, k1_ms, k2_ms, k2b_ms, k3_ms))
 
-    ab = algorithmic_bytes(w, tl, ul, logits.element_size(), grad.element_size(), gradient_rows(torch, grad, tl, ul))
+    r_grad = gradient_rows_f32(torch, grad, tl, ul, lambda g32: binding.rnnt_loss(
+        logits, labels_d, tl_d, ul_d, 0, w.variant, True, ws, g32, loss))
+    ab = algorithmic_bytes(w, tl, ul, logits.element_size(), grad.element_size(), r_grad)
     r_valid, r_total, V = ab["valid_rows"], ab["padded_rows"], w.V
     elems = r_total * V
     k1_bytes, k3_bytes, step_bytes = ab["k1_populate"], ab["k3_grad"], ab["step"]
     k3_gbs = k3_bytes / (k3_ms * 1e-3) / 1e9
-    traffic = profiled_traffic(args.workload)
+    traffic = profiled_traffic(args.workload) if args.traffic_ok else None
     roofline = {
         "bound": "hbm",
         "kernel": "k3_grad (fused gradient)",

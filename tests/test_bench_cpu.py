@@ -126,3 +126,25 @@ def test_stale_traffic_record_is_ignored(tmp_path, monkeypatch):
     rec["source_digest"] = profiling.source_digest(profiling.KERNEL_SOURCES)
     (tmp_path / "k3_grad_bpe_traffic.json").write_text(json.dumps(rec))
     assert bench.profiled_traffic("bpe") == 123
+
+
+def test_gradient_rows_of_a_16_bit_gradient_are_counted_in_float32():
+    # a row whose tiny elements an fp16 store rounds to 0 still needed its logits read
+    import torch
+    tl, ul = np.array([2, 1], np.int32), np.array([1, 0], np.int32)
+    exact = torch.zeros((2, 2, 2, 3), dtype=torch.float32)
+    exact[0, 0, 0, 1] = 1e-9   # below fp16's smallest subnormal
+    exact[0, 1, 1, 2] = 0.25
+    exact[1, 0, 0, 0] = -3e-9
+    exact[1, 1, 1, 0] = 1.0    # padding row: not counted
+    g16 = exact.to(torch.float16)
+    assert bench.gradient_rows(torch, g16, tl, ul) == 1
+    calls = []
+
+    def call_f32(g32):
+        calls.append(g32.dtype)
+        g32.copy_(exact)
+
+    assert bench.gradient_rows_f32(torch, g16, tl, ul, call_f32) == 3
+    assert calls == [torch.float32]
+    assert bench.gradient_rows_f32(torch, exact, tl, ul, call_f32) == 3 and len(calls) == 1
